@@ -1,0 +1,128 @@
+/*
+ * gdn.h -- C ABI of the MI355X (gfx950) gated delta-rule library (libgdn.so).
+ *
+ * The operation (paper, section 2.2 "The model"; section 3.2 "A chunked
+ * delta-rule scan for the recurrent layers"): every recurrent layer keeps one
+ * state matrix per head, updated token by token.  With the state stored as
+ * S in R^{dv x dk}, a scalar log-decay g_t per (token, head), alpha_t = exp(g_t),
+ * and a write strength beta_t,
+ *
+ *     S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *     o_t = S_t (scale q_t)                     (read after the update)
+ *
+ * gdn_chunk_prefill evaluates this over a whole prompt in the chunked
+ * intra-/inter-chunk form of section 3.2 (chunks of `chunk` tokens: token-token
+ * products, a forward-substituted unit-lower-triangular system, correction and
+ * output products, and a short recurrence across chunks).  gdn_decode_step is
+ * one token of the same recurrence for a batch of sequences.
+ *
+ * Conventions shared by every entry point
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
+ *    keeps no reference after the call returns and allocates no device memory.
+ *  - All tensors are contiguous, row-major, and 16-byte aligned.
+ *  - `io_dtype` selects the element type of q, k, v and o: GDN_F32 (float) or
+ *    GDN_BF16 (bfloat16).  g, beta and the state are always fp32.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *    asynchronously; a kernel fault surfaces at the caller's next
+ *    synchronisation, not in the returned status.
+ *  - Errors are returned, never raised; nothing aborts.  Every argument check
+ *    runs before the first HIP call, so an invalid call touches no device state.
+ *    gdn_last_error_message() gives a thread-local description of the last
+ *    failure on the calling thread.
+ *  - Inputs and outputs must not overlap, except S0 == S_T (in place).
+ */
+#ifndef GDN_H
+#define GDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gdn_status {
+    GDN_OK = 0,
+    GDN_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or dtype      */
+    GDN_ERR_UNSUPPORTED = 2,   /* valid but not implemented (dk, dv, chunk)       */
+    GDN_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required      */
+    GDN_ERR_HIP = 4            /* a HIP launch/runtime call failed                */
+} gdn_status;
+
+typedef enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
+
+/* Library version, (major << 16) | minor. */
+int gdn_version(void);
+
+/* Static text for a status code ("GDN_OK", ...); "unknown status" otherwise. */
+const char* gdn_status_string(int status);
+
+/* Thread-local description of the last non-OK status on this thread ("" if none). */
+const char* gdn_last_error_message(void);
+
+/*
+ * Workspace (device scratch, bytes) that gdn_chunk_prefill needs for these
+ * sizes: the per-chunk state-independent terms of section 3.2 (decay prefix
+ * sums, the inverse of the triangular system, the masked query-key product)
+ * and, for ragged input, the sanitised sequence table.  Same argument meaning
+ * as gdn_chunk_prefill (`n_seqs` = 0 for dense input).  Returns 0 for
+ * arguments gdn_chunk_prefill would reject.  Pure host arithmetic.
+ */
+size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk, int dv, int chunk,
+                                         int n_seqs, int io_dtype);
+
+/*
+ * Chunked prefill (section 3.2).
+ *
+ * Dense input (cu_seqlens == NULL, n_seqs == 0): B independent sequences of T
+ * tokens.  Ragged input (cu_seqlens != NULL): B must be 1 and the T tokens are
+ * n_seqs packed sequences; cu_seqlens is a DEVICE int32 array [n_seqs + 1] with
+ * cu[0] = 0, cu[i] <= cu[i+1], cu[n_seqs] = T.  Chunks restart at every
+ * sequence start; a sequence of length 0 returns S_T = S0.  The contents of
+ * cu_seqlens are not checked on the host; offsets outside that contract are
+ * clamped on the device into a nondecreasing partition of [0, T] (no
+ * out-of-bounds access), which is then what gets computed.
+ *
+ *   q, k     [B, T, H, dk]  io_dtype        keys are used as given (no renormalisation)
+ *   v        [B, T, H, dv]  io_dtype
+ *   g, beta  [B, T, H]      fp32            log-decay (alpha = exp g) and write strength
+ *   S0       [n, H, dv, dk] fp32 or NULL    initial state (NULL = zeros); n = B or n_seqs
+ *   o        [B, T, H, dv]  io_dtype        output (written)
+ *   S_T      [n, H, dv, dk] fp32 or NULL    final state (written unless NULL; may == S0)
+ *   dk, dv   64 or 128;  chunk must be 64;  T >= 0;  B, H >= 1
+ *   scale    multiplies q (o_t = S_t (scale q_t)); 1.0f gives the plain rule
+ *   workspace / workspace_bytes   device scratch of at least
+ *            gdn_chunk_prefill_workspace_bytes(...) bytes, 256-byte aligned; its
+ *            contents on entry are ignored and on exit are unspecified.
+ */
+gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
+                             const float* g, const float* beta, const float* S0,
+                             void* o, float* S_T,
+                             int B, int T, int H, int dk, int dv, int chunk,
+                             const int32_t* cu_seqlens, int n_seqs,
+                             int io_dtype, float scale,
+                             void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * One decode step (the recurrence at T = 1; section 2.2, section 3.2): one
+ * token for each of B sequences.
+ *
+ *   q, k     [B, H, dk]        io_dtype
+ *   v        [B, H, dv]        io_dtype
+ *   g, beta  [B, H]            fp32
+ *   S        [B, H, dv, dk]    fp32, read and updated IN PLACE
+ *   o        [B, H, dv]        io_dtype, o = S_new (scale q)
+ *   dk, dv   64 or 128;  B, H >= 1
+ * Needs no workspace.
+ */
+gdn_status gdn_decode_step(const void* q, const void* k, const void* v,
+                           const float* g, const float* beta, float* S, void* o,
+                           int B, int H, int dk, int dv, int io_dtype, float scale,
+                           void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_H */

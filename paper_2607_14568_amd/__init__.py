@@ -1,0 +1,162 @@
+"""Gated delta-rule prefill and decode on MI355X (gfx950).
+
+A thin ctypes binding over ``libgdn.so`` (C ABI in ``include/gdn.h``).  The
+functions carry the C names and only marshal arguments: every step of the
+computation runs in the library's HIP kernels.  PyTorch supplies device memory
+and the current stream.  There is no CPU fallback: if the library is not built
+or no GPU is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
+    "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgdn.so")
+
+GDN_F32, GDN_BF16 = 0, 1
+_IO = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
+_lib = None
+
+
+class GdnError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__("%s: %s" % (gdn_status_string(status), message))
+        self.status = status
+
+
+def lib():
+    """The loaded ``libgdn.so`` (ctypes.CDLL) with argument types declared."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libgdn.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, F, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        L.gdn_version.restype = I
+        L.gdn_status_string.argtypes = [I]
+        L.gdn_status_string.restype = ctypes.c_char_p
+        L.gdn_last_error_message.restype = ctypes.c_char_p
+        L.gdn_chunk_prefill_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
+        L.gdn_chunk_prefill_workspace_bytes.restype = S
+        L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
+        L.gdn_chunk_prefill.restype = I
+        L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
+        L.gdn_decode_step.restype = I
+        _lib = L
+    return _lib
+
+
+def gdn_version() -> int:
+    return int(lib().gdn_version())
+
+
+def gdn_status_string(status: int) -> str:
+    return lib().gdn_status_string(int(status)).decode()
+
+
+def _check(status):
+    if status != 0:
+        raise GdnError(status, lib().gdn_last_error_message().decode())
+
+
+def gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk=64, n_seqs=0, io_dtype=GDN_BF16) -> int:
+    return int(lib().gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io_dtype))
+
+
+def _dev(t, name, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, scale=1.0,
+                      o=None, S_T=None, store_state=True, workspace=None):
+    """Chunked prefill; see ``gdn_chunk_prefill`` in include/gdn.h.
+
+    q,k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype); g, beta [B,T,H]
+    fp32; S0 [n,H,dv,dk] fp32 or None.  Ragged: B == 1 and ``cu_seqlens`` an
+    int32 CUDA tensor [n+1].  Returns ``(o, S_T)`` (S_T is None when
+    ``store_state`` is False).  ``S_T`` may be passed (also ``S_T is S0``).
+    """
+    if q.dtype not in _IO:
+        raise TypeError("q must be float32 or bfloat16")
+    io = _IO[q.dtype]
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, q.dtype)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if k.shape != q.shape or tuple(v.shape[:3]) != (B, T, H) or tuple(g.shape) != (B, T, H) \
+            or beta.shape != g.shape:
+        raise ValueError("inconsistent shapes q%s k%s v%s g%s beta%s" % (
+            tuple(q.shape), tuple(k.shape), tuple(v.shape), tuple(g.shape), tuple(beta.shape)))
+    n_seqs = 0
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        n_seqs = cu_seqlens.numel() - 1
+    n = n_seqs if n_seqs else B
+    if S0 is not None:
+        _dev(S0, "S0", torch.float32)
+        if tuple(S0.shape) != (n, H, dv, dk):
+            raise ValueError("S0 must be [%d,%d,%d,%d]" % (n, H, dv, dk))
+    if o is None:
+        o = torch.empty_like(v)
+    else:
+        _dev(o, "o", q.dtype)
+    if store_state and S_T is None:
+        S_T = torch.empty((n, H, dv, dk), device=q.device, dtype=torch.float32)
+    elif S_T is not None:
+        _dev(S_T, "S_T", torch.float32)
+    need = gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
+    _check(lib().gdn_chunk_prefill(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(o), _ptr(S_T),
+        B, T, H, dk, dv, chunk, _ptr(cu_seqlens), n_seqs, io, float(scale),
+        _ptr(workspace), workspace.numel(), _stream(q.device)))
+    return o, S_T
+
+
+def gdn_decode_step(q, k, v, g, beta, S, *, scale=1.0, o=None):
+    """One decode step; ``S`` [B,H,dv,dk] fp32 is updated in place.  Returns o [B,H,dv]."""
+    if q.dtype not in _IO:
+        raise TypeError("q must be float32 or bfloat16")
+    io = _IO[q.dtype]
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, q.dtype)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    _dev(S, "S", torch.float32)
+    B, H, dk = q.shape
+    dv = v.shape[-1]
+    if k.shape != q.shape or tuple(v.shape[:2]) != (B, H) or tuple(g.shape) != (B, H) \
+            or beta.shape != g.shape or tuple(S.shape) != (B, H, dv, dk):
+        raise ValueError("inconsistent decode shapes")
+    if o is None:
+        o = torch.empty_like(v)
+    else:
+        _dev(o, "o", q.dtype)
+    _check(lib().gdn_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
+                                 B, H, dk, dv, io, float(scale), _stream(q.device)))
+    return o

@@ -1,0 +1,148 @@
+"""C-ABI checks that need no GPU: symbols, status strings, workspace sizes and
+every argument check (they all run before the first HIP call, so only invalid
+calls are made here -- a valid call would launch kernels)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_14568_amd as gdn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdn.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE, HIPERR = 0, 1, 2, 3, 4
+A = 1 << 20          # a fake, 256-byte aligned "device address" (never dereferenced)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(gdn.LIB_PATH):
+        from paper_2607_14568_amd import build
+        build.build_library(force=True)
+    return gdn.lib()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gdn_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared_functions()
+    assert {"gdn_chunk_prefill", "gdn_decode_step", "gdn_chunk_prefill_workspace_bytes"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_version_and_status_strings(L):
+    assert gdn.gdn_version() >= 1
+    assert gdn.gdn_status_string(0) == "GDN_OK"
+    assert gdn.gdn_status_string(3) == "GDN_ERR_WORKSPACE"
+    assert gdn.gdn_status_string(99) == "unknown status"
+
+
+def test_workspace_bytes():
+    ws = gdn.gdn_chunk_prefill_workspace_bytes
+    a = ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_BF16)
+    slots = 160 * 16
+    assert a >= slots * (64 * 4 + 2 * 64 * 64 * 2)
+    assert a % 256 == 0
+    assert ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_F32) > a
+    assert ws(1, 10241, 16, 128, 128, 64, 0, gdn.GDN_BF16) > a       # a partial chunk adds a slot
+    assert ws(1, 20000, 16, 128, 128, 64, 8, gdn.GDN_BF16) > ws(1, 20000, 16, 128, 128, 64, 0, gdn.GDN_BF16)
+    assert ws(1, 0, 16, 128, 128, 64, 0, gdn.GDN_BF16) == 0
+    for bad in [(0, 10, 1, 64, 64, 64, 0, 0), (1, 10, 1, 96, 64, 64, 0, 0), (1, 10, 1, 64, 64, 32, 0, 0),
+                (2, 10, 1, 64, 64, 64, 3, 0), (1, 10, 1, 64, 64, 64, 0, 7), (1, -1, 1, 64, 64, 64, 0, 0)]:
+        assert ws(*bad) == 0, bad
+
+
+def _prefill(L, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=2, dk=64, dv=64, chunk=64,
+             cu=None, n_seqs=0, io=0, scale=1.0, ws=A, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return L.gdn_chunk_prefill(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S0"], a["o"], a["ST"],
+                               a["B"], a["T"], a["H"], a["dk"], a["dv"], a["chunk"], a["cu"], a["n_seqs"],
+                               a["io"], a["scale"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(io=2), INVALID),
+    (dict(io=-1), INVALID),
+    (dict(B=0), INVALID),
+    (dict(H=0), INVALID),
+    (dict(T=-5), INVALID),
+    (dict(dk=0), INVALID),
+    (dict(dk=96), UNSUPPORTED),
+    (dict(dv=256), UNSUPPORTED),
+    (dict(dk=32, dv=32), UNSUPPORTED),
+    (dict(chunk=0), INVALID),
+    (dict(chunk=32), UNSUPPORTED),
+    (dict(chunk=128), UNSUPPORTED),
+    (dict(q=None), INVALID),
+    (dict(k=None), INVALID),
+    (dict(v=None), INVALID),
+    (dict(g=None), INVALID),
+    (dict(beta=None), INVALID),
+    (dict(o=None), INVALID),
+    (dict(q=A + 8), INVALID),
+    (dict(S0=A + 4), INVALID),
+    (dict(ST=A + 2), INVALID),
+    (dict(cu=A), INVALID),                       # cu_seqlens without n_seqs
+    (dict(n_seqs=3), INVALID),                   # n_seqs without cu_seqlens
+    (dict(cu=A, n_seqs=2, B=2), INVALID),        # ragged needs B == 1
+    (dict(cu=A + 2, n_seqs=2), INVALID),         # misaligned offsets
+    (dict(n_seqs=-1, cu=A), INVALID),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=1000), WORKSPACE),
+    (dict(ws=A + 16), INVALID),                  # workspace not 256-byte aligned
+])
+def test_prefill_argument_checks(L, kw, code):
+    rc = _prefill(L, **kw)
+    assert rc == code, (kw, rc, L.gdn_last_error_message())
+    assert L.gdn_last_error_message().decode()
+
+
+def test_prefill_workspace_exact_boundary(L):
+    need = gdn.gdn_chunk_prefill_workspace_bytes(1, 128, 2, 64, 64, 64, 0, 0)
+    assert _prefill(L, ws_bytes=need - 1) == WORKSPACE
+
+
+def _decode(L, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
+    a.update(kw)
+    return L.gdn_decode_step(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S"], a["o"], a["B"], a["H"],
+                             a["dk"], a["dv"], a["io"], a["scale"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(io=3), INVALID), (dict(B=0), INVALID), (dict(H=-1), INVALID),
+    (dict(dk=100), UNSUPPORTED), (dict(dv=32), UNSUPPORTED), (dict(dk=0), INVALID),
+    (dict(q=None), INVALID), (dict(S=None), INVALID), (dict(o=None), INVALID),
+    (dict(g=None), INVALID), (dict(v=A + 4), INVALID), (dict(S=A + 8), INVALID),
+])
+def test_decode_argument_checks(L, kw, code):
+    assert _decode(L, **kw) == code
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 4, 1, 64)
+    g = torch.zeros(1, 4, 1)
+    with pytest.raises(TypeError):
+        gdn.gdn_chunk_prefill(x, x, x, g, g)
+    with pytest.raises(TypeError):
+        gdn.gdn_decode_step(x[0], x[0], x[0], g[0], g[0], torch.zeros(1, 4, 64, 64))
+
+
+def test_product_package_does_not_reach_the_oracle():
+    """The HIP path never imports or calls the oracle (no CPU fallback)."""
+    pkg = os.path.join(ROOT, "paper_2607_14568_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".h")) and fn != "inputs.py":
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in text, fn
+    assert "import oracle" not in open(os.path.join(pkg, "inputs.py")).read()
