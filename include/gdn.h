@@ -19,7 +19,10 @@
  * Conventions shared by every entry point
  *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
  *    keeps no reference after the call returns and allocates no device memory.
- *  - All tensors are contiguous, row-major, and 16-byte aligned.
+ *  - All tensors are contiguous and row-major.  Alignment: the prefill's q, k,
+ *    v, o, S0, S_T and the decode state S start on 16-byte boundaries; every
+ *    other pointer (g, beta, cu_seqlens, the decode step's q, k, v, o) only
+ *    needs the alignment of its element type.
  *  - `io_dtype` selects the element type of q, k, v and o: GDN_F32 (float) or
  *    GDN_BF16 (bfloat16).  g, beta and the state are always fp32.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued

@@ -12,7 +12,10 @@
 //     U  = T diag(beta) (V - diag(gamma) K S0^T)            per-chunk correction
 //     O  = scale (diag(gamma) Q S0^T + P U)                 chunk output
 //     S  = gamma_n S0 + U^T D K                             inter-chunk recurrence
-// T, P and G depend only on the chunk's own inputs, so they are formed for all
+// The prefix sums G are formed in fp64: with very negative g (alpha underflowing)
+// |G| grows far beyond the range where fp32 differences G_r - G_i keep their
+// precision, while every exp() taken of them stays meaningful.
+// T, P and the decay vectors depend only on the chunk's own inputs, so they are formed for all
 // (chunk, head) pairs at once by k_chunk_terms; k_state_chain then walks the
 // chunks of each (sequence, head, 16-row slice of the state) in order, with all
 // contractions on MFMA (bf16 operands with fp32 accumulation for bf16 io, fp32
@@ -109,7 +112,7 @@ struct Params {
     int32_t* seq_start;
     int32_t* seq_len;
     int32_t* chunk_off;  // [n_seq + 1], first chunk slot of each sequence
-    float* wsG;          // [slot][H][64]
+    float* wsG;          // [slot][H][128]: gamma_r = exp(G_r), then exp(G_n - G_r)
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
     float scale;
@@ -193,7 +196,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __shared__ __attribute__((aligned(16))) float sA[CH][CH + 4];
     __shared__ __attribute__((aligned(16))) float sTi[CH][CH + 4];
     __shared__ float sZ[4][16][17];
-    __shared__ float sG[CH], sB[CH];
+    __shared__ double sG[CH];
+    __shared__ float sB[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -207,15 +211,17 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
             gv = p.g[(t0 + lane) * H + h];
             bv = p.beta[(t0 + lane) * H + h];
         }
-        float x = gv;   // inclusive prefix sum over the chunk
+        double x = gv;   // inclusive prefix sum over the chunk, fp64
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
-            const float y = __shfl_up(x, off, 64);
+            const double y = __shfl_up(x, off, 64);
             if (lane >= off) x += y;
         }
+        const double xn = __shfl(x, 63, 64);   // G_n (padded rows add nothing)
         sG[lane] = x;
         sB[lane] = bv;
-        p.wsG[slot * CH + lane] = x;
+        p.wsG[slot * 2 * CH + lane] = expf((float)x);
+        p.wsG[slot * 2 * CH + CH + lane] = expf((float)(xn - x));
     }
     stage_rows<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), t0, n, H, h);
     stage_rows<IO, DK, DK + PAD>(sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
@@ -244,9 +250,9 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         for (int e = 0; e < 4; ++e) {
             const int r = bi * 16 + 4 * lg + e, i = bj * 16 + l16;
             if (which == 0) {
-                sA[r][i] = (r > i) ? sB[r] * expf(sG[r] - sG[i]) * acc[e] : 0.f;
+                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * acc[e] : 0.f;
             } else {
-                Pg[r * CH + i] = from_f<IO>((r >= i) ? expf(sG[r] - sG[i]) * acc[e] : 0.f);
+                Pg[r * CH + i] = from_f<IO>((r >= i) ? expf((float)(sG[r] - sG[i])) * acc[e] : 0.f);
             }
         }
     }
@@ -323,7 +329,7 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
     __shared__ __attribute__((aligned(16))) IO sT[CH][CH + PAD];
     __shared__ __attribute__((aligned(16))) IO sP[CH][CH + PAD];
     __shared__ float sV[CH][SL + 1], sR[CH][SL + 1], sU[CH][SL + 1];
-    __shared__ float sG[CH], sBeta[CH];
+    __shared__ float sGam[CH], sDec[CH], sBeta[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -357,7 +363,8 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
             sV[r][j] = (r < n) ? to_f(gv[((t0 + r) * H + h) * (long)DV + js * SL + j]) : 0.f;
         }
         if (tid < CH) {
-            sG[tid] = p.wsG[slot * CH + tid];
+            sGam[tid] = p.wsG[slot * 2 * CH + tid];
+            sDec[tid] = p.wsG[slot * 2 * CH + CH + tid];
             sBeta[tid] = (tid < n) ? p.beta[(t0 + tid) * H + h] : 0.f;
         }
         __syncthreads();
@@ -375,7 +382,7 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int r = wave * 16 + 4 * lg + e;
-            sR[r][l16] = sBeta[r] * (sV[r][l16] - expf(sG[r]) * x[e]);
+            sR[r][l16] = sBeta[r] * (sV[r][l16] - sGam[r] * x[e]);
         }
         __syncthreads();
 
@@ -413,12 +420,11 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
             const int r = wave * 16 + 4 * lg + e;
             if (r < n)
                 go[((t0 + r) * H + h) * (long)DV + js * SL + l16] =
-                    from_f<IO>(p.scale * (expf(sG[r]) * oq[e] + op[e]));
+                    from_f<IO>(p.scale * (sGam[r] * oq[e] + op[e]));
         }
 
         // S^T <- gamma_n S^T + K^T D U   (tiles of 16 key channels)
-        const float Gn = sG[CH - 1];
-        const float gn = expf(Gn);
+        const float gn = sGam[CH - 1];
         floatx4 acc[(NMT + 3) / 4];
 #pragma unroll
         for (int m = 0; m < (NMT + 3) / 4; ++m) {
@@ -434,7 +440,7 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
                     for (int e = 0; e < M::KL; ++e) {
                         const int r = kk * M::KS + lg * M::KL + e;
                         ka[e] = to_f(sK[r][mt * 16 + l16]);
-                        ub[e] = expf(Gn - sG[r]) * sU[r][l16];
+                        ub[e] = sDec[r] * sU[r][l16];
                     }
                     acc[m] = M::mma(M::pack(ka), M::pack(ub), acc[m]);
                 }
@@ -526,7 +532,7 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     const size_t per = (size_t)L->slots * H;
     L->meta = 0;
     L->G = n_seqs > 0 ? round_up((size_t)3 * (n_seqs + 1) * sizeof(int32_t), 256) : 0;
-    L->T = L->G + round_up(per * CH * sizeof(float), 256);
+    L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
     L->P = L->T + round_up(per * CH * CH * esz, 256);
     L->total = L->P + round_up(per * CH * CH * esz, 256);
     return true;
@@ -607,10 +613,12 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     if (n_seqs > 0 && B != 1) return fail(GDN_ERR_INVALID_ARG, "ragged input needs B == 1 (got %d)", B);
     if (T > 0 && (!q || !k || !v || !g || !beta || !o))
         return fail(GDN_ERR_INVALID_ARG, "q, k, v, g, beta and o must be non-null");
-    const void* ptrs[] = {q, k, v, g, beta, S0, o, S_T};
-    for (const void* ptr : ptrs)
+    const void* vec_ptrs[] = {q, k, v, o, S0, S_T};   // read/written with 16-byte vectors
+    for (const void* ptr : vec_ptrs)
         if (ptr && !aligned(ptr, 16)) return fail(GDN_ERR_INVALID_ARG, "tensor pointer %p is not 16-byte aligned", ptr);
-    if (cu_seqlens && !aligned(cu_seqlens, 4)) return fail(GDN_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
+    const void* scalar_ptrs[] = {g, beta, cu_seqlens};
+    for (const void* ptr : scalar_ptrs)
+        if (ptr && !aligned(ptr, 4)) return fail(GDN_ERR_INVALID_ARG, "pointer %p is not 4-byte aligned", ptr);
     const int n_seq = n_seqs > 0 ? n_seqs : B;
     if ((long)n_seq * H * (dv / SL) > (1L << 30)) return fail(GDN_ERR_UNSUPPORTED, "too many sequences x heads");
     if ((long)B * T * H > (1L << 40)) return fail(GDN_ERR_UNSUPPORTED, "B*T*H too large");
@@ -664,9 +672,12 @@ extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* 
     if (st != GDN_OK) return st;
     if (!q || !k || !v || !g || !beta || !S || !o)
         return fail(GDN_ERR_INVALID_ARG, "q, k, v, g, beta, S and o must be non-null");
-    const void* ptrs[] = {q, k, v, g, beta, S, o};
-    for (const void* ptr : ptrs)
-        if (!aligned(ptr, 16)) return fail(GDN_ERR_INVALID_ARG, "tensor pointer %p is not 16-byte aligned", ptr);
+    if (!aligned(S, 16)) return fail(GDN_ERR_INVALID_ARG, "state pointer %p is not 16-byte aligned", (const void*)S);
+    const size_t esz = io_dtype == GDN_BF16 ? 2 : 4;
+    const void* io_ptrs[] = {q, k, v, o};
+    for (const void* ptr : io_ptrs)
+        if (!aligned(ptr, esz)) return fail(GDN_ERR_INVALID_ARG, "pointer %p is not element-aligned", ptr);
+    if (!aligned(g, 4) || !aligned(beta, 4)) return fail(GDN_ERR_INVALID_ARG, "g/beta are not 4-byte aligned");
     if ((long)B * H > 65535L * 1024) return fail(GDN_ERR_UNSUPPORTED, "B*H=%ld too large", (long)B * H);
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();

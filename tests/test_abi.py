@@ -48,7 +48,7 @@ def test_workspace_bytes():
     ws = gdn.gdn_chunk_prefill_workspace_bytes
     a = ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_BF16)
     slots = 160 * 16
-    assert a >= slots * (64 * 4 + 2 * 64 * 64 * 2)
+    assert a >= slots * (128 * 4 + 2 * 64 * 64 * 2)
     assert a % 256 == 0
     assert ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_F32) > a
     assert ws(1, 10241, 16, 128, 128, 64, 0, gdn.GDN_BF16) > a       # a partial chunk adds a slot
@@ -94,6 +94,10 @@ def _prefill(L, **kw):
     (dict(n_seqs=3), INVALID),                   # n_seqs without cu_seqlens
     (dict(cu=A, n_seqs=2, B=2), INVALID),        # ragged needs B == 1
     (dict(cu=A + 2, n_seqs=2), INVALID),         # misaligned offsets
+    (dict(g=A + 2), INVALID),
+    (dict(beta=A + 1), INVALID),
+    (dict(v=A + 4), INVALID),
+    (dict(o=A + 8), INVALID),
     (dict(n_seqs=-1, cu=A), INVALID),
     (dict(ws=None), WORKSPACE),
     (dict(ws_bytes=1000), WORKSPACE),
@@ -121,7 +125,8 @@ def _decode(L, **kw):
     (dict(io=3), INVALID), (dict(B=0), INVALID), (dict(H=-1), INVALID),
     (dict(dk=100), UNSUPPORTED), (dict(dv=32), UNSUPPORTED), (dict(dk=0), INVALID),
     (dict(q=None), INVALID), (dict(S=None), INVALID), (dict(o=None), INVALID),
-    (dict(g=None), INVALID), (dict(v=A + 4), INVALID), (dict(S=A + 8), INVALID),
+    (dict(g=None), INVALID), (dict(v=A + 2), INVALID), (dict(S=A + 8), INVALID),
+    (dict(g=A + 2), INVALID), (dict(q=A + 1, io=1), INVALID),
 ])
 def test_decode_argument_checks(L, kw, code):
     assert _decode(L, **kw) == code
