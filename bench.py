@@ -1,0 +1,199 @@
+"""Benchmark of the gated delta-rule hot path on one MI355X.
+
+Default workload: chunked prefill of one recurrent layer, B=1, T=10240, H=16,
+dk=dv=128, chunk 64, bf16 q/k/v/o with fp32 gates and state (the paper's
+16 value heads with H_k = H_v = 128, section 2.2, at its 10k-token tier).
+A step is one gdn_chunk_prefill call over the whole prompt (every kernel of
+the path).  Prints ONE JSON line on stdout.
+
+Inputs are resident in HBM before timing starts; each step reads a different
+one of ``--sets`` input sets (4 x 171 MB by default, larger than the 256 MB
+Infinity Cache), so no step finds its inputs in cache from the previous one.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {"hbm": 8.0e12, "bf16": 2.5e15, "f32": 157.3e12}   # MI355X published peaks
+
+
+def algorithmic(w, lens, dk, dv, H, io, s0, decode=False):
+    """Bytes and flops the method must move / perform (no padding, no re-reads)."""
+    s_io = 2 if io == "bf16" else 4
+    ntok = sum(lens)
+    if decode:
+        n = len(lens)
+        byts = n * H * ((2 * dk + 2 * dv) * s_io + 8 + 2 * 4 * dv * dk)
+        flops = n * H * 6 * dk * dv
+        return byts, flops
+    byts = ntok * H * ((2 * dk + 2 * dv) * s_io + 8) + len(lens) * H * 4 * dv * dk * (2 if s0 else 1)
+    flops = 0
+    for L in lens:
+        for c0 in range(0, L, 64):
+            n = min(64, L - c0)
+            flops += (n * (n - 1) * dk + n * (n + 1) * dk + n * (n - 1) * (dk + dv) + n * (n + 1) * dv
+                      + 6 * n * dk * dv)
+    return byts, flops * H
+
+
+def cpu_baseline(w, x, budget_s):
+    """The fp64 oracle, as it stands, on this host's cores, on the same inputs."""
+    import oracle
+    from paper_2607_14568_amd import inputs as I
+    f = I.as_f64
+    if w.decode:
+        args = [f(x[k][0]) for k in ("q", "k", "v", "g", "beta")]
+        S = f(x["S"])
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.decode_step(*args, S)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > budget_s or reps >= 1000:
+                break
+        tok = reps * w.B
+        sample = "%d decode steps of the %d-sequence batch" % (reps, w.B)
+    else:
+        cu = None if x["cu_seqlens"] is None else x["cu_seqlens"].numpy()
+        args = [f(x[k]) for k in ("q", "k", "v", "g", "beta")]
+        S0 = f(x["S0"])
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.recurrence(*args, S0, cu_seqlens=cu)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > budget_s:
+                break
+        tok = reps * int(x["q"].shape[0] * x["q"].shape[1])
+        sample = "%d full call(s) of the same workload (all %d heads)" % (reps, w.H)
+    return {"value": tok / el, "unit": "tokens/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": sample, "seconds": round(el, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="prefill_10k_bf16")
+    ap.add_argument("--sets", type=int, default=4, help="rotating resident input sets")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
+              "(the multi-GPU sharding is a design note only)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_14568_amd as gdn
+    from paper_2607_14568_amd import inputs as I
+
+    if not os.path.exists(gdn.LIB_PATH):
+        from paper_2607_14568_amd import build as B
+        B.build_library(force=True)
+    w = I.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    x_host = I.make_workload(args.workload)
+    sets = []
+    for i in range(max(1, args.sets)):
+        d = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in x_host.items()}
+        if i > 0:   # distinct buffers with the same values (the parity tests cover the values)
+            d = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in d.items()}
+        sets.append(d)
+
+    if w.decode:
+        lens = [1] * w.B
+        for d in sets:
+            d["S"] = d["S"].clone()
+            d["o"] = torch.empty_like(d["v"][0])
+
+        def step(i):
+            d = sets[i % len(sets)]
+            j = i % d["q"].shape[0]
+            gdn.gdn_decode_step(d["q"][j], d["k"][j], d["v"][j], d["g"][j], d["beta"][j], d["S"], o=d["o"])
+    else:
+        cu = x_host["cu_seqlens"]
+        lens = [int(a) for a in (cu[1:] - cu[:-1])] if cu is not None else [w.T] * w.B
+        n_seqs = 0 if cu is None else len(lens)
+        io_code = gdn.GDN_BF16 if w.io == "bf16" else gdn.GDN_F32
+        need = gdn.gdn_chunk_prefill_workspace_bytes(x_host["q"].shape[0], x_host["q"].shape[1], w.H, w.dk,
+                                                     w.dv, 64, n_seqs, io_code)
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        for d in sets:
+            d["o"] = torch.empty_like(d["v"])
+            d["S_T"] = torch.empty_like(d["S0"]) if d["S0"] is not None else None
+
+        def step(i):
+            d = sets[i % len(sets)]
+            gdn.gdn_chunk_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], cu_seqlens=d["cu_seqlens"],
+                                  o=d["o"], S_T=d["S_T"], workspace=ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # per-call durations with HIP events on the stream the library launches on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(args.warmup + i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    call_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = t_wall * 1e3 / args.steps
+    avg_call_s = sum(call_ms) / len(call_ms) * 1e-3
+
+    ntok = sum(lens)
+    value = ntok / (ms_per_step * 1e-3)
+    byts, flops = algorithmic(w, lens, w.dk, w.dv, w.H, w.io, w.s0_std > 0, decode=w.decode)
+    t_hbm = byts / PEAK["hbm"]
+    t_mfma = flops / PEAK[w.io]
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": byts / avg_call_s / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": flops / avg_call_s / 1e12, "peak": PEAK[w.io] / 1e12,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = "one gdn_decode_step call" if w.decode else \
+        "one gdn_chunk_prefill call (k_chunk_terms + k_state_chain)"
+    roof["alg_bytes"] = byts
+    roof["alg_flops"] = flops
+    roof["avg_call_us"] = avg_call_s * 1e6
+    roof["min_call_us"] = min(call_ms) * 1e3
+
+    out = {
+        "metric": "gated-delta-rule prefill tokens/s at T=10240,H=16,d=128; % of roofline",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.io, "data": "synthetic",
+        "config": {"workload": w.name, "B": len(lens) if w.ragged else w.B, "T": ntok if w.ragged else w.T,
+                   "H": w.H, "dk": w.dk, "dv": w.dv, "chunk": 64, "io": w.io, "state": "fp32",
+                   "parallelism": "none (1 GPU)", "input_sets": len(sets)},
+        "roofline": roof,
+    }
+    if w.decode:
+        out["metric"] = "gated-delta-rule decode-step tokens/s (B=64,H=16,d=128)"
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, x_host, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
