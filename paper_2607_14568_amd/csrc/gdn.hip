@@ -94,6 +94,25 @@ template <> struct Mma<float> {
     __device__ static __forceinline__ frag pack(const float* x) { return x[0]; }
 };
 
+// Fragment order of the lower-triangular 64x64 matrices T and P for bf16 io.
+// A 16x16x32 MFMA over a 64-long token contraction needs, for output row tile
+// mt, contraction blocks kk = 0..mt/2 (the rest is zero): six fragments
+// f = (mt, kk) = (0,0) (1,0) (2,0) (2,1) (3,0) (3,1).  Lane l, element e of
+// fragment f holds M[frag_row(f, l)][frag_col(f, l, e)], so that contraction
+// element e of lane group l/16 is token 32*kk + 16*(e/4) + 4*(l/16) + e%4 --
+// exactly the rows an MFMA accumulator tile pair holds in that lane.
+constexpr int NFRAG = 6;
+__host__ __device__ constexpr int frag_id(int mt, int kk) { return mt < 2 ? mt : 2 + 2 * (mt - 2) + kk; }
+__device__ __forceinline__ int frag_mt(int f) { return f < 2 ? f : 2 + ((f - 2) >> 1); }
+__device__ __forceinline__ int frag_kk(int f) { return f < 2 ? 0 : ((f - 2) & 1); }
+__device__ __forceinline__ int frag_row(int f, int l) { return 16 * frag_mt(f) + (l & 15); }
+__device__ __forceinline__ int frag_col(int f, int l, int e) {
+    return 32 * frag_kk(f) + 16 * (e >> 2) + 4 * (l >> 4) + (e & 3);
+}
+
+// Elements per (chunk, head) slot of T and of P in the workspace.
+template <typename IO> __host__ __device__ constexpr int tp_elems() { return sizeof(IO) == 2 ? NFRAG * 64 * 8 : CH * CH; }
+
 // ------------------------------------------------------------------ parameters
 struct Params {
     const void* q;
@@ -195,6 +214,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __shared__ __attribute__((aligned(16))) IO sQ[CH][DK + PAD];
     __shared__ __attribute__((aligned(16))) float sA[CH][CH + 4];
     __shared__ __attribute__((aligned(16))) float sTi[CH][CH + 4];
+    __shared__ __attribute__((aligned(16))) float sP[CH][CH + 4];
     __shared__ float sZ[4][16][17];
     __shared__ double sG[CH];
     __shared__ float sB[CH];
@@ -202,8 +222,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const long slot = (long)gc * H + h;
-    IO* Tg = reinterpret_cast<IO*>(p.wsT) + slot * CH * CH;
-    IO* Pg = reinterpret_cast<IO*>(p.wsP) + slot * CH * CH;
+    IO* Tg = reinterpret_cast<IO*>(p.wsT) + slot * tp_elems<IO>();
+    IO* Pg = reinterpret_cast<IO*>(p.wsP) + slot * tp_elems<IO>();
 
     if (wave == 0) {
         float gv = 0.f, bv = 0.f;   // padded rows: no decay, no write
@@ -225,11 +245,6 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     }
     stage_rows<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), t0, n, H, h);
     stage_rows<IO, DK, DK + PAD>(sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
-    // strictly-upper 16x16 blocks of P are zero
-    for (int i = tid; i < CH * CH; i += NT) {
-        const int r = i / CH, cc = i % CH;
-        if ((cc >> 4) > (r >> 4)) Pg[i] = from_f<IO>(0.f);
-    }
     __syncthreads();
 
     // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P)
@@ -252,7 +267,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
             if (which == 0) {
                 sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * acc[e] : 0.f;
             } else {
-                Pg[r * CH + i] = from_f<IO>((r >= i) ? expf((float)(sG[r] - sG[i])) * acc[e] : 0.f);
+                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * acc[e] : 0.f;
             }
         }
     }
@@ -300,9 +315,30 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
         __syncthreads();
     }
-    for (int i = tid; i < CH * CH; i += NT) {
-        const int r = i / CH, cc = i % CH;
-        Tg[i] = from_f<IO>((cc >> 4) > (r >> 4) ? 0.f : sTi[r][cc]);
+    // T and P leave in the layout their consumer reads: row-major squares for
+    // fp32 io, MFMA fragment order (see frag_row/frag_col) for bf16 io.  Blocks
+    // above the diagonal are zero.
+    if (sizeof(IO) == 4) {
+        for (int i = tid; i < CH * CH; i += NT) {
+            const int r = i / CH, cc = i % CH;
+            const bool up = (cc >> 4) > (r >> 4);
+            Tg[i] = from_f<IO>(up ? 0.f : sTi[r][cc]);
+            Pg[i] = from_f<IO>(up ? 0.f : sP[r][cc]);
+        }
+    } else {
+        for (int i = tid; i < 2 * NFRAG * 64; i += NT) {
+            const int which = i / (NFRAG * 64), f = (i / 64) % NFRAG, l = i % 64;
+            const float(*Msrc)[CH + 4] = which ? sP : sTi;
+            IO* dst = (which ? Pg : Tg) + (f * 64 + l) * 8;
+            const int r = frag_row(f, l);
+            bf16_t v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int cc = frag_col(f, l, e);
+                v[e] = from_f<bf16_t>((cc >> 4) > (r >> 4) ? 0.f : Msrc[r][cc]);
+            }
+            *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
+        }
     }
 }
 
@@ -350,8 +386,8 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
         stage_rows<IO, DK, DK + PAD>(sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
         {
             constexpr int VE = 16 / sizeof(IO), VPR = CH / VE;
-            const IO* Tg = reinterpret_cast<const IO*>(p.wsT) + slot * CH * CH;
-            const IO* Pg = reinterpret_cast<const IO*>(p.wsP) + slot * CH * CH;
+            const IO* Tg = reinterpret_cast<const IO*>(p.wsT) + slot * tp_elems<IO>();
+            const IO* Pg = reinterpret_cast<const IO*>(p.wsP) + slot * tp_elems<IO>();
             for (int i = tid; i < CH * VPR; i += NT) {
                 const int r = i / VPR, cv = i % VPR;
                 *reinterpret_cast<uint4*>(&sT[r][cv * VE]) = *reinterpret_cast<const uint4*>(Tg + r * CH + cv * VE);
@@ -461,6 +497,306 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
         for (int i = tid; i < SL * DK; i += NT) p.ST[srow0 + i] = sS[i / DK][i % DK];
 }
 
+// ------------------------------------------------------------------ bf16 state chain
+// One workgroup per (sequence, head, 16-row slice of S), bf16 io.
+//  waves 0,1 ("chain"): wave w keeps S^T rows [DK/2 w, DK/2 (w+1)) of the slice
+//    as fp32 MFMA accumulators.  Per chunk: partial X = K S^T over its half of
+//    the key channels, one LDS exchange of the partials, R = diag(beta)(V -
+//    diag(gamma) X), U = T R, and S^T <- gamma_n S^T + K^T D U for its half.
+//    Every B operand (S, R, D U) is packed from the lane's own accumulators:
+//    accumulator tile m holds rows 16m + 4(l/16) + e, so contraction element e'
+//    of lane group l/16 in block kk stands for index 32kk + 16(e'/4) + 4(l/16) +
+//    e'%4, and the A operands (K, T, K^T) are read in that same order.  K^T comes
+//    from the row-major K tile through LDS transpose reads.
+//  waves 2,3 ("output"): O of the previous chunk for one half of its tokens,
+//    O = scale (diag(gamma) Q S^T + P U), from the S and U fragments the chain
+//    waves left in LDS; they also stage the next chunk's K, V slice and decay
+//    vectors into the other half of the double-buffered LDS.
+// Two barriers per chunk: the X exchange and the end of the chunk.
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 pack_bf16(floatx4 a, floatx4 b) {
+    const floatx8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_convertvector(x, bf16x8);
+}
+__device__ __forceinline__ bf16x8 join4(short4v a, short4v b) {
+    const short8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, x);
+}
+__device__ __forceinline__ short4v lds_ld8(const bf16_t* ptr) { return *reinterpret_cast<const short4v*>(ptr); }
+// Transpose read: within each 16-lane group, lane i element e receives element
+// i%4 of the 8 bytes addressed by lane 4e + i/4 of the group.
+__device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
+    typedef __attribute__((address_space(3))) short4v lds_short4v;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(ptr));
+}
+__device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)(uint16_t)x << 16); }
+__device__ __forceinline__ short4v gld8(const bf16_t* ptr) { return *reinterpret_cast<const short4v*>(ptr); }
+
+template <int DK>
+__global__ __launch_bounds__(NT) void k_state_chain_bf16(Params p) {
+    constexpr int NKD = DK / 32;   // MFMA contraction blocks over the key channels
+    constexpr int HKD = NKD / 2;   // ... per chain wave
+    constexpr int HMD = DK / 32;   // 16-row S^T tiles per chain wave
+    constexpr int LDK = DK + 8;    // padded LDS row of K (bf16)
+    constexpr int KV = DK / 16;    // 16-byte K loads per staging thread
+    const int H = p.H, DV = p.DV, nsl = DV / SL;
+    const int js = blockIdx.x % nsl;
+    const int h = (blockIdx.x / nsl) % H;
+    const int s = blockIdx.x / (nsl * H);
+    long start;
+    int len, cbase;
+    seq_info(p, s, start, len, cbase);
+    const int nc = (len + CH - 1) / CH;
+
+    __shared__ __attribute__((aligned(16))) bf16_t sK[2][CH][LDK];
+    __shared__ __attribute__((aligned(16))) bf16_t sVt[2][SL][CH + 8];
+    __shared__ __attribute__((aligned(16))) floatx4 sXp[2][4][64];
+    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];
+    __shared__ __attribute__((aligned(16))) bf16x8 sUf[2][2][64];
+    __shared__ __attribute__((aligned(16))) float sGam[2][CH];
+    __shared__ __attribute__((aligned(16))) float sDec[2][CH];
+    __shared__ __attribute__((aligned(16))) float sBeta[2][CH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
+    const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
+    const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
+    const bf16_t* gvv = reinterpret_cast<const bf16_t*>(p.v);
+    const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
+    const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
+    bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
+    auto rows = [&](int c) { return min(CH, len - c * CH); };
+    auto tok0 = [&](int c) { return start + (long)c * CH; };
+    auto slot = [&](int c) { return (long)(cbase + c) * H + h; };
+
+    // staging of chunk c by the 128 threads t of waves 2,3 (or by all in the prologue)
+    struct Stage {
+        uint4 k[KV];
+        uint4 v;
+        float gam, dec, bet;
+    };
+    auto stage_load = [&](int c, Stage& st, int t) {
+        const long t0 = tok0(c);
+        const int n = rows(c);
+#pragma unroll
+        for (int i = 0; i < KV; ++i) {
+            const int idx = t + 128 * i, r = idx / (DK / 8), cv = idx % (DK / 8);
+            st.k[i] = make_uint4(0, 0, 0, 0);
+            if (r < n) st.k[i] = *reinterpret_cast<const uint4*>(gk + ((t0 + r) * H + h) * (long)DK + cv * 8);
+        }
+        {
+            const int r = t >> 1, hf = t & 1;
+            st.v = make_uint4(0, 0, 0, 0);
+            if (r < n) st.v = *reinterpret_cast<const uint4*>(gvv + ((t0 + r) * H + h) * (long)DV + js * SL + hf * 8);
+        }
+        if (t < CH) {
+            st.gam = p.wsG[slot(c) * 2 * CH + t];
+            st.dec = p.wsG[slot(c) * 2 * CH + CH + t];
+            st.bet = (t < n) ? p.beta[(t0 + t) * H + h] : 0.f;
+        }
+    };
+    auto stage_store = [&](int b, const Stage& st, int t) {
+#pragma unroll
+        for (int i = 0; i < KV; ++i) {
+            const int idx = t + 128 * i, r = idx / (DK / 8), cv = idx % (DK / 8);
+            *reinterpret_cast<uint4*>(&sK[b][r][cv * 8]) = st.k[i];
+        }
+        {
+            const int r = t >> 1, hf = t & 1;
+            const bf16_t* vv = reinterpret_cast<const bf16_t*>(&st.v);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sVt[b][hf * 8 + e][r] = vv[e];
+        }
+        if (t < CH) {
+            sGam[b][t] = st.gam;
+            sDec[b][t] = st.dec;
+            sBeta[b][t] = st.bet;
+        }
+    };
+
+    if (wave < 2) {
+        // ------------------------------------------------ chain waves
+        const int w = wave;
+        floatx4 acc[HMD];
+#pragma unroll
+        for (int m = 0; m < HMD; ++m) {
+            const int md = w * HMD + m;
+            acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + 16 * md + 4 * lg);
+        }
+        bf16x8 tf[NFRAG], tfn[NFRAG];
+        if (nc > 0) {
+#pragma unroll
+            for (int f = 0; f < NFRAG; ++f)
+                tf[f] = *reinterpret_cast<const bf16x8*>(wsT + slot(0) * tp_elems<bf16_t>() + (f * 64 + lane) * 8);
+        }
+        __syncthreads();   // prologue staging of chunk 0
+        for (int c = 0; c <= nc; ++c) {
+            const int b = c & 1;
+            if (c < nc) {
+                if (c + 1 < nc) {
+#pragma unroll
+                    for (int f = 0; f < NFRAG; ++f)
+                        tfn[f] = *reinterpret_cast<const bf16x8*>(wsT + slot(c + 1) * tp_elems<bf16_t>() +
+                                                                   (f * 64 + lane) * 8);
+                }
+                // S fragments of this wave's key blocks; partial X = K S^T
+                bf16x8 sf[HKD];
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) {
+                    sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
+                    sSf[b][w * HKD + k2][lane] = sf[k2];
+                }
+                floatx4 x[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    x[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int k2 = 0; k2 < HKD; ++k2) {
+                        const int kk = w * HKD + k2;
+                        const bf16_t* row = &sK[b][16 * mt + l16][32 * kk + 4 * lg];
+                        x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(join4(lds_ld8(row), lds_ld8(row + 16)), sf[k2],
+                                                                        x[mt], 0, 0, 0);
+                    }
+                    sXp[w][mt][lane] = x[mt];
+                }
+                __syncthreads();   // A: partials visible
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) x[mt] += sXp[1 - w][mt][lane];
+                // R = diag(beta) (V - diag(gamma) X)
+                floatx4 r[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    const short4v v4 = lds_ld8(&sVt[b][l16][16 * mt + 4 * lg]);
+                    const floatx4 gm = *reinterpret_cast<const floatx4*>(&sGam[b][16 * mt + 4 * lg]);
+                    const floatx4 bt = *reinterpret_cast<const floatx4*>(&sBeta[b][16 * mt + 4 * lg]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) r[mt][e] = bt[e] * (bf(v4[e]) - gm[e] * x[mt][e]);
+                }
+                const bf16x8 rf0 = pack_bf16(r[0], r[1]), rf1 = pack_bf16(r[2], r[3]);
+                // U = T R (lower triangular: tile mt needs contraction blocks 0..mt/2)
+                floatx4 u[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    u[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tf[frag_id(mt, 0)], rf0,
+                                                                    floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    if (mt >= 2) u[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tf[frag_id(mt, 1)], rf1, u[mt], 0, 0, 0);
+                }
+                if (w == 0) {
+                    sUf[b][0][lane] = pack_bf16(u[0], u[1]);
+                    sUf[b][1][lane] = pack_bf16(u[2], u[3]);
+                }
+                floatx4 du[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) du[mt] = u[mt] * *reinterpret_cast<const floatx4*>(&sDec[b][16 * mt + 4 * lg]);
+                const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
+                // S^T <- gamma_n S^T + K^T (D U) on this wave's key tiles
+                const float gn = sGam[b][CH - 1];
+#pragma unroll
+                for (int m = 0; m < HMD; ++m) {
+                    const int md = w * HMD + m;
+                    acc[m] *= gn;
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk) {
+                        const bf16_t* p0 = &sK[b][32 * kk + 4 * lg + (l16 >> 2)][16 * md + 4 * (l16 & 3)];
+                        acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(join4(lds_tr8(p0), lds_tr8(p0 + 16 * LDK)),
+                                                                         kk ? df1 : df0, acc[m], 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int f = 0; f < NFRAG; ++f) tf[f] = tfn[f];
+            } else {
+                __syncthreads();   // A (no chunk left)
+            }
+            __syncthreads();   // B
+        }
+        if (p.ST) {
+#pragma unroll
+            for (int m = 0; m < HMD; ++m)
+                *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + 16 * (w * HMD + m) + 4 * lg) = acc[m];
+        }
+    } else {
+        // ------------------------------------------------ output + staging waves
+        const int t = tid - 128, ow = wave - 2;
+        Stage st;
+        if (nc > 0) {
+            stage_load(0, st, t);
+            stage_store(0, st, t);
+        }
+        bf16x8 qf[2][NKD], qfn[2][NKD], pf[2][2], pfn[2][2];
+        __syncthreads();   // prologue staging visible
+        for (int c = 0; c <= nc; ++c) {
+            if (c + 1 < nc) stage_load(c + 1, st, t);
+            if (c < nc) {   // Q and P fragments of chunk c, used next iteration
+                const long t0 = tok0(c);
+                const int n = rows(c);
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int mt = 2 * ow + i, row = 16 * mt + l16;
+#pragma unroll
+                    for (int kk = 0; kk < NKD; ++kk) {
+                        short4v a = {0, 0, 0, 0}, bq = {0, 0, 0, 0};
+                        if (row < n) {
+                            const bf16_t* qp = gq + ((t0 + row) * H + h) * (long)DK + 32 * kk + 4 * lg;
+                            a = gld8(qp);
+                            bq = gld8(qp + 16);
+                        }
+                        qfn[i][kk] = join4(a, bq);
+                    }
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk)
+                        if (kk <= mt / 2)
+                            pfn[i][kk] = *reinterpret_cast<const bf16x8*>(wsP + slot(c) * tp_elems<bf16_t>() +
+                                                                          (frag_id(mt, kk) * 64 + lane) * 8);
+                }
+            }
+            floatx4 gm[2];
+            if (c >= 1) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    gm[i] = *reinterpret_cast<const floatx4*>(&sGam[(c - 1) & 1][16 * (2 * ow + i) + 4 * lg]);
+            }
+            __syncthreads();   // A
+            if (c >= 1) {
+                const int cp = c - 1, bp = cp & 1;
+                const long t0 = tok0(cp);
+                const int n = rows(cp);
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int mt = 2 * ow + i;
+                    floatx4 oq = {0.f, 0.f, 0.f, 0.f}, op = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kk = 0; kk < NKD; ++kk)
+                        oq = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[i][kk], sSf[bp][kk][lane], oq, 0, 0, 0);
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk)
+                        if (kk <= mt / 2)
+                            op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[i][kk], sUf[bp][kk][lane], op, 0, 0, 0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int rr = 16 * mt + 4 * lg + e;
+                        if (rr < n)
+                            go[((t0 + rr) * H + h) * (long)DV + js * SL + l16] =
+                                from_f<bf16_t>(p.scale * (gm[i][e] * oq[e] + op[e]));
+                    }
+                }
+            }
+            if (c + 1 < nc) stage_store((c + 1) & 1, st, t);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+#pragma unroll
+                for (int kk = 0; kk < NKD; ++kk) qf[i][kk] = qfn[i][kk];
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) pf[i][kk] = pfn[i][kk];
+            }
+            __syncthreads();   // B
+        }
+    }
+}
+
 // ------------------------------------------------------------------ decode
 // One token per sequence.  LPR lanes hold one state row as float4s; rows of S
 // evolve independently: s_j <- alpha (s_j - beta (s_j.k) k) + beta v_j k.
@@ -533,8 +869,9 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     L->meta = 0;
     L->G = n_seqs > 0 ? round_up((size_t)3 * (n_seqs + 1) * sizeof(int32_t), 256) : 0;
     L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
-    L->P = L->T + round_up(per * CH * CH * esz, 256);
-    L->total = L->P + round_up(per * CH * CH * esz, 256);
+    const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
+    L->P = L->T + round_up(per * tp * esz, 256);
+    L->total = L->P + round_up(per * tp * esz, 256);
     return true;
 }
 
@@ -547,8 +884,11 @@ void launch_prefill(const Params& p, long slots, hipStream_t st) {
                            p.seq_len, p.chunk_off);
     if (slots > 0 && p.T > 0)
         hipLaunchKernelGGL((k_chunk_terms<IO, DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
-    hipLaunchKernelGGL((k_state_chain<IO, DK>), dim3((unsigned)(p.n_seq * p.H * (p.DV / SL))), dim3(NT), 0,
-                       st, p);
+    const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
+    if (sizeof(IO) == 2)
+        hipLaunchKernelGGL((k_state_chain_bf16<DK>), grid, dim3(NT), 0, st, p);
+    else
+        hipLaunchKernelGGL((k_state_chain<IO, DK>), grid, dim3(NT), 0, st, p);
 }
 
 template <typename IO, int DK>
