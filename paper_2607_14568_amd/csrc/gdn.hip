@@ -217,7 +217,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __shared__ __attribute__((aligned(16))) float sP[CH][CH + 4];
     __shared__ float sZ[4][16][17];
     __shared__ double sG[CH];
-    __shared__ float sB[CH];
+    __shared__ float sB[CH], sD[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -240,6 +240,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         const double xn = __shfl(x, 63, 64);   // G_n (padded rows add nothing)
         sG[lane] = x;
         sB[lane] = bv;
+        sD[lane] = expf((float)(xn - x));
         p.wsG[slot * 2 * CH + lane] = expf((float)x);
         p.wsG[slot * 2 * CH + CH + lane] = expf((float)(xn - x));
     }
@@ -315,30 +316,51 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
         __syncthreads();
     }
-    // T and P leave in the layout their consumer reads: row-major squares for
-    // fp32 io, MFMA fragment order (see frag_row/frag_col) for bf16 io.  Blocks
-    // above the diagonal are zero.
     if (sizeof(IO) == 4) {
+        // fp32 io: T and P as row-major squares, zero above the diagonal blocks
         for (int i = tid; i < CH * CH; i += NT) {
             const int r = i / CH, cc = i % CH;
             const bool up = (cc >> 4) > (r >> 4);
             Tg[i] = from_f<IO>(up ? 0.f : sTi[r][cc]);
             Pg[i] = from_f<IO>(up ? 0.f : sP[r][cc]);
         }
-    } else {
-        for (int i = tid; i < 2 * NFRAG * 64; i += NT) {
-            const int which = i / (NFRAG * 64), f = (i / 64) % NFRAG, l = i % 64;
-            const float(*Msrc)[CH + 4] = which ? sP : sTi;
-            IO* dst = (which ? Pg : Tg) + (f * 64 + l) * 8;
-            const int r = frag_row(f, l);
-            bf16_t v[8];
+        return;
+    }
+    // bf16 io: beta and the decay to the chunk end are folded into the two
+    // matrices the state chain applies to R' = V - diag(gamma) K S0^T:
+    //   D U   = (diag(D) T diag(beta)) R'     (input of the state update)
+    //   P U   = (P T diag(beta)) R'           (output correction)
+    // Both are lower triangular; P T is formed here with fp32 MFMA over the
+    // needed 16-blocks (sA is free once the solve is done).
+    float(*sPT)[CH + 4] = sA;
+    for (int job = wave; job < 10; job += 4) {
+        int t = job, bi = 0;
+        while (t > bi) { t -= bi + 1; ++bi; }
+        const int bj = t;
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int m = bj; m <= bi; ++m) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int cc = frag_col(f, l, e);
-                v[e] = from_f<bf16_t>((cc >> 4) > (r >> 4) ? 0.f : Msrc[r][cc]);
-            }
-            *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
+            for (int kk = 0; kk < 4; ++kk)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sP[16 * bi + l16][16 * m + 4 * kk + lg],
+                                                           sTi[16 * m + 4 * kk + lg][16 * bj + l16], acc, 0, 0, 0);
         }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sPT[16 * bi + 4 * lg + e][16 * bj + l16] = acc[e];
+    }
+    __syncthreads();
+    // fragment order (frag_row / frag_col); blocks above the diagonal are zero
+    for (int i = tid; i < 2 * NFRAG * 64; i += NT) {
+        const int which = i / (NFRAG * 64), f = (i / 64) % NFRAG, l = i % 64;
+        IO* dst = (which ? Pg : Tg) + (f * 64 + l) * 8;
+        const int r = frag_row(f, l);
+        bf16_t v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int cc = frag_col(f, l, e);
+            const float val = which ? sPT[r][cc] * sB[cc] : sD[r] * sTi[r][cc] * sB[cc];
+            v[e] = from_f<bf16_t>((cc >> 4) > (r >> 4) ? 0.f : val);
+        }
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
     }
 }
 
@@ -498,23 +520,45 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
 }
 
 // ------------------------------------------------------------------ bf16 state chain
-// One workgroup per (sequence, head, 16-row slice of S), bf16 io.
-//  waves 0,1 ("chain"): wave w keeps S^T rows [DK/2 w, DK/2 (w+1)) of the slice
-//    as fp32 MFMA accumulators.  Per chunk: partial X = K S^T over its half of
-//    the key channels, one LDS exchange of the partials, R = diag(beta)(V -
-//    diag(gamma) X), U = T R, and S^T <- gamma_n S^T + K^T D U for its half.
-//    Every B operand (S, R, D U) is packed from the lane's own accumulators:
-//    accumulator tile m holds rows 16m + 4(l/16) + e, so contraction element e'
-//    of lane group l/16 in block kk stands for index 32kk + 16(e'/4) + 4(l/16) +
-//    e'%4, and the A operands (K, T, K^T) are read in that same order.  K^T comes
-//    from the row-major K tile through LDS transpose reads.
-//  waves 2,3 ("output"): O of the previous chunk for one half of its tokens,
-//    O = scale (diag(gamma) Q S^T + P U), from the S and U fragments the chain
-//    waves left in LDS; they also stage the next chunk's K, V slice and decay
-//    vectors into the other half of the double-buffered LDS.
-// Two barriers per chunk: the X exchange and the end of the chunk.
+// One workgroup of 5 waves per (sequence, head, 16-row slice of S), bf16 io.
+//  waves 0,1 ("chain"): wave w keeps S^T rows of key-channel tiles
+//    [NMD/2 w, NMD/2 (w+1)) of the slice as fp32 MFMA accumulators.  Per chunk:
+//    partial X = K S^T over its key channels, one LDS exchange of the partials,
+//    R' = V - diag(gamma) X, D U = (diag(D) T diag(beta)) R', and
+//    S^T <- gamma_n S^T + K^T (D U) for its tiles (beta and D are folded into
+//    the matrix by the chunk-terms kernel).  Every B operand (S, R', D U) is
+//    packed from the lane's own accumulators; the A operands are read in the
+//    matching contraction order:
+//      - token contractions: element e of lane group g in block kk is token
+//        32 kk + 16 (e/4) + 4 g + e%4 (the rows an accumulator tile pair holds);
+//      - key contractions: accumulator tile md, lane group g, element e holds
+//        key channel 32 (md/2) + 8 g + 4 (md%2) + e, so a lane's 8 contraction
+//        elements of block kk are the contiguous channels 32 kk + 8 g .. +7 and
+//        the K (and Q) operands are single 16-byte reads.  K^T comes from the
+//        same row-major K tile through LDS transpose reads.
+//  waves 2,3 ("output"): O^T = scale (S Q^T diag(gamma) + R'^T (P T diag(beta))^T)
+//    for one half of the chunk's tokens -- the operands of the O products
+//    swapped, so a lane ends up with 4 consecutive value channels of one token
+//    and writes them with one 8-byte store.
+//  wave 4 ("loader"): copies chunk c+2 (K, Q, both chunk matrices, the V slice,
+//    gamma) from global memory straight into a 3-deep LDS ring with buffer
+//    loads to LDS.  Per chunk, the buffer descriptors end at row n-1 of the
+//    head, so the rows of a partial chunk read back as zeros.  It waits for
+//    chunk c+1 before the end of chunk c; the other waves issue no global
+//    loads, so nothing they do waits on memory.
+// K and Q rows sit in LDS with their 16-byte chunks XOR-swizzled by row, which
+// keeps both the row reads (16 rows, one chunk) and the transpose reads
+// (4 rows, 4 chunks) free of bank conflicts.
+// Three barriers per chunk: X partials ready (A), R' ready (C), end of chunk (B);
+// they order LDS traffic only, so global loads and stores stay in flight.
+// The chunk loop is unrolled by the ring depth so ring slots are constants.
 typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short short4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+constexpr int NT_CHAIN = 320;
+constexpr int RING = 3;
+template <int N> struct Ic { static constexpr int value = N; };
 
 __device__ __forceinline__ bf16x8 pack_bf16(floatx4 a, floatx4 b) {
     const floatx8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
@@ -524,7 +568,6 @@ __device__ __forceinline__ bf16x8 join4(short4v a, short4v b) {
     const short8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, x);
 }
-__device__ __forceinline__ short4v lds_ld8(const bf16_t* ptr) { return *reinterpret_cast<const short4v*>(ptr); }
 // Transpose read: within each 16-lane group, lane i element e receives element
 // i%4 of the 8 bytes addressed by lane 4e + i/4 of the group.
 __device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
@@ -532,268 +575,507 @@ __device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(ptr));
 }
 __device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)(uint16_t)x << 16); }
-__device__ __forceinline__ short4v gld8(const bf16_t* ptr) { return *reinterpret_cast<const short4v*>(ptr); }
+// Buffer resource over [base, base + bytes); loads past the end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+// global -> LDS without registers: lane l's 16 (4) bytes land at dst + 16 l (4 l)
+__device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, 0, 0, 0);
+}
+__device__ __forceinline__ void bdma4(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, 0, 0, 0);
+}
+// Workgroup barrier ordering LDS traffic only: the wave's own LDS operations
+// complete, the compiler moves no memory access across it, and -- unlike
+// __syncthreads() -- it does not wait for outstanding global loads or stores.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 template <int DK>
-__global__ __launch_bounds__(NT) void k_state_chain_bf16(Params p) {
-    constexpr int NKD = DK / 32;   // MFMA contraction blocks over the key channels
-    constexpr int HKD = NKD / 2;   // ... per chain wave
-    constexpr int HMD = DK / 32;   // 16-row S^T tiles per chain wave
-    constexpr int LDK = DK + 8;    // padded LDS row of K (bf16)
-    constexpr int KV = DK / 16;    // 16-byte K loads per staging thread
-    const int H = p.H, DV = p.DV, nsl = DV / SL;
-    const int js = blockIdx.x % nsl;
-    const int h = (blockIdx.x / nsl) % H;
-    const int s = blockIdx.x / (nsl * H);
+__global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
+    constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
+    constexpr int HKD = NKD / 2;        // ... per chain wave
+    constexpr int HMD = DK / 32;        // 16-row S^T tiles per chain wave
+    constexpr int NCH = DK / 8;         // 16-byte chunks per K/Q row
+    constexpr int RPI = 64 / NCH;       // rows per 1 KB direct load
+    constexpr int NISSUE = 2 * NCH + 2 * NFRAG + 2 + 1;   // direct loads per chunk
+    const int H = p.H, DV = p.DV;
+    // Slices of one (sequence, head) are blockIdx values congruent modulo the
+    // number of (sequence, head) pairs, so with 8 | n_seq*H they share an XCD
+    // (dispatch is round-robin over the 8 XCDs) and its L2 copy of K, Q and the
+    // chunk matrices.
+    const int G = p.n_seq * H;
+    const int js = blockIdx.x / G;
+    const int h = (blockIdx.x % G) % H;
+    const int s = (blockIdx.x % G) / H;
     long start;
     int len, cbase;
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
 
-    __shared__ __attribute__((aligned(16))) bf16_t sK[2][CH][LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t sVt[2][SL][CH + 8];
+    __shared__ __attribute__((aligned(16))) bf16_t sK[RING][CH * DK];
+    __shared__ __attribute__((aligned(16))) bf16_t sQ[RING][CH * DK];
+    __shared__ __attribute__((aligned(16))) bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
+    __shared__ __attribute__((aligned(16))) bf16x8 sP[RING][NFRAG][64];   // P T diag(beta)
+    __shared__ __attribute__((aligned(16))) bf16_t sV[RING][CH * SL];
+    __shared__ __attribute__((aligned(16))) float sG[RING][CH];           // gamma_r
     __shared__ __attribute__((aligned(16))) floatx4 sXp[2][4][64];
-    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];
-    __shared__ __attribute__((aligned(16))) bf16x8 sUf[2][2][64];
-    __shared__ __attribute__((aligned(16))) float sGam[2][CH];
-    __shared__ __attribute__((aligned(16))) float sDec[2][CH];
-    __shared__ __attribute__((aligned(16))) float sBeta[2][CH];
+    __shared__ __attribute__((aligned(16))) bf16x8 sSf[NKD][64];
+    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
-    const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
-    const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
-    const bf16_t* gvv = reinterpret_cast<const bf16_t*>(p.v);
-    const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
-    const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
-    bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
     auto rows = [&](int c) { return min(CH, len - c * CH); };
     auto tok0 = [&](int c) { return start + (long)c * CH; };
     auto slot = [&](int c) { return (long)(cbase + c) * H + h; };
+    auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
+    // element offset of logical (row r, column cc) in a swizzled K/Q tile
+    auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
 
-    // staging of chunk c by the 128 threads t of waves 2,3 (or by all in the prologue)
-    struct Stage {
-        uint4 k[KV];
-        uint4 v;
-        float gam, dec, bet;
-    };
-    auto stage_load = [&](int c, Stage& st, int t) {
-        const long t0 = tok0(c);
-        const int n = rows(c);
+    if (wave == 4) {
+        // ------------------------------------------------ loader
+        const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
+        const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
+        const bf16_t* gv = reinterpret_cast<const bf16_t*>(p.v);
+        const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
+        const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
+        // loop-invariant byte offsets of this lane's loads within a chunk
+        int koff[NCH];
 #pragma unroll
-        for (int i = 0; i < KV; ++i) {
-            const int idx = t + 128 * i, r = idx / (DK / 8), cv = idx % (DK / 8);
-            st.k[i] = make_uint4(0, 0, 0, 0);
-            if (r < n) st.k[i] = *reinterpret_cast<const uint4*>(gk + ((t0 + r) * H + h) * (long)DK + cv * 8);
+        for (int i = 0; i < NCH; ++i) {
+            const int r = RPI * i + lane / NCH;
+            koff[i] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
         }
-        {
-            const int r = t >> 1, hf = t & 1;
-            st.v = make_uint4(0, 0, 0, 0);
-            if (r < n) st.v = *reinterpret_cast<const uint4*>(gvv + ((t0 + r) * H + h) * (long)DV + js * SL + hf * 8);
-        }
-        if (t < CH) {
-            st.gam = p.wsG[slot(c) * 2 * CH + t];
-            st.dec = p.wsG[slot(c) * 2 * CH + CH + t];
-            st.bet = (t < n) ? p.beta[(t0 + t) * H + h] : 0.f;
-        }
-    };
-    auto stage_store = [&](int b, const Stage& st, int t) {
+        int voff[2];
 #pragma unroll
-        for (int i = 0; i < KV; ++i) {
-            const int idx = t + 128 * i, r = idx / (DK / 8), cv = idx % (DK / 8);
-            *reinterpret_cast<uint4*>(&sK[b][r][cv * 8]) = st.k[i];
-        }
-        {
-            const int r = t >> 1, hf = t & 1;
-            const bf16_t* vv = reinterpret_cast<const bf16_t*>(&st.v);
+        for (int i = 0; i < 2; ++i) voff[i] = ((32 * i + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
+        auto issue_kq = [&](int c, auto SLOT) {
+            constexpr int sl = decltype(SLOT)::value;
+            const long row0 = tok0(c) * H + h;
+            const uint32_t bytes = (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2);
+            const auto rk = rsrc(gk + row0 * DK, bytes), rq = rsrc(gq + row0 * DK, bytes);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) sVt[b][hf * 8 + e][r] = vv[e];
+            for (int i = 0; i < NCH; ++i) {
+                bdma16(rk, &sK[sl][RPI * i * DK], koff[i]);
+                bdma16(rq, &sQ[sl][RPI * i * DK], koff[i]);
+            }
+        };
+        auto issue_rest = [&](int c, auto SLOT) {
+            constexpr int sl = decltype(SLOT)::value;
+            const long sc = slot(c);
+            const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
+            const auto rp = rsrc(wsP + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
+#pragma unroll
+            for (int f = 0; f < NFRAG; ++f) {
+                bdma16(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
+                bdma16(rp, &sP[sl][f][0], (f * 64 + lane) * 16);
+            }
+            const auto rv = rsrc(gv + (tok0(c) * H + h) * DV, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DV * 2));
+            bdma16(rv, &sV[sl][0], voff[0]);
+            bdma16(rv, &sV[sl][32 * SL], voff[1]);
+            bdma4(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+        };
+        auto lstep = [&](int c, auto SLOT) {
+            constexpr int bn = (decltype(SLOT)::value + 2) % RING;
+            const int cn = min(c + 2, nc - 1);
+            issue_kq(cn, Ic<bn>{});
+            lds_barrier();   // A
+            issue_rest(cn, Ic<bn>{});
+            lds_barrier();   // C
+            // all but this chunk's own loads have landed: chunk c+1 is resident
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NISSUE) : "memory");
+            lds_barrier();   // B
+        };
+        if (nc > 0) {
+            issue_kq(0, Ic<0>{});
+            issue_rest(0, Ic<0>{});
+            issue_kq(min(1, nc - 1), Ic<1>{});
+            issue_rest(min(1, nc - 1), Ic<1>{});
         }
-        if (t < CH) {
-            sGam[b][t] = st.gam;
-            sDec[b][t] = st.dec;
-            sBeta[b][t] = st.bet;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        lds_barrier();   // prologue: chunks 0 and 1 resident
+        for (int c = 0; c < nc; c += RING) {
+            lstep(c, Ic<0>{});
+            if (c + 1 < nc) lstep(c + 1, Ic<1>{});
+            if (c + 2 < nc) lstep(c + 2, Ic<2>{});
         }
-    };
-
-    if (wave < 2) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    } else if (wave < 2) {
         // ------------------------------------------------ chain waves
         const int w = wave;
+        auto chan = [&](int md) { return 32 * (md >> 1) + 8 * lg + 4 * (md & 1); };   // + e
         floatx4 acc[HMD];
 #pragma unroll
         for (int m = 0; m < HMD; ++m) {
-            const int md = w * HMD + m;
             acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
-            if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + 16 * md + 4 * lg);
+            if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(w * HMD + m));
         }
-        bf16x8 tf[NFRAG], tfn[NFRAG];
-        if (nc > 0) {
+        // loop-invariant LDS offsets of this lane's operands
+        int offX[4][HKD], offT[HMD][2][2], offV[4];
 #pragma unroll
-            for (int f = 0; f < NFRAG; ++f)
-                tf[f] = *reinterpret_cast<const bf16x8*>(wsT + slot(0) * tp_elems<bf16_t>() + (f * 64 + lane) * 8);
+        for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+            for (int k2 = 0; k2 < HKD; ++k2) offX[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
+            offV[mt] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
         }
-        __syncthreads();   // prologue staging of chunk 0
-        for (int c = 0; c <= nc; ++c) {
-            const int b = c & 1;
-            if (c < nc) {
-                if (c + 1 < nc) {
 #pragma unroll
-                    for (int f = 0; f < NFRAG; ++f)
-                        tfn[f] = *reinterpret_cast<const bf16x8*>(wsT + slot(c + 1) * tp_elems<bf16_t>() +
-                                                                   (f * 64 + lane) * 8);
-                }
-                // S fragments of this wave's key blocks; partial X = K S^T
-                bf16x8 sf[HKD];
+        for (int m = 0; m < HMD; ++m) {
+            const int md = w * HMD + m;
 #pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2) {
-                    sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
-                    sSf[b][w * HKD + k2][lane] = sf[k2];
-                }
-                floatx4 x[4];
+            for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    x[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+                for (int h2 = 0; h2 < 2; ++h2)
+                    offT[m][kk][h2] = kq(32 * kk + 16 * h2 + 4 * lg + (l16 >> 2),
+                                         32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1));
+        }
+        auto cstep = [&](auto SLOT) {
+            constexpr int b = decltype(SLOT)::value;
+            const bf16_t* K = sK[b];
+            bf16x8 xa[4][HKD];
 #pragma unroll
-                    for (int k2 = 0; k2 < HKD; ++k2) {
-                        const int kk = w * HKD + k2;
-                        const bf16_t* row = &sK[b][16 * mt + l16][32 * kk + 4 * lg];
-                        x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(join4(lds_ld8(row), lds_ld8(row + 16)), sf[k2],
-                                                                        x[mt], 0, 0, 0);
-                    }
-                    sXp[w][mt][lane] = x[mt];
-                }
-                __syncthreads();   // A: partials visible
+            for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt) x[mt] += sXp[1 - w][mt][lane];
-                // R = diag(beta) (V - diag(gamma) X)
-                floatx4 r[4];
+                for (int k2 = 0; k2 < HKD; ++k2) xa[mt][k2] = *reinterpret_cast<const bf16x8*>(K + offX[mt][k2]);
+            // S fragments of this wave's key blocks; partial X = K S^T
+            bf16x8 sf[HKD];
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    const short4v v4 = lds_ld8(&sVt[b][l16][16 * mt + 4 * lg]);
-                    const floatx4 gm = *reinterpret_cast<const floatx4*>(&sGam[b][16 * mt + 4 * lg]);
-                    const floatx4 bt = *reinterpret_cast<const floatx4*>(&sBeta[b][16 * mt + 4 * lg]);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) r[mt][e] = bt[e] * (bf(v4[e]) - gm[e] * x[mt][e]);
-                }
-                const bf16x8 rf0 = pack_bf16(r[0], r[1]), rf1 = pack_bf16(r[2], r[3]);
-                // U = T R (lower triangular: tile mt needs contraction blocks 0..mt/2)
-                floatx4 u[4];
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    u[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tf[frag_id(mt, 0)], rf0,
-                                                                    floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                    if (mt >= 2) u[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tf[frag_id(mt, 1)], rf1, u[mt], 0, 0, 0);
-                }
-                if (w == 0) {
-                    sUf[b][0][lane] = pack_bf16(u[0], u[1]);
-                    sUf[b][1][lane] = pack_bf16(u[2], u[3]);
-                }
-                floatx4 du[4];
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) du[mt] = u[mt] * *reinterpret_cast<const floatx4*>(&sDec[b][16 * mt + 4 * lg]);
-                const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
-                // S^T <- gamma_n S^T + K^T (D U) on this wave's key tiles
-                const float gn = sGam[b][CH - 1];
-#pragma unroll
-                for (int m = 0; m < HMD; ++m) {
-                    const int md = w * HMD + m;
-                    acc[m] *= gn;
-#pragma unroll
-                    for (int kk = 0; kk < 2; ++kk) {
-                        const bf16_t* p0 = &sK[b][32 * kk + 4 * lg + (l16 >> 2)][16 * md + 4 * (l16 & 3)];
-                        acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(join4(lds_tr8(p0), lds_tr8(p0 + 16 * LDK)),
-                                                                         kk ? df1 : df0, acc[m], 0, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (int f = 0; f < NFRAG; ++f) tf[f] = tfn[f];
-            } else {
-                __syncthreads();   // A (no chunk left)
+            for (int k2 = 0; k2 < HKD; ++k2) {
+                sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
+                sSf[w * HKD + k2][lane] = sf[k2];
             }
-            __syncthreads();   // B
+            floatx4 x[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][0], sf[0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+#pragma unroll
+                for (int k2 = 1; k2 < HKD; ++k2)
+                    x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][k2], sf[k2], x[mt], 0, 0, 0);
+                sXp[w][mt][lane] = x[mt];
+            }
+            // operands of the rest of the step, read while the partials are exchanged
+            bf16x8 wf[NFRAG], ka[HMD][2];
+            short4v vv[4];
+            floatx4 gm[4];
+#pragma unroll
+            for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                vv[mt] = lds_tr8(&sV[b][offV[mt]]);
+                gm[mt] = *reinterpret_cast<const floatx4*>(&sG[b][16 * mt + 4 * lg]);
+            }
+            const float gn = sG[b][CH - 1];
+#pragma unroll
+            for (int m = 0; m < HMD; ++m)
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) ka[m][kk] = join4(lds_tr8(K + offT[m][kk][0]), lds_tr8(K + offT[m][kk][1]));
+            lds_barrier();   // A: partials visible
+            // R' = V - diag(gamma) X
+            floatx4 rr[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                x[mt] += sXp[1 - w][mt][lane];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) rr[mt][e] = bf(vv[mt][e]) - gm[mt][e] * x[mt][e];
+            }
+            const bf16x8 rf0 = pack_bf16(rr[0], rr[1]), rf1 = pack_bf16(rr[2], rr[3]);
+            if (w == 0) {
+                sRf[0][lane] = rf0;
+                sRf[1][lane] = rf1;
+            }
+            lds_barrier();   // C: R' fragments visible
+            // D U = (diag(D) T diag(beta)) R'; lower triangular: tile mt needs blocks 0..mt/2
+            floatx4 du[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 0)], rf0, floatx4{0.f, 0.f, 0.f, 0.f},
+                                                                 0, 0, 0);
+                if (mt >= 2) du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 1)], rf1, du[mt], 0, 0, 0);
+            }
+            const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
+            // S^T <- gamma_n S^T + K^T (D U) on this wave's key tiles
+#pragma unroll
+            for (int m = 0; m < HMD; ++m) {
+                acc[m] *= gn;
+                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
+                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
+            }
+            lds_barrier();   // B
+        };
+        lds_barrier();   // prologue
+        for (int c = 0; c < nc; c += RING) {
+            cstep(Ic<0>{});
+            if (c + 1 < nc) cstep(Ic<1>{});
+            if (c + 2 < nc) cstep(Ic<2>{});
         }
         if (p.ST) {
 #pragma unroll
             for (int m = 0; m < HMD; ++m)
-                *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + 16 * (w * HMD + m) + 4 * lg) = acc[m];
+                *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
         }
     } else {
-        // ------------------------------------------------ output + staging waves
-        const int t = tid - 128, ow = wave - 2;
-        Stage st;
-        if (nc > 0) {
-            stage_load(0, st, t);
-            stage_store(0, st, t);
-        }
-        bf16x8 qf[2][NKD], qfn[2][NKD], pf[2][2], pfn[2][2];
-        __syncthreads();   // prologue staging visible
-        for (int c = 0; c <= nc; ++c) {
-            if (c + 1 < nc) stage_load(c + 1, st, t);
-            if (c < nc) {   // Q and P fragments of chunk c, used next iteration
-                const long t0 = tok0(c);
-                const int n = rows(c);
+        // ------------------------------------------------ output waves
+        const int ow = wave - 2;
+        bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
+        int offQ[2][NKD];
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int mt = 2 * ow + i, row = 16 * mt + l16;
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-                    for (int kk = 0; kk < NKD; ++kk) {
-                        short4v a = {0, 0, 0, 0}, bq = {0, 0, 0, 0};
-                        if (row < n) {
-                            const bf16_t* qp = gq + ((t0 + row) * H + h) * (long)DK + 32 * kk + 4 * lg;
-                            a = gld8(qp);
-                            bq = gld8(qp + 16);
-                        }
-                        qfn[i][kk] = join4(a, bq);
-                    }
-#pragma unroll
-                    for (int kk = 0; kk < 2; ++kk)
-                        if (kk <= mt / 2)
-                            pfn[i][kk] = *reinterpret_cast<const bf16x8*>(wsP + slot(c) * tp_elems<bf16_t>() +
-                                                                          (frag_id(mt, kk) * 64 + lane) * 8);
-                }
-            }
-            floatx4 gm[2];
-            if (c >= 1) {
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    gm[i] = *reinterpret_cast<const floatx4*>(&sGam[(c - 1) & 1][16 * (2 * ow + i) + 4 * lg]);
-            }
-            __syncthreads();   // A
-            if (c >= 1) {
-                const int cp = c - 1, bp = cp & 1;
-                const long t0 = tok0(cp);
-                const int n = rows(cp);
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int mt = 2 * ow + i;
-                    floatx4 oq = {0.f, 0.f, 0.f, 0.f}, op = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int kk = 0; kk < NKD; ++kk)
-                        oq = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[i][kk], sSf[bp][kk][lane], oq, 0, 0, 0);
-#pragma unroll
-                    for (int kk = 0; kk < 2; ++kk)
-                        if (kk <= mt / 2)
-                            op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[i][kk], sUf[bp][kk][lane], op, 0, 0, 0);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int rr = 16 * mt + 4 * lg + e;
-                        if (rr < n)
-                            go[((t0 + rr) * H + h) * (long)DV + js * SL + l16] =
-                                from_f<bf16_t>(p.scale * (gm[i][e] * oq[e] + op[e]));
-                    }
-                }
-            }
-            if (c + 1 < nc) stage_store((c + 1) & 1, st, t);
+            for (int kk = 0; kk < NKD; ++kk) offQ[i][kk] = kq(16 * (2 * ow + i) + l16, 32 * kk + 8 * lg);
+        auto ostep = [&](int c, auto SLOT) {
+            constexpr int b = decltype(SLOT)::value;
+            const int n = rows(c);
+            bf16x8 qa[2][NKD], pf[2][2];
+            float gm[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
+                const int mt = 2 * ow + i;
 #pragma unroll
-                for (int kk = 0; kk < NKD; ++kk) qf[i][kk] = qfn[i][kk];
+                for (int kk = 0; kk < NKD; ++kk) qa[i][kk] = *reinterpret_cast<const bf16x8*>(sQ[b] + offQ[i][kk]);
 #pragma unroll
-                for (int kk = 0; kk < 2; ++kk) pf[i][kk] = pfn[i][kk];
+                for (int kk = 0; kk < 2; ++kk) pf[i][kk] = sP[b][frag_id(mt, mt >= 2 ? kk : 0)][lane];
+                gm[i] = sG[b][16 * mt + l16];
             }
-            __syncthreads();   // B
+            lds_barrier();   // A: S fragments visible
+            floatx4 oq[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                oq[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kk = 0; kk < NKD; ++kk)
+                    oq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sSf[kk][lane], qa[i][kk], oq[i], 0, 0, 0);
+            }
+            lds_barrier();   // C: R' fragments visible
+            const bf16x8 rf0 = sRf[0][lane], rf1 = sRf[1][lane];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int mt = 2 * ow + i, tok = 16 * mt + l16;
+                floatx4 op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf0, pf[i][0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                if (mt >= 2) op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pf[i][1], op, 0, 0, 0);
+                const floatx4 ov = p.scale * (gm[i] * oq[i] + op);   // value channels 4 lg .. 4 lg + 3 of token tok
+                if (tok < n)
+                    *reinterpret_cast<bf16x4*>(go + ((tok0(c) + tok) * H + h) * (long)DV + js * SL + 4 * lg) =
+                        __builtin_convertvector(ov, bf16x4);
+            }
+            lds_barrier();   // B
+        };
+        lds_barrier();   // prologue
+        for (int c = 0; c < nc; c += RING) {
+            ostep(c, Ic<0>{});
+            if (c + 1 < nc) ostep(c + 1, Ic<1>{});
+            if (c + 2 < nc) ostep(c + 2, Ic<2>{});
         }
+    }
+}
+
+// ------------------------------------------------------------------ bf16 chunk terms
+// One workgroup (4 waves) per (chunk slot, head), bf16 io.  Produces, for the
+// state chain: gamma_r and exp(G_n - G_r), and in MFMA fragment order
+// (frag_row / frag_col) the two lower-triangular matrices
+//     W_D = diag(D) T diag(beta)     and     P_T = P T diag(beta),
+// T = (I + A)^{-1}.  K and Q arrive through buffer loads to LDS (rows past the
+// chunk read as zero); the in-chunk prefix sums are kept in fp64 and in log2
+// units, so every decay factor is one exp2 of an fp64 difference.  The four
+// diagonal 16x16 blocks of T are inverted together by one wave (lane = 16 block
+// + column); the off-diagonal blocks follow by fp32 MFMA block products.
+// P_T is formed transposed, (T^T P^T), with bf16 MFMA whose T^T operand comes
+// from LDS transpose reads of a bf16 copy of T, so each P_T fragment is packed
+// straight from the accumulators.  LDS stays under 64 KB (two workgroups per
+// CU): the K/Q tiles' space is reused for T once the products are formed.
+template <int DK>
+__global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
+    constexpr int NCH = DK / 8;     // 16-byte chunks per K/Q row
+    constexpr int RPI = 64 / NCH;   // rows per 1 KB buffer load
+    constexpr int NKD = DK / 32;    // MFMA contraction blocks over the key channels
+    constexpr int R0 = (2 * CH * DK * 2 > CH * (CH + 4) * 4 + CH * (CH + 8) * 2) ? 2 * CH * DK * 2
+                                                                                 : CH * (CH + 4) * 4 + CH * (CH + 8) * 2;
+    const int H = p.H;
+    const int gc = blockIdx.x / H, h = blockIdx.x % H;
+    int s;
+    if (p.ragged) {
+        if (gc >= p.chunk_off[p.n_seq]) return;
+        int lo = 0, hi = p.n_seq;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (p.chunk_off[mid] <= gc) lo = mid; else hi = mid;
+        }
+        s = lo;
+    } else {
+        s = gc / p.NC;
+    }
+    long start;
+    int len, cbase;
+    seq_info(p, s, start, len, cbase);
+    const int c = gc - cbase;
+    const long t0 = start + (long)c * CH;
+    const int n = min(CH, len - c * CH);
+    const long slot = (long)gc * H + h;
+
+    __shared__ __attribute__((aligned(16))) char r0[R0];
+    __shared__ __attribute__((aligned(16))) float sA[CH][CH + 4];
+    __shared__ __attribute__((aligned(16))) bf16_t sPb[CH][CH + 8];
+    __shared__ float sZ[4][16][17];
+    __shared__ double sGl[CH];
+    __shared__ __attribute__((aligned(16))) float sB[CH];
+    __shared__ __attribute__((aligned(16))) float sD[CH];
+    bf16_t* sK = reinterpret_cast<bf16_t*>(r0);
+    bf16_t* sQ = sK + CH * DK;
+    float(*sTi)[CH + 4] = reinterpret_cast<float(*)[CH + 4]>(r0);
+    bf16_t(*sTb)[CH + 8] = reinterpret_cast<bf16_t(*)[CH + 8]>(r0 + CH * (CH + 4) * 4);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, lg = lane >> 4;
+    auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
+    auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
+
+    {   // K and Q tiles straight into LDS; loads i = wave, wave + 4, ...
+        const long row0 = t0 * H + h;
+        const uint32_t bytes = (uint32_t)(((long)(n - 1) * H + 1) * DK * 2);
+        const auto rk = rsrc(reinterpret_cast<const bf16_t*>(p.k) + row0 * DK, bytes);
+        const auto rq = rsrc(reinterpret_cast<const bf16_t*>(p.q) + row0 * DK, bytes);
+        for (int i = wave; i < NCH; i += 4) {
+            const int r = RPI * i + lane / NCH;
+            const int off = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+            bdma16(rk, sK + RPI * i * DK, off);
+            bdma16(rq, sQ + RPI * i * DK, off);
+        }
+    }
+    if (wave == 0) {
+        // prefix sums of g in log2 units, fp64; padded rows: no decay, no write
+        const float gv = lane < n ? p.g[(t0 + lane) * H + h] : 0.f;
+        const float bv = lane < n ? p.beta[(t0 + lane) * H + h] : 0.f;
+        double x = (double)gv * 1.4426950408889634;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const double y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        const double xn = __shfl(x, 63, 64);
+        const float dec = __builtin_amdgcn_exp2f((float)(xn - x));
+        sGl[lane] = x;
+        sB[lane] = bv;
+        sD[lane] = dec;
+        p.wsG[slot * 2 * CH + lane] = __builtin_amdgcn_exp2f((float)x);
+        p.wsG[slot * 2 * CH + CH + lane] = dec;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+
+    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P); the 6 upper
+    // blocks of P are zero
+    for (int job = wave; job < 26; job += 4) {
+        if (job >= 20) {
+            int t = job - 20, bj = 1;   // upper block (bi, bj), bi < bj
+            while (t >= bj) { t -= bj; ++bj; }
+            const int bi = t;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sPb[16 * bi + 4 * lg + e][16 * bj + l16] = 0;
+            continue;
+        }
+        const int which = job / 10;
+        int t = job % 10, bi = 0;
+        while (t > bi) { t -= bi + 1; ++bi; }
+        const int bj = t;
+        const bf16_t* X = which ? sQ : sK;
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(X + kq(16 * bi + l16, 32 * kk + 8 * lg));
+            const bf16x8 b = *reinterpret_cast<const bf16x8*>(sK + kq(16 * bj + l16, 32 * kk + 8 * lg));
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+        }
+        const int i = 16 * bj + l16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = 16 * bi + 4 * lg + e;
+            const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - sGl[i]));
+            if (which == 0) sA[r][i] = (r > i) ? sB[r] * gam * acc[e] : 0.f;
+            else sPb[r][i] = from_f<bf16_t>((r >= i) ? gam * acc[e] : 0.f);
+        }
+    }
+    __syncthreads();
+
+    // T = (I + A)^{-1}: diagonal blocks by forward substitution, one wave, lane =
+    // 16 * block + column; meanwhile the other waves clear T's upper blocks
+    if (wave == 0) {
+        const int b = lg;
+        float x[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float acc = (r == l16) ? 1.f : 0.f;
+#pragma unroll
+            for (int i = 0; i < r; ++i) acc -= sA[16 * b + r][16 * b + i] * x[i];
+            x[r] = acc;
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sTi[16 * b + r][16 * b + l16] = x[r];
+    } else {
+        for (int i = tid - 64; i < 6 * 256; i += NT - 64) {
+            int t = i / 256, bj = 1;
+            while (t >= bj) { t -= bj; ++bj; }
+            const int bi = t, e = i % 256;
+            sTi[16 * bi + e / 16][16 * bj + e % 16] = 0.f;
+        }
+    }
+    __syncthreads();
+    for (int b = 1; b < 4; ++b) {   // block row b: T_bj = -T_bb sum_{j <= m < b} A_bm T_mj
+        if (wave < b) {
+            const int j = wave;
+            floatx4 z = {0.f, 0.f, 0.f, 0.f};
+            for (int m = j; m < b; ++m) {
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk)
+                    z = __builtin_amdgcn_mfma_f32_16x16x4f32(sA[16 * b + l16][16 * m + 4 * kk + lg],
+                                                             sTi[16 * m + 4 * kk + lg][16 * j + l16], z, 0, 0, 0);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sZ[wave][4 * lg + e][l16] = z[e];
+            __builtin_amdgcn_wave_barrier();   // LDS ops of one wave complete in order
+            floatx4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                t = __builtin_amdgcn_mfma_f32_16x16x4f32(sTi[16 * b + l16][16 * b + 4 * kk + lg],
+                                                         sZ[wave][4 * kk + lg][l16], t, 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sTi[16 * b + 4 * lg + e][16 * j + l16] = -t[e];
+        }
+        __syncthreads();
+    }
+    for (int i = tid; i < CH * CH / 4; i += NT) {   // bf16 copy of T
+        const int r = i / (CH / 4), c4 = 4 * (i % (CH / 4));
+        const floatx4 v = *reinterpret_cast<const floatx4*>(&sTi[r][c4]);
+        *reinterpret_cast<bf16x4*>(&sTb[r][c4]) = __builtin_convertvector(v, bf16x4);
+    }
+    __syncthreads();
+
+    bf16_t* Wg = reinterpret_cast<bf16_t*>(p.wsT) + slot * tp_elems<bf16_t>();
+    bf16_t* Pg = reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>();
+    for (int f = wave; f < NFRAG; f += 4) {
+        const int mt = frag_mt(f), kk2 = frag_kk(f), r = 16 * mt + l16;
+        // W_D fragment: D_r T[r][tau] beta_tau
+        const float dr = sD[r];
+        const floatx4 b0 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 4 * lg]);
+        const floatx4 b1 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 16 + 4 * lg]);
+        const floatx4 w0 = dr * b0 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 4 * lg]);
+        const floatx4 w1 = dr * b1 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 16 + 4 * lg]);
+        *reinterpret_cast<bf16x8*>(Wg + (f * 64 + lane) * 8) = pack_bf16(w0, w1);
+        // P_T fragment from (T^T P^T) tiles (tau block 2 kk2 + hb, token block mt)
+        floatx4 pt[2];
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+            const int bt = 2 * kk2 + hb;
+            pt[hb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (bt > mt) continue;   // above the diagonal: zero
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const bf16_t* t0p = &sTb[32 * kk + 8 * lg + (l16 >> 2)][16 * bt + 4 * (l16 & 3)];
+                const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 4 * (CH + 8)));
+                const bf16x8 bb = *reinterpret_cast<const bf16x8*>(&sPb[16 * mt + l16][32 * kk + 8 * lg]);
+                pt[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb, pt[hb], 0, 0, 0);
+            }
+            pt[hb] *= hb ? b1 : b0;
+        }
+        *reinterpret_cast<bf16x8*>(Pg + (f * 64 + lane) * 8) = pack_bf16(pt[0], pt[1]);
     }
 }
 
@@ -882,11 +1164,15 @@ void launch_prefill(const Params& p, long slots, hipStream_t st) {
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(64), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
                            p.seq_len, p.chunk_off);
-    if (slots > 0 && p.T > 0)
-        hipLaunchKernelGGL((k_chunk_terms<IO, DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+    if (slots > 0 && p.T > 0) {
+        if (sizeof(IO) == 2)
+            hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+        else
+            hipLaunchKernelGGL((k_chunk_terms<IO, DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+    }
     const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
     if (sizeof(IO) == 2)
-        hipLaunchKernelGGL((k_state_chain_bf16<DK>), grid, dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p);
     else
         hipLaunchKernelGGL((k_state_chain<IO, DK>), grid, dim3(NT), 0, st, p);
 }
@@ -962,6 +1248,8 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     const int n_seq = n_seqs > 0 ? n_seqs : B;
     if ((long)n_seq * H * (dv / SL) > (1L << 30)) return fail(GDN_ERR_UNSUPPORTED, "too many sequences x heads");
     if ((long)B * T * H > (1L << 40)) return fail(GDN_ERR_UNSUPPORTED, "B*T*H too large");
+    if ((long)H * (dk > dv ? dk : dv) > (1L << 24))   // 32-bit in-chunk offsets of 64 rows
+        return fail(GDN_ERR_UNSUPPORTED, "H=%d too large", H);
     Layout L;
     if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L))
         return fail(GDN_ERR_UNSUPPORTED, "too many chunks x heads for one call");

@@ -78,6 +78,7 @@ def _prefill(L, **kw):
     (dict(dk=96), UNSUPPORTED),
     (dict(dv=256), UNSUPPORTED),
     (dict(dk=32, dv=32), UNSUPPORTED),
+    (dict(H=1 << 19), UNSUPPORTED),
     (dict(chunk=0), INVALID),
     (dict(chunk=32), UNSUPPORTED),
     (dict(chunk=128), UNSUPPORTED),
