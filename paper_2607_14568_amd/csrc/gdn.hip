@@ -539,25 +539,29 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
 //  waves 2,3 ("output"): O^T = scale (S Q^T diag(gamma) + R'^T (P T diag(beta))^T)
 //    for one half of the chunk's tokens -- the operands of the O products
 //    swapped, so a lane ends up with 4 consecutive value channels of one token
-//    and writes them with one 8-byte store.
-//  wave 4 ("loader"): copies chunk c+2 (K, Q, both chunk matrices, the V slice,
-//    gamma) from global memory straight into a 3-deep LDS ring with buffer
-//    loads to LDS.  Per chunk, the buffer descriptors end at row n-1 of the
-//    head, so the rows of a partial chunk read back as zeros.  It waits for
-//    chunk c+1 before the end of chunk c; the other waves issue no global
-//    loads, so nothing they do waits on memory.
-// K and Q rows sit in LDS with their 16-byte chunks XOR-swizzled by row, which
-// keeps both the row reads (16 rows, one chunk) and the transpose reads
-// (4 rows, 4 chunks) free of bank conflicts.
-// Three barriers per chunk: X partials ready (A), R' ready (C), end of chunk (B);
-// they order LDS traffic only, so global loads and stores stay in flight.
+//    and writes them with one 8-byte store.  Their Q fragments come straight
+//    from global memory one chunk ahead (buffer loads; a descriptor that ends
+//    at row n-1 of the head makes the rows of a partial chunk read as zeros).
+//  wave 4 ("loader"): copies chunk c+3 (K, both chunk matrices, the V slice,
+//    gamma) from global memory straight into a 4-deep LDS ring with buffer
+//    loads to LDS, with the same per-chunk descriptors.  The chain waves issue
+//    no global loads, so nothing they do waits on memory.
+// K rows sit in LDS with their 16-byte chunks XOR-swizzled by row, which keeps
+// both the row reads (16 rows, one chunk) and the transpose reads (4 rows,
+// 4 chunks) free of bank conflicts.
+// One barrier per chunk, between the X partials and their sum.  It also orders
+// the ring: after barrier c every wave is done with chunk c-1, so the loader
+// refills that slot, and chunk c+1 was waited for before it.  The chain hands
+// R' to the output waves through an LDS flag (the chunk count) that they poll;
+// the exchange buffers alternate by chunk parity.  Barriers order LDS traffic
+// only, so global loads and stores stay in flight across them.
 // The chunk loop is unrolled by the ring depth so ring slots are constants.
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short short4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 constexpr int NT_CHAIN = 320;
-constexpr int RING = 3;
+constexpr int RING = 4;
 template <int N> struct Ic { static constexpr int value = N; };
 
 __device__ __forceinline__ bf16x8 pack_bf16(floatx4 a, floatx4 b) {
@@ -596,9 +600,9 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
     constexpr int HKD = NKD / 2;        // ... per chain wave
     constexpr int HMD = DK / 32;        // 16-row S^T tiles per chain wave
-    constexpr int NCH = DK / 8;         // 16-byte chunks per K/Q row
+    constexpr int NCH = DK / 8;         // 16-byte chunks per K row
     constexpr int RPI = 64 / NCH;       // rows per 1 KB direct load
-    constexpr int NISSUE = 2 * NCH + 2 * NFRAG + 2 + 1;   // direct loads per chunk
+    constexpr int NISSUE = NCH + 2 * NFRAG + 2 + 1;   // direct loads per chunk
     const int H = p.H, DV = p.DV;
     // Slices of one (sequence, head) are blockIdx values congruent modulo the
     // number of (sequence, head) pairs, so with 8 | n_seq*H they share an XCD
@@ -613,15 +617,17 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
 
+    // ring of chunk inputs (slot = chunk % RING)
     __shared__ __attribute__((aligned(16))) bf16_t sK[RING][CH * DK];
-    __shared__ __attribute__((aligned(16))) bf16_t sQ[RING][CH * DK];
     __shared__ __attribute__((aligned(16))) bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
     __shared__ __attribute__((aligned(16))) bf16x8 sP[RING][NFRAG][64];   // P T diag(beta)
     __shared__ __attribute__((aligned(16))) bf16_t sV[RING][CH * SL];
     __shared__ __attribute__((aligned(16))) float sG[RING][CH];           // gamma_r
-    __shared__ __attribute__((aligned(16))) floatx4 sXp[2][4][64];
-    __shared__ __attribute__((aligned(16))) bf16x8 sSf[NKD][64];
-    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][64];
+    // exchange buffers, double-buffered by chunk parity
+    __shared__ __attribute__((aligned(16))) floatx4 sXp[2][2][4][64];     // X partials
+    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];       // S fragments
+    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][2][64];         // R' fragments
+    __shared__ int sFlag;                                                  // chunks whose R' is in sRf
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -630,18 +636,17 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     auto tok0 = [&](int c) { return start + (long)c * CH; };
     auto slot = [&](int c) { return (long)(cbase + c) * H + h; };
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
-    // element offset of logical (row r, column cc) in a swizzled K/Q tile
+    // element offset of logical (row r, column cc) in a swizzled K tile
     auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
+    if (tid == 0) sFlag = 0;
 
     if (wave == 4) {
         // ------------------------------------------------ loader
         const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
-        const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
         const bf16_t* gv = reinterpret_cast<const bf16_t*>(p.v);
         const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
         const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
-        // loop-invariant byte offsets of this lane's loads within a chunk
-        int koff[NCH];
+        int koff[NCH];   // loop-invariant byte offsets of this lane's K loads within a chunk
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = RPI * i + lane / NCH;
@@ -650,20 +655,12 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
         int voff[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) voff[i] = ((32 * i + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
-        auto issue_kq = [&](int c, auto SLOT) {
+        auto issue = [&](int c, auto SLOT) {
             constexpr int sl = decltype(SLOT)::value;
-            const long row0 = tok0(c) * H + h;
-            const uint32_t bytes = (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2);
-            const auto rk = rsrc(gk + row0 * DK, bytes), rq = rsrc(gq + row0 * DK, bytes);
+            const long row0 = tok0(c) * H + h, sc = slot(c);
+            const auto rk = rsrc(gk + row0 * DK, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2));
 #pragma unroll
-            for (int i = 0; i < NCH; ++i) {
-                bdma16(rk, &sK[sl][RPI * i * DK], koff[i]);
-                bdma16(rq, &sQ[sl][RPI * i * DK], koff[i]);
-            }
-        };
-        auto issue_rest = [&](int c, auto SLOT) {
-            constexpr int sl = decltype(SLOT)::value;
-            const long sc = slot(c);
+            for (int i = 0; i < NCH; ++i) bdma16(rk, &sK[sl][RPI * i * DK], koff[i]);
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
             const auto rp = rsrc(wsP + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
@@ -671,34 +668,33 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                 bdma16(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
                 bdma16(rp, &sP[sl][f][0], (f * 64 + lane) * 16);
             }
-            const auto rv = rsrc(gv + (tok0(c) * H + h) * DV, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DV * 2));
+            const auto rv = rsrc(gv + row0 * DV, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DV * 2));
             bdma16(rv, &sV[sl][0], voff[0]);
             bdma16(rv, &sV[sl][32 * SL], voff[1]);
             bdma4(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
         };
+        // Chunk c+1 is read by the chain right after barrier c, so it must be
+        // resident before that barrier.  After barrier c every wave is past chunk
+        // c-1, whose slot is (c+3) % RING: chunk c+3 is loaded there, then the
+        // wait leaves only those loads in flight (chunk c+2 has landed).
         auto lstep = [&](int c, auto SLOT) {
-            constexpr int bn = (decltype(SLOT)::value + 2) % RING;
-            const int cn = min(c + 2, nc - 1);
-            issue_kq(cn, Ic<bn>{});
-            lds_barrier();   // A
-            issue_rest(cn, Ic<bn>{});
-            lds_barrier();   // C
-            // all but this chunk's own loads have landed: chunk c+1 is resident
+            constexpr int bn = (decltype(SLOT)::value + 3) % RING;
+            lds_barrier();
+            issue(min(c + 3, nc - 1), Ic<bn>{});
             asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NISSUE) : "memory");
-            lds_barrier();   // B
         };
         if (nc > 0) {
-            issue_kq(0, Ic<0>{});
-            issue_rest(0, Ic<0>{});
-            issue_kq(min(1, nc - 1), Ic<1>{});
-            issue_rest(min(1, nc - 1), Ic<1>{});
+            issue(0, Ic<0>{});
+            issue(min(1, nc - 1), Ic<1>{});
+            issue(min(2, nc - 1), Ic<2>{});
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        lds_barrier();   // prologue: chunks 0 and 1 resident
+        lds_barrier();   // prologue: chunks 0, 1 and 2 resident
         for (int c = 0; c < nc; c += RING) {
             lstep(c, Ic<0>{});
             if (c + 1 < nc) lstep(c + 1, Ic<1>{});
             if (c + 2 < nc) lstep(c + 2, Ic<2>{});
+            if (c + 3 < nc) lstep(c + 3, Ic<3>{});
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     } else if (wave < 2) {
@@ -711,8 +707,7 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
             acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
             if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(w * HMD + m));
         }
-        // loop-invariant LDS offsets of this lane's operands
-        int offX[4][HKD], offT[HMD][2][2], offV[4];
+        int offX[4][HKD], offT[HMD][2][2], offV[4];   // loop-invariant LDS offsets of this lane's operands
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll
@@ -729,34 +724,17 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                     offT[m][kk][h2] = kq(32 * kk + 16 * h2 + 4 * lg + (l16 >> 2),
                                          32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1));
         }
-        auto cstep = [&](auto SLOT) {
-            constexpr int b = decltype(SLOT)::value;
+        auto cstep = [&](int c, auto SLOT) {
+            constexpr int b = decltype(SLOT)::value, x2 = b & 1;
             const bf16_t* K = sK[b];
-            bf16x8 xa[4][HKD];
+            // every LDS operand of the chunk is read first
+            bf16x8 xa[4][HKD], wf[NFRAG], ka[HMD][2];
+            short4v vv[4];
+            floatx4 gm[4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
                 for (int k2 = 0; k2 < HKD; ++k2) xa[mt][k2] = *reinterpret_cast<const bf16x8*>(K + offX[mt][k2]);
-            // S fragments of this wave's key blocks; partial X = K S^T
-            bf16x8 sf[HKD];
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) {
-                sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
-                sSf[w * HKD + k2][lane] = sf[k2];
-            }
-            floatx4 x[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][0], sf[0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-#pragma unroll
-                for (int k2 = 1; k2 < HKD; ++k2)
-                    x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][k2], sf[k2], x[mt], 0, 0, 0);
-                sXp[w][mt][lane] = x[mt];
-            }
-            // operands of the rest of the step, read while the partials are exchanged
-            bf16x8 wf[NFRAG], ka[HMD][2];
-            short4v vv[4];
-            floatx4 gm[4];
 #pragma unroll
             for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
 #pragma unroll
@@ -769,21 +747,40 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
             for (int m = 0; m < HMD; ++m)
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) ka[m][kk] = join4(lds_tr8(K + offT[m][kk][0]), lds_tr8(K + offT[m][kk][1]));
-            lds_barrier();   // A: partials visible
+            __builtin_amdgcn_sched_barrier(0);
+            // S fragments of this wave's key blocks; partial X = K S^T
+            bf16x8 sf[HKD];
+#pragma unroll
+            for (int k2 = 0; k2 < HKD; ++k2) {
+                sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
+                sSf[x2][w * HKD + k2][lane] = sf[k2];
+            }
+            floatx4 x[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][0], sf[0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+#pragma unroll
+                for (int k2 = 1; k2 < HKD; ++k2)
+                    x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][k2], sf[k2], x[mt], 0, 0, 0);
+                sXp[x2][w][mt][lane] = x[mt];
+            }
+            lds_barrier();   // the chunk's one barrier: both partials (and S fragments) visible
             // R' = V - diag(gamma) X
             floatx4 rr[4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
-                x[mt] += sXp[1 - w][mt][lane];
+                x[mt] += sXp[x2][1 - w][mt][lane];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) rr[mt][e] = bf(vv[mt][e]) - gm[mt][e] * x[mt][e];
             }
             const bf16x8 rf0 = pack_bf16(rr[0], rr[1]), rf1 = pack_bf16(rr[2], rr[3]);
             if (w == 0) {
-                sRf[0][lane] = rf0;
-                sRf[1][lane] = rf1;
+                sRf[x2][0][lane] = rf0;
+                sRf[x2][1][lane] = rf1;
+                // publish: the R' fragments of chunk c are written before the flag moves
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                if (lane == 0) __hip_atomic_store(&sFlag, c + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
-            lds_barrier();   // C: R' fragments visible
             // D U = (diag(D) T diag(beta)) R'; lower triangular: tile mt needs blocks 0..mt/2
             floatx4 du[4];
 #pragma unroll
@@ -800,13 +797,13 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
             }
-            lds_barrier();   // B
         };
         lds_barrier();   // prologue
         for (int c = 0; c < nc; c += RING) {
-            cstep(Ic<0>{});
-            if (c + 1 < nc) cstep(Ic<1>{});
-            if (c + 2 < nc) cstep(Ic<2>{});
+            cstep(c, Ic<0>{});
+            if (c + 1 < nc) cstep(c + 1, Ic<1>{});
+            if (c + 2 < nc) cstep(c + 2, Ic<2>{});
+            if (c + 3 < nc) cstep(c + 3, Ic<3>{});
         }
         if (p.ST) {
 #pragma unroll
@@ -816,37 +813,53 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     } else {
         // ------------------------------------------------ output waves
         const int ow = wave - 2;
+        const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
         bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
-        int offQ[2][NKD];
+        typedef int int4v __attribute__((ext_vector_type(4)));
+        int qoff[2][NKD];   // byte offsets of this lane's Q fragments within a chunk
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int kk = 0; kk < NKD; ++kk) offQ[i][kk] = kq(16 * (2 * ow + i) + l16, 32 * kk + 8 * lg);
-        auto ostep = [&](int c, auto SLOT) {
-            constexpr int b = decltype(SLOT)::value;
+            for (int kk = 0; kk < NKD; ++kk) qoff[i][kk] = ((16 * (2 * ow + i) + l16) * H * DK + 32 * kk + 8 * lg) * 2;
+        // Q fragments come straight from global memory, one chunk ahead (rows past
+        // the chunk fall outside the descriptor and read as zeros)
+        auto load_q = [&](int c, bf16x8(&qa)[2][NKD]) {
+            const auto rq = rsrc(gq + (tok0(c) * H + h) * DK, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2));
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int kk = 0; kk < NKD; ++kk)
+                    qa[i][kk] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, qoff[i][kk], 0, 0));
+        };
+        auto ostep = [&](int c, auto SLOT, bf16x8(&qa)[2][NKD], bf16x8(&qn)[2][NKD]) {
+            constexpr int b = decltype(SLOT)::value, x2 = b & 1;
             const int n = rows(c);
-            bf16x8 qa[2][NKD], pf[2][2];
+            lds_barrier();   // the chunk's barrier: S fragments of chunk c visible
+            load_q(min(c + 1, nc - 1), qn);
+            bf16x8 pf[2][2];
             float gm[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int mt = 2 * ow + i;
 #pragma unroll
-                for (int kk = 0; kk < NKD; ++kk) qa[i][kk] = *reinterpret_cast<const bf16x8*>(sQ[b] + offQ[i][kk]);
-#pragma unroll
                 for (int kk = 0; kk < 2; ++kk) pf[i][kk] = sP[b][frag_id(mt, mt >= 2 ? kk : 0)][lane];
                 gm[i] = sG[b][16 * mt + l16];
             }
-            lds_barrier();   // A: S fragments visible
             floatx4 oq[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 oq[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < NKD; ++kk)
-                    oq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sSf[kk][lane], qa[i][kk], oq[i], 0, 0, 0);
+                    oq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sSf[x2][kk][lane], qa[i][kk], oq[i], 0, 0, 0);
             }
-            lds_barrier();   // C: R' fragments visible
-            const bf16x8 rf0 = sRf[0][lane], rf1 = sRf[1][lane];
+            // wait (bounded) until the chain has published R' of chunk c
+            for (int spin = 0; spin < (1 << 22); ++spin) {
+                if (__hip_atomic_load(&sFlag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) > c) break;
+                __builtin_amdgcn_s_sleep(1);
+            }
+            asm volatile("" ::: "memory");
+            const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int mt = 2 * ow + i, tok = 16 * mt + l16;
@@ -857,13 +870,15 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                     *reinterpret_cast<bf16x4*>(go + ((tok0(c) + tok) * H + h) * (long)DV + js * SL + 4 * lg) =
                         __builtin_convertvector(ov, bf16x4);
             }
-            lds_barrier();   // B
         };
+        bf16x8 qA[2][NKD], qB[2][NKD];
+        if (nc > 0) load_q(0, qA);
         lds_barrier();   // prologue
-        for (int c = 0; c < nc; c += RING) {
-            ostep(c, Ic<0>{});
-            if (c + 1 < nc) ostep(c + 1, Ic<1>{});
-            if (c + 2 < nc) ostep(c + 2, Ic<2>{});
+        for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and Q buffer are both constants
+            ostep(c, Ic<0>{}, qA, qB);
+            if (c + 1 < nc) ostep(c + 1, Ic<1>{}, qB, qA);
+            if (c + 2 < nc) ostep(c + 2, Ic<2>{}, qA, qB);
+            if (c + 3 < nc) ostep(c + 3, Ic<3>{}, qB, qA);
         }
     }
 }
