@@ -102,6 +102,7 @@ template <> struct Mma<float> {
 // element e of lane group l/16 is token 32*kk + 16*(e/4) + 4*(l/16) + e%4 --
 // exactly the rows an MFMA accumulator tile pair holds in that lane.
 constexpr int NFRAG = 6;
+constexpr int NBF = 8;    // fragments of the full 64x64 cross-chunk matrix (4 row tiles x 2 blocks)
 __host__ __device__ constexpr int frag_id(int mt, int kk) { return mt < 2 ? mt : 2 + 2 * (mt - 2) + kk; }
 __device__ __forceinline__ int frag_mt(int f) { return f < 2 ? f : 2 + ((f - 2) >> 1); }
 __device__ __forceinline__ int frag_kk(int f) { return f < 2 ? 0 : ((f - 2) & 1); }
@@ -134,6 +135,7 @@ struct Params {
     float* wsG;          // [slot][H][128]: gamma_r = exp(G_r), then exp(G_n - G_r)
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
+    void* wsB;           // bf16 io: [slot][H][NBF fragments] of K_{c+1} K_c^T W_c
     float scale;
 };
 
@@ -520,47 +522,53 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
 }
 
 // ------------------------------------------------------------------ bf16 state chain
-// One workgroup of 5 waves per (sequence, head, 16-row slice of S), bf16 io.
-//  waves 0,1 ("chain"): wave w keeps S^T rows of key-channel tiles
-//    [NMD/2 w, NMD/2 (w+1)) of the slice as fp32 MFMA accumulators.  Per chunk:
-//    partial X = K S^T over its key channels, one LDS exchange of the partials,
-//    R' = V - diag(gamma) X, D U = (diag(D) T diag(beta)) R', and
-//    S^T <- gamma_n S^T + K^T (D U) for its tiles (beta and D are folded into
-//    the matrix by the chunk-terms kernel).  Every B operand (S, R', D U) is
-//    packed from the lane's own accumulators; the A operands are read in the
-//    matching contraction order:
+// One workgroup of 8 waves per (sequence, head, 16-row slice of S), bf16 io.
+// Write S_c for the state entering chunk c, X_c = K_c S_c^T and
+// R'_c = V_c - diag(gamma_c) X_c.  The chunk recurrence
+// S_{c+1}^T = gamma_n S_c^T + K_c^T W_c R'_c (W_c = diag(D) T diag(beta)) gives
+//     X_{c+1} = gamma_n K_{c+1} S_c^T + B_c R'_c,     B_c = K_{c+1} K_c^T W_c,
+// so the next chunk's R' needs only S_c and R'_c, and its product runs beside
+// the state update instead of after it.
+//  waves 0,1 ("chain"): wave w keeps the S^T rows of key-channel tiles
+//    [NMD/2 w, NMD/2 (w+1)) as fp32 MFMA accumulators and the R' rows of token
+//    tiles 2w, 2w+1.  At barrier c the two waves swap their halves of S_c and
+//    R'_c (bf16 MFMA operands); then each forms X_{c+1} and R'_{c+1} for its
+//    token tiles, D U = W_c R'_c, and S^T <- gamma_n S^T + K_c^T (D U) for its
+//    key tiles.  Every B operand (S, R', D U) is packed from accumulators; the
+//    A operands are read in the matching contraction order:
 //      - token contractions: element e of lane group g in block kk is token
 //        32 kk + 16 (e/4) + 4 g + e%4 (the rows an accumulator tile pair holds);
 //      - key contractions: accumulator tile md, lane group g, element e holds
 //        key channel 32 (md/2) + 8 g + 4 (md%2) + e, so a lane's 8 contraction
 //        elements of block kk are the contiguous channels 32 kk + 8 g .. +7 and
 //        the K (and Q) operands are single 16-byte reads.  K^T comes from the
-//        same row-major K tile through LDS transpose reads.
-//  waves 2,3 ("output"): O^T = scale (S Q^T diag(gamma) + R'^T (P T diag(beta))^T)
-//    for one half of the chunk's tokens -- the operands of the O products
-//    swapped, so a lane ends up with 4 consecutive value channels of one token
-//    and writes them with one 8-byte store.  Their Q fragments come straight
-//    from global memory one chunk ahead (buffer loads; a descriptor that ends
-//    at row n-1 of the head makes the rows of a partial chunk read as zeros).
-//  wave 4 ("loader"): copies chunk c+3 (K, both chunk matrices, the V slice,
-//    gamma) from global memory straight into a 4-deep LDS ring with buffer
-//    loads to LDS, with the same per-chunk descriptors.  The chain waves issue
-//    no global loads, so nothing they do waits on memory.
-// K rows sit in LDS with their 16-byte chunks XOR-swizzled by row, which keeps
-// both the row reads (16 rows, one chunk) and the transpose reads (4 rows,
-// 4 chunks) free of bank conflicts.
-// One barrier per chunk, between the X partials and their sum.  It also orders
-// the ring: after barrier c every wave is done with chunk c-1, so the loader
-// refills that slot, and chunk c+1 was waited for before it.  The chain hands
-// R' to the output waves through an LDS flag (the chunk count) that they poll;
-// the exchange buffers alternate by chunk parity.  Barriers order LDS traffic
-// only, so global loads and stores stay in flight across them.
-// The chunk loop is unrolled by the ring depth so ring slots are constants.
+//        row-major K tile through LDS transpose reads.
+//  waves 2,3 ("output"): O_c^T = scale (S_c Q_c^T diag(gamma_c) + R'_c^T P'_c^T)
+//    for one half of the chunk's tokens, from the same exchanged S_c and R'_c --
+//    the operands swapped, so a lane ends up with 4 consecutive value channels
+//    of one token and writes them with one 8-byte store.  Each stages its Q rows
+//    in LDS one chunk ahead (buffer loads of whole cache lines: register loads
+//    in the MFMA layout would read 64-byte halves) and loads its P' fragments
+//    straight into registers.
+//  waves 4..7 ("loaders"): copy chunk c+3 (K, W, B, the V slice, gamma) into a
+//    4-deep LDS ring with buffer loads to LDS, each a quarter of the loads (one
+//    wave alone issues global loads at about a third of a CU's rate).
+// Global loads use per-chunk buffer descriptors that end at row n-1 of the
+// head, so the rows of a partial chunk read as zeros.  K rows sit in LDS with
+// their 16-byte chunks XOR-swizzled by row, which keeps the transpose reads
+// (4 rows, 4 chunks) free of bank conflicts.
+// One barrier per chunk, at its start: S_c and R'_c are complete (exchange
+// buffers alternate by chunk parity); every wave is done with chunk c-1, so
+// the loader refills that slot; chunk c+1, read during chunk c, was waited for
+// before it.  Barriers order LDS traffic only, so global loads and stores stay
+// in flight across them.  The chunk loop is unrolled by the ring depth so ring
+// slots are constants.
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short short4v __attribute__((ext_vector_type(4)));
+typedef int int4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
-constexpr int NT_CHAIN = 320;
+constexpr int NT_CHAIN = 512;
 constexpr int RING = 4;
 template <int N> struct Ic { static constexpr int value = N; };
 
@@ -572,6 +580,11 @@ __device__ __forceinline__ bf16x8 join4(short4v a, short4v b) {
     const short8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
     return __builtin_bit_cast(bf16x8, x);
 }
+// whole-register select (a runtime index into a register array would be
+// lowered element by element)
+__device__ __forceinline__ bf16x8 sel(bool c, bf16x8 a, bf16x8 b) {
+    return __builtin_bit_cast(bf16x8, c ? __builtin_bit_cast(int4v, a) : __builtin_bit_cast(int4v, b));
+}
 // Transpose read: within each 16-lane group, lane i element e receives element
 // i%4 of the 8 bytes addressed by lane 4e + i/4 of the group.
 __device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
@@ -582,6 +595,9 @@ __device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)
 // Buffer resource over [base, base + bytes); loads past the end return zeros.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+__device__ __forceinline__ bf16x8 bload16(__amdgpu_buffer_rsrc_t r, int voff) {
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
 }
 // global -> LDS without registers: lane l's 16 (4) bytes land at dst + 16 l (4 l)
 __device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
@@ -598,11 +614,10 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 template <int DK>
 __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
-    constexpr int HKD = NKD / 2;        // ... per chain wave
+    constexpr int HKD = NKD / 2;        // ... whose S^T rows one chain wave keeps
     constexpr int HMD = DK / 32;        // 16-row S^T tiles per chain wave
     constexpr int NCH = DK / 8;         // 16-byte chunks per K row
     constexpr int RPI = 64 / NCH;       // rows per 1 KB direct load
-    constexpr int NISSUE = NCH + 2 * NFRAG + 2 + 1;   // direct loads per chunk
     const int H = p.H, DV = p.DV;
     // Slices of one (sequence, head) are blockIdx values congruent modulo the
     // number of (sequence, head) pairs, so with 8 | n_seq*H they share an XCD
@@ -620,14 +635,13 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     // ring of chunk inputs (slot = chunk % RING)
     __shared__ __attribute__((aligned(16))) bf16_t sK[RING][CH * DK];
     __shared__ __attribute__((aligned(16))) bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
-    __shared__ __attribute__((aligned(16))) bf16x8 sP[RING][NFRAG][64];   // P T diag(beta)
+    __shared__ __attribute__((aligned(16))) bf16x8 sBt[RING][NBF][64];    // K_{c+1} K_c^T W_c
     __shared__ __attribute__((aligned(16))) bf16_t sV[RING][CH * SL];
     __shared__ __attribute__((aligned(16))) float sG[RING][CH];           // gamma_r
-    // exchange buffers, double-buffered by chunk parity
-    __shared__ __attribute__((aligned(16))) floatx4 sXp[2][2][4][64];     // X partials
-    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];       // S fragments
-    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][2][64];         // R' fragments
-    __shared__ int sFlag;                                                  // chunks whose R' is in sRf
+    // S_c and R'_c as MFMA operands, by chunk parity
+    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];
+    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][2][64];
+    __shared__ __attribute__((aligned(16))) bf16_t sQ[2][32 * DK];        // Q rows of each output wave
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -638,65 +652,76 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
     // element offset of logical (row r, column cc) in a swizzled K tile
     auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
-    if (tid == 0) sFlag = 0;
+    // descriptor over the rows of chunk c of this head in a [token][H][width] tensor
+    auto crsrc = [&](const void* base, int width, int c) {
+        return rsrc(reinterpret_cast<const bf16_t*>(base) + (tok0(c) * H + h) * width,
+                    (uint32_t)(((long)(rows(c) - 1) * H + 1) * width * 2));
+    };
 
-    if (wave == 4) {
-        // ------------------------------------------------ loader
-        const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
-        const bf16_t* gv = reinterpret_cast<const bf16_t*>(p.v);
+    if (wave >= 4) {
+        // ------------------------------------------------ loaders
+        // One wave issues global loads at about a third of a CU's rate, so four
+        // waves share the copies: K load groups, W and B fragments with index
+        // = loader (mod 4), the two V loads on loaders 2 and 3, gamma on loader 0.
+        const int li = wave - 4;
         const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
-        const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
-        int koff[NCH];   // loop-invariant byte offsets of this lane's K loads within a chunk
+        const bf16_t* wsB = reinterpret_cast<const bf16_t*>(p.wsB);
+        int koff[NCH / 4];   // loop-invariant byte offsets of this lane's K loads within a chunk
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            const int r = RPI * i + lane / NCH;
-            koff[i] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+        for (int j = 0; j < NCH / 4; ++j) {
+            const int r = RPI * (li + 4 * j) + lane / NCH;
+            koff[j] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
         }
-        int voff[2];
+        const int voff = ((32 * (li & 1) + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
+        auto issue = [&](int c, auto SLOT, auto LI) {
+            constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
+            const long sc = slot(c);
+            const auto rk = crsrc(p.k, DK, c);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) voff[i] = ((32 * i + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
-        auto issue = [&](int c, auto SLOT) {
-            constexpr int sl = decltype(SLOT)::value;
-            const long row0 = tok0(c) * H + h, sc = slot(c);
-            const auto rk = rsrc(gk + row0 * DK, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2));
-#pragma unroll
-            for (int i = 0; i < NCH; ++i) bdma16(rk, &sK[sl][RPI * i * DK], koff[i]);
+            for (int j = 0; j < NCH / 4; ++j) bdma16(rk, &sK[sl][RPI * (L + 4 * j) * DK], koff[j]);
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
-            const auto rp = rsrc(wsP + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
-            for (int f = 0; f < NFRAG; ++f) {
-                bdma16(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
-                bdma16(rp, &sP[sl][f][0], (f * 64 + lane) * 16);
+            for (int f = L; f < NFRAG; f += 4) bdma16(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
+            const auto rb = rsrc(wsB + sc * (NBF * 512), NBF * 512 * 2);
+#pragma unroll
+            for (int f = L; f < NBF; f += 4) bdma16(rb, &sBt[sl][f][0], (f * 64 + lane) * 16);
+            if constexpr (L >= 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L & 1) * SL], voff);
+            if constexpr (L == 0) bdma4(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+        };
+        // After barrier c every wave is done with chunk c-1, whose slot is
+        // (c+3) % RING: chunk c+3 is loaded there, and the wait leaves only
+        // those loads in flight, so chunk c+2 has landed before barrier c+1.
+        auto run = [&](auto LI) {
+            constexpr int L = decltype(LI)::value;
+            constexpr int NI = NCH / 4 + (NFRAG - L + 3) / 4 + (NBF - L + 3) / 4 + (L >= 2) + (L == 0);
+            auto lstep = [&](int c, auto SLOT) {
+                constexpr int bn = (decltype(SLOT)::value + 3) % RING;
+                lds_barrier();
+                issue(min(c + 3, nc - 1), Ic<bn>{}, LI);
+                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
+            };
+            if (nc > 0) {
+                issue(0, Ic<0>{}, LI);
+                issue(min(1, nc - 1), Ic<1>{}, LI);
+                issue(min(2, nc - 1), Ic<2>{}, LI);
             }
-            const auto rv = rsrc(gv + row0 * DV, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DV * 2));
-            bdma16(rv, &sV[sl][0], voff[0]);
-            bdma16(rv, &sV[sl][32 * SL], voff[1]);
-            bdma4(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
+            lds_barrier();   // prologue 2: S_0 halves visible
+            for (int c = 0; c < nc; c += RING) {
+                lstep(c, Ic<0>{});
+                if (c + 1 < nc) lstep(c + 1, Ic<1>{});
+                if (c + 2 < nc) lstep(c + 2, Ic<2>{});
+                if (c + 3 < nc) lstep(c + 3, Ic<3>{});
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         };
-        // Chunk c+1 is read by the chain right after barrier c, so it must be
-        // resident before that barrier.  After barrier c every wave is past chunk
-        // c-1, whose slot is (c+3) % RING: chunk c+3 is loaded there, then the
-        // wait leaves only those loads in flight (chunk c+2 has landed).
-        auto lstep = [&](int c, auto SLOT) {
-            constexpr int bn = (decltype(SLOT)::value + 3) % RING;
-            lds_barrier();
-            issue(min(c + 3, nc - 1), Ic<bn>{});
-            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NISSUE) : "memory");
-        };
-        if (nc > 0) {
-            issue(0, Ic<0>{});
-            issue(min(1, nc - 1), Ic<1>{});
-            issue(min(2, nc - 1), Ic<2>{});
+        switch (li) {
+            case 0: run(Ic<0>{}); break;
+            case 1: run(Ic<1>{}); break;
+            case 2: run(Ic<2>{}); break;
+            default: run(Ic<3>{}); break;
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        lds_barrier();   // prologue: chunks 0, 1 and 2 resident
-        for (int c = 0; c < nc; c += RING) {
-            lstep(c, Ic<0>{});
-            if (c + 1 < nc) lstep(c + 1, Ic<1>{});
-            if (c + 2 < nc) lstep(c + 2, Ic<2>{});
-            if (c + 3 < nc) lstep(c + 3, Ic<3>{});
-        }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     } else if (wave < 2) {
         // ------------------------------------------------ chain waves
         const int w = wave;
@@ -707,12 +732,19 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
             acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
             if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(w * HMD + m));
         }
-        int offX[4][HKD], offT[HMD][2][2], offV[4];   // loop-invariant LDS offsets of this lane's operands
+        // loop-invariant LDS offsets of this lane's operands
+        int offT[HMD][2][2];      // K^T fragments of this wave's key tiles (transpose reads)
+        int offX[2][2][HKD];      // K rows of this wave's token tiles: [tile][own / other key half][block]
+        int offV[2];              // V rows of this wave's token tiles (transpose reads)
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
+        for (int i = 0; i < 2; ++i) {
+            const int mt = 2 * w + i;
 #pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) offX[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
-            offV[mt] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
+            for (int k2 = 0; k2 < HKD; ++k2) {
+                offX[i][0][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
+                offX[i][1][k2] = kq(16 * mt + l16, 32 * ((1 - w) * HKD + k2) + 8 * lg);
+            }
+            offV[i] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
         }
 #pragma unroll
         for (int m = 0; m < HMD; ++m) {
@@ -724,64 +756,91 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                     offT[m][kk][h2] = kq(32 * kk + 16 * h2 + 4 * lg + (l16 >> 2),
                                          32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1));
         }
+        bf16x8 sfo[HKD], rfo;   // this wave's halves of S_c and R'_c
+        auto publish_s = [&](int par) {
+#pragma unroll
+            for (int k2 = 0; k2 < HKD; ++k2) {
+                sfo[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
+                sSf[par][w * HKD + k2][lane] = sfo[k2];
+            }
+        };
+        // R' rows of this wave's token tiles from X = gn y + z: V - diag(gamma) X
+        auto rprime = [&](const floatx4 (&y)[2], const floatx4 (&z)[2], float gn, int bn) {
+            floatx4 rr[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const short4v vv = lds_tr8(&sV[bn][offV[i]]);
+                const floatx4 gm = *reinterpret_cast<const floatx4*>(&sG[bn][16 * (2 * w + i) + 4 * lg]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) rr[i][e] = bf(vv[e]) - gm[e] * (gn * y[i][e] + z[i][e]);
+            }
+            return pack_bf16(rr[0], rr[1]);
+        };
+        lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
+        if (nc > 0) publish_s(0);
+        lds_barrier();   // prologue 2: S_0 halves visible
+        if (nc > 0) {    // R'_0 = V_0 - diag(gamma_0) K_0 S_0^T for this wave's token tiles
+            bf16x8 sfx[HKD];
+#pragma unroll
+            for (int k2 = 0; k2 < HKD; ++k2) sfx[k2] = sSf[0][(1 - w) * HKD + k2][lane];
+            floatx4 y[2], z[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                y[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+                z[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) {
+                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(&sK[0][offX[i][0][k2]]), sfo[k2], y[i], 0, 0, 0);
+                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(&sK[0][offX[i][1][k2]]), sfx[k2], y[i], 0, 0, 0);
+                }
+            }
+            rfo = rprime(y, z, 1.f, 0);
+            sRf[0][w][lane] = rfo;
+        }
         auto cstep = [&](int c, auto SLOT) {
-            constexpr int b = decltype(SLOT)::value, x2 = b & 1;
-            const bf16_t* K = sK[b];
-            // every LDS operand of the chunk is read first
-            bf16x8 xa[4][HKD], wf[NFRAG], ka[HMD][2];
-            short4v vv[4];
-            floatx4 gm[4];
+            constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
+            lds_barrier();   // barrier c: both halves of S_c and R'_c visible
+            // the other wave's halves, then chunk c's operands and chunk c+1's K rows
+            bf16x8 sfx[HKD];
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
+            for (int k2 = 0; k2 < HKD; ++k2) sfx[k2] = sSf[x2][(1 - w) * HKD + k2][lane];
+            const bf16x8 rfx = sRf[x2][1 - w][lane];
+            const bf16x8 rf0 = sel(w == 0, rfo, rfx), rf1 = sel(w == 0, rfx, rfo);
+            bf16x8 xo[2][HKD], xx[2][HKD], bo[2], bx[2], wf[NFRAG], ka[HMD][2];
 #pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2) xa[mt][k2] = *reinterpret_cast<const bf16x8*>(K + offX[mt][k2]);
+            for (int i = 0; i < 2; ++i) {
 #pragma unroll
-            for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                vv[mt] = lds_tr8(&sV[b][offV[mt]]);
-                gm[mt] = *reinterpret_cast<const floatx4*>(&sG[b][16 * mt + 4 * lg]);
+                for (int k2 = 0; k2 < HKD; ++k2) {
+                    xo[i][k2] = *reinterpret_cast<const bf16x8*>(&sK[bn][offX[i][0][k2]]);
+                    xx[i][k2] = *reinterpret_cast<const bf16x8*>(&sK[bn][offX[i][1][k2]]);
+                }
+                bo[i] = sBt[b][2 * (2 * w + i) + w][lane];
+                bx[i] = sBt[b][2 * (2 * w + i) + 1 - w][lane];
             }
             const float gn = sG[b][CH - 1];
 #pragma unroll
+            for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
+#pragma unroll
             for (int m = 0; m < HMD; ++m)
 #pragma unroll
-                for (int kk = 0; kk < 2; ++kk) ka[m][kk] = join4(lds_tr8(K + offT[m][kk][0]), lds_tr8(K + offT[m][kk][1]));
-            __builtin_amdgcn_sched_barrier(0);
-            // S fragments of this wave's key blocks; partial X = K S^T
-            bf16x8 sf[HKD];
+                for (int kk = 0; kk < 2; ++kk)
+                    ka[m][kk] = join4(lds_tr8(&sK[b][offT[m][kk][0]]), lds_tr8(&sK[b][offT[m][kk][1]]));
+            // X_{c+1} for this wave's token tiles: gn (K_{c+1} S_c^T) + B_c R'_c
+            floatx4 y[2], z[2];
 #pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) {
-                sf[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
-                sSf[x2][w * HKD + k2][lane] = sf[k2];
+            for (int i = 0; i < 2; ++i) {
+                z[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bo[i], rfo, floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                z[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bx[i], rfx, z[i], 0, 0, 0);
+                y[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) {
+                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xo[i][k2], sfo[k2], y[i], 0, 0, 0);
+                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xx[i][k2], sfx[k2], y[i], 0, 0, 0);
+                }
             }
-            floatx4 x[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][0], sf[0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-#pragma unroll
-                for (int k2 = 1; k2 < HKD; ++k2)
-                    x[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt][k2], sf[k2], x[mt], 0, 0, 0);
-                sXp[x2][w][mt][lane] = x[mt];
-            }
-            lds_barrier();   // the chunk's one barrier: both partials (and S fragments) visible
-            // R' = V - diag(gamma) X
-            floatx4 rr[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                x[mt] += sXp[x2][1 - w][mt][lane];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) rr[mt][e] = bf(vv[mt][e]) - gm[mt][e] * x[mt][e];
-            }
-            const bf16x8 rf0 = pack_bf16(rr[0], rr[1]), rf1 = pack_bf16(rr[2], rr[3]);
-            if (w == 0) {
-                sRf[x2][0][lane] = rf0;
-                sRf[x2][1][lane] = rf1;
-                // publish: the R' fragments of chunk c are written before the flag moves
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                if (lane == 0) __hip_atomic_store(&sFlag, c + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
-            // D U = (diag(D) T diag(beta)) R'; lower triangular: tile mt needs blocks 0..mt/2
+            // D U = W R' (lower triangular: tile mt needs blocks 0..mt/2); S^T <- gn S^T + K^T (D U)
             floatx4 du[4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
@@ -790,15 +849,17 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                 if (mt >= 2) du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 1)], rf1, du[mt], 0, 0, 0);
             }
             const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
-            // S^T <- gamma_n S^T + K^T (D U) on this wave's key tiles
 #pragma unroll
             for (int m = 0; m < HMD; ++m) {
                 acc[m] *= gn;
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
             }
+            // R'_{c+1} and S_{c+1}, published for chunk c+1
+            rfo = rprime(y, z, gn, bn);
+            sRf[1 - x2][w][lane] = rfo;
+            publish_s(1 - x2);
         };
-        lds_barrier();   // prologue
         for (int c = 0; c < nc; c += RING) {
             cstep(c, Ic<0>{});
             if (c + 1 < nc) cstep(c + 1, Ic<1>{});
@@ -812,98 +873,202 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
         }
     } else {
         // ------------------------------------------------ output waves
-        const int ow = wave - 2;
-        const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
+        // Wave 2 + o handles token tiles 2o, 2o + 1 (rows 32o .. 32o + 31).  Its Q
+        // rows are staged in LDS by buffer loads (whole 128-byte lines, XOR-swizzled
+        // like K), one chunk ahead.  P' token tile mt needs fragments (mt, 0..mt/2):
+        // wave 2 fragments 0, 1; wave 3 fragments 2, 3, 4, 5.
         bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
-        typedef int int4v __attribute__((ext_vector_type(4)));
-        int qoff[2][NKD];   // byte offsets of this lane's Q fragments within a chunk
+        auto run = [&](auto OW) {
+            constexpr int ow = decltype(OW)::value, NPP = ow ? 4 : 2;
+            const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
+            bf16_t* sq = sQ[ow];
+            int qoff[32 / RPI];   // byte offsets of this lane's Q row loads within a chunk
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+            for (int j = 0; j < 32 / RPI; ++j) {
+                const int r = RPI * j + lane / NCH;
+                qoff[j] = ((32 * ow + r) * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+            }
+            auto load_q = [&](int c) {   // last global load of a step: the next step waits for all
+                const auto rq = crsrc(p.q, DK, c);
 #pragma unroll
-            for (int kk = 0; kk < NKD; ++kk) qoff[i][kk] = ((16 * (2 * ow + i) + l16) * H * DK + 32 * kk + 8 * lg) * 2;
-        // Q fragments come straight from global memory, one chunk ahead (rows past
-        // the chunk fall outside the descriptor and read as zeros)
-        auto load_q = [&](int c, bf16x8(&qa)[2][NKD]) {
-            const auto rq = rsrc(gq + (tok0(c) * H + h) * DK, (uint32_t)(((long)(rows(c) - 1) * H + 1) * DK * 2));
+                for (int j = 0; j < 32 / RPI; ++j) bdma16(rq, sq + RPI * j * DK, qoff[j]);
+            };
+            auto load_p = [&](int c, bf16x8(&pa)[NPP]) {
+                const auto rp = rsrc(wsP + slot(c) * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+                for (int k = 0; k < NPP; ++k) pa[k] = bload16(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
+            };
+            auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
+                constexpr int b = decltype(SLOT)::value, x2 = b & 1;
+                const int n = rows(c);
+                lds_barrier();   // barrier c: S_c and R'_c visible
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // Q_c staged, P'_c loaded
+                bf16x8 qa[2][NKD];
 #pragma unroll
-                for (int kk = 0; kk < NKD; ++kk)
-                    qa[i][kk] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, qoff[i][kk], 0, 0));
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int kk = 0; kk < NKD; ++kk)
+                        qa[i][kk] = *reinterpret_cast<const bf16x8*>(sq + kq(16 * i + l16, 32 * kk + 8 * lg));
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // staging area read: free for Q_{c+1}
+                load_p(min(c + 1, nc - 1), pn);
+                const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int mt = 2 * ow + i, tok = 16 * mt + l16;
+                    const float gm = sG[b][tok];
+                    floatx4 oq = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kk = 0; kk < NKD; ++kk)
+                        oq = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sSf[x2][kk][lane], qa[i][kk], oq, 0, 0, 0);
+                    floatx4 op;
+                    if constexpr (ow == 0) {
+                        op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf0, pa[i], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    } else {   // fragments (mt, 0) = pa[2 i], (mt, 1) = pa[2 i + 1]
+                        op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf0, pa[2 * i], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                        op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pa[2 * i + 1], op, 0, 0, 0);
+                    }
+                    const floatx4 ov = p.scale * (gm * oq + op);   // value channels 4 lg .. 4 lg + 3 of token tok
+                    if (tok < n)
+                        *reinterpret_cast<bf16x4*>(go + ((tok0(c) + tok) * H + h) * (long)DV + js * SL + 4 * lg) =
+                            __builtin_convertvector(ov, bf16x4);
+                }
+                load_q(min(c + 1, nc - 1));
+            };
+            bf16x8 pA[NPP], pB[NPP];
+            if (nc > 0) {
+                load_p(0, pA);
+                load_q(0);
+            }
+            lds_barrier();   // prologue 1
+            lds_barrier();   // prologue 2
+            for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
+                ostep(c, Ic<0>{}, pA, pB);
+                if (c + 1 < nc) ostep(c + 1, Ic<1>{}, pB, pA);
+                if (c + 2 < nc) ostep(c + 2, Ic<2>{}, pA, pB);
+                if (c + 3 < nc) ostep(c + 3, Ic<3>{}, pB, pA);
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         };
-        auto ostep = [&](int c, auto SLOT, bf16x8(&qa)[2][NKD], bf16x8(&qn)[2][NKD]) {
-            constexpr int b = decltype(SLOT)::value, x2 = b & 1;
-            const int n = rows(c);
-            lds_barrier();   // the chunk's barrier: S fragments of chunk c visible
-            load_q(min(c + 1, nc - 1), qn);
-            bf16x8 pf[2][2];
-            float gm[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int mt = 2 * ow + i;
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk) pf[i][kk] = sP[b][frag_id(mt, mt >= 2 ? kk : 0)][lane];
-                gm[i] = sG[b][16 * mt + l16];
-            }
-            floatx4 oq[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                oq[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int kk = 0; kk < NKD; ++kk)
-                    oq[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sSf[x2][kk][lane], qa[i][kk], oq[i], 0, 0, 0);
-            }
-            // wait (bounded) until the chain has published R' of chunk c
-            for (int spin = 0; spin < (1 << 22); ++spin) {
-                if (__hip_atomic_load(&sFlag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) > c) break;
-                __builtin_amdgcn_s_sleep(1);
-            }
-            asm volatile("" ::: "memory");
-            const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int mt = 2 * ow + i, tok = 16 * mt + l16;
-                floatx4 op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf0, pf[i][0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                if (mt >= 2) op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pf[i][1], op, 0, 0, 0);
-                const floatx4 ov = p.scale * (gm[i] * oq[i] + op);   // value channels 4 lg .. 4 lg + 3 of token tok
-                if (tok < n)
-                    *reinterpret_cast<bf16x4*>(go + ((tok0(c) + tok) * H + h) * (long)DV + js * SL + 4 * lg) =
-                        __builtin_convertvector(ov, bf16x4);
-            }
-        };
-        bf16x8 qA[2][NKD], qB[2][NKD];
-        if (nc > 0) load_q(0, qA);
-        lds_barrier();   // prologue
-        for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and Q buffer are both constants
-            ostep(c, Ic<0>{}, qA, qB);
-            if (c + 1 < nc) ostep(c + 1, Ic<1>{}, qB, qA);
-            if (c + 2 < nc) ostep(c + 2, Ic<2>{}, qA, qB);
-            if (c + 3 < nc) ostep(c + 3, Ic<3>{}, qB, qA);
-        }
+        if (wave == 2) run(Ic<0>{});
+        else run(Ic<1>{});
     }
 }
 
 // ------------------------------------------------------------------ bf16 chunk terms
-// One workgroup (4 waves) per (chunk slot, head), bf16 io.  Produces, for the
-// state chain: gamma_r and exp(G_n - G_r), and in MFMA fragment order
-// (frag_row / frag_col) the two lower-triangular matrices
-//     W_D = diag(D) T diag(beta)     and     P_T = P T diag(beta),
-// T = (I + A)^{-1}.  K and Q arrive through buffer loads to LDS (rows past the
-// chunk read as zero); the in-chunk prefix sums are kept in fp64 and in log2
-// units, so every decay factor is one exp2 of an fp64 difference.  The four
-// diagonal 16x16 blocks of T are inverted together by one wave (lane = 16 block
-// + column); the off-diagonal blocks follow by fp32 MFMA block products.
-// P_T is formed transposed, (T^T P^T), with bf16 MFMA whose T^T operand comes
-// from LDS transpose reads of a bf16 copy of T, so each P_T fragment is packed
-// straight from the accumulators.  LDS stays under 64 KB (two workgroups per
-// CU): the K/Q tiles' space is reused for T once the products are formed.
+// One workgroup (4 waves) per (chunk slot, head), bf16 io.  Produces for the
+// state chain gamma_r and exp(G_n - G_r), and in MFMA fragment order
+//     W  = diag(D) T diag(beta)     lower triangular, 6 fragments
+//     P' = P T diag(beta)           lower triangular, 6 fragments
+//     B  = K' K^T W                 64 x 64, 8 fragments
+// with T = (I + A)^{-1} and K' the key tile of the sequence's next chunk (B is
+// zero for a sequence's last chunk).  B carries a chunk's contribution to the
+// state into the next chunk's product K' S^T, so the chain can form that
+// product from the state it already has.
+// Stages: K, Q and K' arrive by buffer loads to LDS (rows past a chunk read as
+// zero); prefix sums of g in fp64 log2 units (every decay factor is one exp2
+// of an fp64 difference); each wave forms its share of the 16x16 blocks of
+// K K^T and Q K^T (lower) and K K'^T (all) with all its operands in registers,
+// so the tiles' LDS space holds A, P and T afterwards; T's diagonal blocks by
+// forward substitution with the rows of A in registers; its off-diagonal
+// blocks one block diagonal at a time by fp32 MFMA block products; the
+// fragments of W, P' and B from a bf16 copy of T.
+template <int DK, int W>
+__device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, const bf16_t* sKn,
+                                            const double* sGl, const float* sB, const float* sD, int l16, int lg,
+                                            floatx4 (&ablk)[3], floatx4 (&pblk)[3], bf16x8 (&def)[2]) {
+    constexpr int NCH = DK / 8, NKD = DK / 32;
+    // lower 16x16 blocks (bi, bj): KK^T takes entries W, W+4, ..; QK^T entries (W+2)%4, ..
+    constexpr int BI[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
+    constexpr int BJ[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
+    constexpr int QW = (W + 2) % 4;
+    constexpr int NA = W < 2 ? 3 : 2, NP = QW < 2 ? 3 : 2;
+    auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
+    auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
+    bf16x8 kf[4][NKD], kn[NKD];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) kf[rb][kk] = *reinterpret_cast<const bf16x8*>(sK + kq(16 * rb + l16, 32 * kk + 8 * lg));
+#pragma unroll
+    for (int kk = 0; kk < NKD; ++kk) kn[kk] = *reinterpret_cast<const bf16x8*>(sKn + kq(16 * W + l16, 32 * kk + 8 * lg));
+    bf16x8 qf[NP][NKD];
+#pragma unroll
+    for (int j = 0; j < NP; ++j)
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk)
+            qf[j][kk] = *reinterpret_cast<const bf16x8*>(sQ + kq(16 * BI[QW + 4 * j] + l16, 32 * kk + 8 * lg));
+    // K K'^T transposed, tiles (ib, W): lane holds E^T[16 ib + 4 lg + e][16 W + l16]
+    floatx4 et[4];
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {
+        et[ib] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) et[ib] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ib][kk], kn[kk], et[ib], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+        const int bi = BI[W + 4 * j], bj = BJ[W + 4 * j];
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bi][kk], kf[bj][kk], acc, 0, 0, 0);
+        const int i = 16 * bj + l16;
+        const double gi = sGl[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = 16 * bi + 4 * lg + e;
+            const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - gi));
+            ablk[j][e] = r > i ? sB[r] * gam * acc[e] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+        const int bi = BI[QW + 4 * j], bj = BJ[QW + 4 * j];
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[j][kk], kf[bj][kk], acc, 0, 0, 0);
+        const int i = 16 * bj + l16;
+        const double gi = sGl[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = 16 * bi + 4 * lg + e;
+            const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - gi));
+            pblk[j][e] = r >= i ? gam * acc[e] : 0.f;
+        }
+    }
+    // diag(D) E^T, packed as B operands over the chunk's tokens (contraction order
+    // 32 kk + 16 (e/4) + 4 lg + e%4 -- the rows an accumulator tile pair holds)
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) et[ib] *= *reinterpret_cast<const floatx4*>(&sD[16 * ib + 4 * lg]);
+    def[0] = pack_bf16(et[0], et[1]);
+    def[1] = pack_bf16(et[2], et[3]);
+}
+
+template <int DK, int W>
+__device__ __forceinline__ void store_gram(float (*sA)[CH + 4], bf16_t (*sPb)[CH + 8], int l16, int lg,
+                                           const floatx4 (&ablk)[3], const floatx4 (&pblk)[3]) {
+    constexpr int BI[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
+    constexpr int BJ[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
+    constexpr int QW = (W + 2) % 4;
+    constexpr int NA = W < 2 ? 3 : 2, NP = QW < 2 ? 3 : 2;
+#pragma unroll
+    for (int j = 0; j < NA; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sA[16 * BI[W + 4 * j] + 4 * lg + e][16 * BJ[W + 4 * j] + l16] = ablk[j][e];
+#pragma unroll
+    for (int j = 0; j < NP; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sPb[16 * BI[QW + 4 * j] + 4 * lg + e][16 * BJ[QW + 4 * j] + l16] = from_f<bf16_t>(pblk[j][e]);
+}
+
 template <int DK>
 __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     constexpr int NCH = DK / 8;     // 16-byte chunks per K/Q row
     constexpr int RPI = 64 / NCH;   // rows per 1 KB buffer load
-    constexpr int NKD = DK / 32;    // MFMA contraction blocks over the key channels
-    constexpr int R0 = (2 * CH * DK * 2 > CH * (CH + 4) * 4 + CH * (CH + 8) * 2) ? 2 * CH * DK * 2
-                                                                                 : CH * (CH + 4) * 4 + CH * (CH + 8) * 2;
+    constexpr int TILE = CH * DK;
+    constexpr int PA = CH + 4, PB = CH + 8;   // row pitches of the fp32 and bf16 64 x 64 matrices
+    constexpr int SZ_TILES = 3 * TILE * 2;
+    constexpr int SZ_MATS = 2 * CH * PA * 4 + CH * PB * 2;
+    constexpr int R0 = SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS;
     const int H = p.H;
     const int gc = blockIdx.x / H, h = blockIdx.x % H;
     int s;
@@ -924,35 +1089,41 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     const int c = gc - cbase;
     const long t0 = start + (long)c * CH;
     const int n = min(CH, len - c * CH);
+    const int n1 = min(CH, len - (c + 1) * CH);   // rows of the next chunk (<= 0: none)
     const long slot = (long)gc * H + h;
 
     __shared__ __attribute__((aligned(16))) char r0[R0];
-    __shared__ __attribute__((aligned(16))) float sA[CH][CH + 4];
-    __shared__ __attribute__((aligned(16))) bf16_t sPb[CH][CH + 8];
-    __shared__ float sZ[4][16][17];
     __shared__ double sGl[CH];
     __shared__ __attribute__((aligned(16))) float sB[CH];
     __shared__ __attribute__((aligned(16))) float sD[CH];
+    // phase 1: the K, Q and K' tiles; phase 2: A, T (fp32) and P (bf16); T's bf16 copy over A
     bf16_t* sK = reinterpret_cast<bf16_t*>(r0);
-    bf16_t* sQ = sK + CH * DK;
-    float(*sTi)[CH + 4] = reinterpret_cast<float(*)[CH + 4]>(r0);
-    bf16_t(*sTb)[CH + 8] = reinterpret_cast<bf16_t(*)[CH + 8]>(r0 + CH * (CH + 4) * 4);
+    bf16_t* sQ = sK + TILE;
+    bf16_t* sKn = sQ + TILE;
+    float(*sA)[PA] = reinterpret_cast<float(*)[PA]>(r0);
+    float(*sTi)[PA] = reinterpret_cast<float(*)[PA]>(r0 + CH * PA * 4);
+    bf16_t(*sPb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0 + 2 * CH * PA * 4);
+    bf16_t(*sTb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
-    auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
 
-    {   // K and Q tiles straight into LDS; loads i = wave, wave + 4, ...
+    {   // K, Q and K' tiles straight into LDS; loads i = wave, wave + 4, ...
+        const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
+        const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
         const long row0 = t0 * H + h;
         const uint32_t bytes = (uint32_t)(((long)(n - 1) * H + 1) * DK * 2);
-        const auto rk = rsrc(reinterpret_cast<const bf16_t*>(p.k) + row0 * DK, bytes);
-        const auto rq = rsrc(reinterpret_cast<const bf16_t*>(p.q) + row0 * DK, bytes);
+        const auto rk = rsrc(gk + row0 * DK, bytes);
+        const auto rq = rsrc(gq + row0 * DK, bytes);
+        const auto rn = n1 > 0 ? rsrc(gk + (row0 + (long)CH * H) * DK, (uint32_t)(((long)(n1 - 1) * H + 1) * DK * 2))
+                               : rsrc(gk, 0);   // empty: the tile reads as zeros
         for (int i = wave; i < NCH; i += 4) {
             const int r = RPI * i + lane / NCH;
             const int off = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             bdma16(rk, sK + RPI * i * DK, off);
             bdma16(rq, sQ + RPI * i * DK, off);
+            bdma16(rn, sKn + RPI * i * DK, off);
         }
     }
     if (wave == 0) {
@@ -976,87 +1147,85 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
 
-    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P); the 6 upper
-    // blocks of P are zero
-    for (int job = wave; job < 26; job += 4) {
-        if (job >= 20) {
-            int t = job - 20, bj = 1;   // upper block (bi, bj), bi < bj
-            while (t >= bj) { t -= bj; ++bj; }
-            const int bi = t;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sPb[16 * bi + 4 * lg + e][16 * bj + l16] = 0;
-            continue;
-        }
-        const int which = job / 10;
-        int t = job % 10, bi = 0;
-        while (t > bi) { t -= bi + 1; ++bi; }
-        const int bj = t;
-        const bf16_t* X = which ? sQ : sK;
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < NKD; ++kk) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(X + kq(16 * bi + l16, 32 * kk + 8 * lg));
-            const bf16x8 b = *reinterpret_cast<const bf16x8*>(sK + kq(16 * bj + l16, 32 * kk + 8 * lg));
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-        }
-        const int i = 16 * bj + l16;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = 16 * bi + 4 * lg + e;
-            const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - sGl[i]));
-            if (which == 0) sA[r][i] = (r > i) ? sB[r] * gam * acc[e] : 0.f;
-            else sPb[r][i] = from_f<bf16_t>((r >= i) ? gam * acc[e] : 0.f);
-        }
+    // token-token blocks, all operands in registers
+    floatx4 ablk[3], pblk[3];
+    bf16x8 def[2];
+    switch (wave) {
+        case 0: gram_blocks<DK, 0>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
+        case 1: gram_blocks<DK, 1>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
+        case 2: gram_blocks<DK, 2>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
+        default: gram_blocks<DK, 3>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
+    }
+    __syncthreads();   // every tile read done: A, P and T take the space over
+    switch (wave) {
+        case 0: store_gram<DK, 0>(sA, sPb, l16, lg, ablk, pblk); break;
+        case 1: store_gram<DK, 1>(sA, sPb, l16, lg, ablk, pblk); break;
+        case 2: store_gram<DK, 2>(sA, sPb, l16, lg, ablk, pblk); break;
+        default: store_gram<DK, 3>(sA, sPb, l16, lg, ablk, pblk); break;
+    }
+    for (int i = tid; i < 6 * 256; i += NT) {   // P's six upper blocks are zero
+        int t = i / 256, bj = 1;
+        while (t >= bj) { t -= bj; ++bj; }
+        const int e = i % 256;
+        sPb[16 * t + e / 16][16 * bj + e % 16] = 0;
     }
     __syncthreads();
 
     // T = (I + A)^{-1}: diagonal blocks by forward substitution, one wave, lane =
-    // 16 * block + column; meanwhile the other waves clear T's upper blocks
+    // 16 * block + column, A's block rows in registers; meanwhile the other
+    // waves clear T's upper blocks
     if (wave == 0) {
         const int b = lg;
+        float a[16][16];
+#pragma unroll
+        for (int r = 1; r < 16; ++r)
+#pragma unroll
+            for (int q = 0; 4 * q < r; ++q) {
+                const floatx4 v = *reinterpret_cast<const floatx4*>(&sA[16 * b + r][16 * b + 4 * q]);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) a[r][4 * q + t] = v[t];
+            }
         float x[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float acc = (r == l16) ? 1.f : 0.f;
+        for (int r = 0; r < 16; ++r) x[r] = r == l16 ? 1.f : 0.f;
 #pragma unroll
-            for (int i = 0; i < r; ++i) acc -= sA[16 * b + r][16 * b + i] * x[i];
-            x[r] = acc;
-        }
+        for (int i = 0; i < 15; ++i)
+#pragma unroll
+            for (int r = i + 1; r < 16; ++r) x[r] -= a[r][i] * x[i];
 #pragma unroll
         for (int r = 0; r < 16; ++r) sTi[16 * b + r][16 * b + l16] = x[r];
     } else {
         for (int i = tid - 64; i < 6 * 256; i += NT - 64) {
             int t = i / 256, bj = 1;
             while (t >= bj) { t -= bj; ++bj; }
-            const int bi = t, e = i % 256;
-            sTi[16 * bi + e / 16][16 * bj + e % 16] = 0.f;
+            const int e = i % 256;
+            sTi[16 * t + e / 16][16 * bj + e % 16] = 0.f;
         }
     }
     __syncthreads();
-    for (int b = 1; b < 4; ++b) {   // block row b: T_bj = -T_bb sum_{j <= m < b} A_bm T_mj
-        if (wave < b) {
-            const int j = wave;
+    // off-diagonal blocks, diagonal d: T_{b,b-d} = -T_bb sum_{m} A_bm T_{m,b-d}.
+    // In MFMA step kk, lane group lg carries contraction index 4 lg + kk, so the
+    // sum Z comes out of the accumulator exactly as the second product's B operand.
+    for (int d = 1; d < 4; ++d) {
+        if (wave < 4 - d) {
+            const int j = wave, b = wave + d;
             floatx4 z = {0.f, 0.f, 0.f, 0.f};
             for (int m = j; m < b; ++m) {
+                const floatx4 av = *reinterpret_cast<const floatx4*>(&sA[16 * b + l16][16 * m + 4 * lg]);
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk)
-                    z = __builtin_amdgcn_mfma_f32_16x16x4f32(sA[16 * b + l16][16 * m + 4 * kk + lg],
-                                                             sTi[16 * m + 4 * kk + lg][16 * j + l16], z, 0, 0, 0);
+                    z = __builtin_amdgcn_mfma_f32_16x16x4f32(av[kk], sTi[16 * m + 4 * lg + kk][16 * j + l16], z, 0, 0, 0);
             }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sZ[wave][4 * lg + e][l16] = z[e];
-            __builtin_amdgcn_wave_barrier();   // LDS ops of one wave complete in order
+            const floatx4 tv = *reinterpret_cast<const floatx4*>(&sTi[16 * b + l16][16 * b + 4 * lg]);
             floatx4 t = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-                t = __builtin_amdgcn_mfma_f32_16x16x4f32(sTi[16 * b + l16][16 * b + 4 * kk + lg],
-                                                         sZ[wave][4 * kk + lg][l16], t, 0, 0, 0);
+            for (int kk = 0; kk < 4; ++kk) t = __builtin_amdgcn_mfma_f32_16x16x4f32(tv[kk], z[kk], t, 0, 0, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) sTi[16 * b + 4 * lg + e][16 * j + l16] = -t[e];
         }
         __syncthreads();
     }
-    for (int i = tid; i < CH * CH / 4; i += NT) {   // bf16 copy of T
+    for (int i = tid; i < CH * CH / 4; i += NT) {   // bf16 copy of T (A is no longer read)
         const int r = i / (CH / 4), c4 = 4 * (i % (CH / 4));
         const floatx4 v = *reinterpret_cast<const floatx4*>(&sTi[r][c4]);
         *reinterpret_cast<bf16x4*>(&sTb[r][c4]) = __builtin_convertvector(v, bf16x4);
@@ -1065,16 +1234,17 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
 
     bf16_t* Wg = reinterpret_cast<bf16_t*>(p.wsT) + slot * tp_elems<bf16_t>();
     bf16_t* Pg = reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>();
+    bf16_t* Bg = reinterpret_cast<bf16_t*>(p.wsB) + slot * (NBF * 64 * 8);
     for (int f = wave; f < NFRAG; f += 4) {
         const int mt = frag_mt(f), kk2 = frag_kk(f), r = 16 * mt + l16;
-        // W_D fragment: D_r T[r][tau] beta_tau
+        // W fragment: D_r T[r][tau] beta_tau
         const float dr = sD[r];
         const floatx4 b0 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 4 * lg]);
         const floatx4 b1 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 16 + 4 * lg]);
         const floatx4 w0 = dr * b0 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 4 * lg]);
         const floatx4 w1 = dr * b1 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 16 + 4 * lg]);
         *reinterpret_cast<bf16x8*>(Wg + (f * 64 + lane) * 8) = pack_bf16(w0, w1);
-        // P_T fragment from (T^T P^T) tiles (tau block 2 kk2 + hb, token block mt)
+        // P' fragment from (T^T P^T) tiles (tau block 2 kk2 + hb, token block mt)
         floatx4 pt[2];
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb) {
@@ -1084,13 +1254,31 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
 #pragma unroll
             for (int kk = 0; kk < 2; ++kk) {
                 const bf16_t* t0p = &sTb[32 * kk + 8 * lg + (l16 >> 2)][16 * bt + 4 * (l16 & 3)];
-                const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 4 * (CH + 8)));
+                const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 4 * PB));
                 const bf16x8 bb = *reinterpret_cast<const bf16x8*>(&sPb[16 * mt + l16][32 * kk + 8 * lg]);
                 pt[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb, pt[hb], 0, 0, 0);
             }
             pt[hb] *= hb ? b1 : b0;
         }
         *reinterpret_cast<bf16x8*>(Pg + (f * 64 + lane) * 8) = pack_bf16(pt[0], pt[1]);
+    }
+    {   // B fragments (row block mt = wave) from B^T = diag(beta) T^T (diag(D) E^T) tiles
+        // (tau block bt, token block mt); T^T's contraction order matches def's
+        floatx4 bt4[4];
+#pragma unroll
+        for (int bt = 0; bt < 4; ++bt) {
+            bt4[bt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = bt < 2 ? 0 : 1; kk < 2; ++kk) {   // T^T[tau][i] = 0 for i < tau
+                const bf16_t* t0p = &sTb[32 * kk + 4 * lg + (l16 >> 2)][16 * bt + 4 * (l16 & 3)];
+                const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 16 * PB));
+                bt4[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, def[kk], bt4[bt], 0, 0, 0);
+            }
+            bt4[bt] *= *reinterpret_cast<const floatx4*>(&sB[16 * bt + 4 * lg]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+            *reinterpret_cast<bf16x8*>(Bg + ((2 * wave + kk) * 64 + lane) * 8) = pack_bf16(bt4[2 * kk], bt4[2 * kk + 1]);
     }
 }
 
@@ -1151,7 +1339,7 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
     long slots;          // chunk slots per head
-    size_t meta, G, T, P, total;
+    size_t meta, G, T, P, B, total;
 };
 
 // Workspace layout; returns false for arguments that are out of range.
@@ -1168,7 +1356,8 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
-    L->total = L->P + round_up(per * tp * esz, 256);
+    L->B = L->P + round_up(per * tp * esz, 256);
+    L->total = L->B + (io == GDN_BF16 ? round_up(per * NBF * 512 * 2, 256) : 0);
     return true;
 }
 
@@ -1287,8 +1476,9 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.wsG = reinterpret_cast<float*>(ws + L.G);
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
+    p.wsB = ws + L.B;
     p.scale = scale;
-    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; }
+    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsB = nullptr; }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
