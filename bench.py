@@ -172,7 +172,7 @@ def main():
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = None
     roof["kernel"] = "one gdn_decode_step call" if w.decode else \
-        "one gdn_chunk_prefill call (k_chunk_terms + k_state_chain)"
+        "one gdn_chunk_prefill call (k_prefill_fused_bf16 for bf16 io)"
     roof["alg_bytes"] = byts
     roof["alg_flops"] = flops
     roof["avg_call_us"] = avg_call_s * 1e6

@@ -25,10 +25,12 @@
 // row by row (rows of S never mix).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
+#include <time.h>
 
 #include "gdn.h"
 
@@ -136,6 +138,9 @@ struct Params {
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
     void* wsB;           // bf16 io: [slot][H][NBF fragments] of K_{c+1} K_c^T W_c
+    uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
+    uint64_t epoch;      // per-call tag of those flags
+    int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
     float scale;
 };
 
@@ -596,23 +601,46 @@ __device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
-__device__ __forceinline__ bf16x8 bload16(__amdgpu_buffer_rsrc_t r, int voff) {
-    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+// AUX: cache policy of the access (0: default; 17 = sc0 sc1: system coherent,
+// bypassing the caches that other workgroups' data could be stale in)
+template <int AUX = 0> __device__ __forceinline__ bf16x8 bload16(__amdgpu_buffer_rsrc_t r, int voff) {
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, AUX));
 }
 // global -> LDS without registers: lane l's 16 (4) bytes land at dst + 16 l (4 l)
-__device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, 0, 0, 0);
+template <int AUX = 0> __device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, 0, 0, AUX);
 }
-__device__ __forceinline__ void bdma4(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, 0, 0, 0);
+template <int AUX = 0> __device__ __forceinline__ void bdma4(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, 0, 0, AUX);
+}
+template <int AUX = 0> __device__ __forceinline__ void bstore16(bf16x8 v, __amdgpu_buffer_rsrc_t r, int voff) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff, 0, AUX);
+}
+template <int AUX = 0> __device__ __forceinline__ void bstore4(float v, __amdgpu_buffer_rsrc_t r, int voff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, AUX);
 }
 // Workgroup barrier ordering LDS traffic only: the wave's own LDS operations
 // complete, the compiler moves no memory access across it, and -- unlike
 // __syncthreads() -- it does not wait for outstanding global loads or stores.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int DK>
-__global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
+// LDS of one chain workgroup
+template <int DK> struct ChainLds {
+    bf16_t sK[RING][CH * DK];     // ring of chunk inputs (slot = chunk % RING)
+    bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
+    bf16x8 sBt[RING][NBF][64];    // K_{c+1} K_c^T W_c
+    bf16_t sV[RING][CH * SL];
+    float sG[RING][CH];           // gamma_r
+    bf16x8 sSf[2][DK / 32][64];   // S_c and R'_c as MFMA operands, by chunk parity
+    bf16x8 sRf[2][2][64];
+    bf16_t sQ[2][32 * DK];        // Q rows of each output wave
+};
+
+// Chain workgroup `bid`.  FUSED: the chunk terms come from workgroups of the
+// same launch; a chunk's terms are read only once its flag carries this call's
+// epoch, with loads that bypass the caches (their writers store the same way).
+template <int DK, bool FUSED>
+__device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid, ChainLds<DK>& lds) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
     constexpr int HKD = NKD / 2;        // ... whose S^T rows one chain wave keeps
     constexpr int HMD = DK / 32;        // 16-row S^T tiles per chain wave
@@ -624,24 +652,22 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
     // (dispatch is round-robin over the 8 XCDs) and its L2 copy of K, Q and the
     // chunk matrices.
     const int G = p.n_seq * H;
-    const int js = blockIdx.x / G;
-    const int h = (blockIdx.x % G) % H;
-    const int s = (blockIdx.x % G) / H;
+    const int js = bid / G;
+    const int h = (bid % G) % H;
+    const int s = (bid % G) / H;
     long start;
     int len, cbase;
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
-
-    // ring of chunk inputs (slot = chunk % RING)
-    __shared__ __attribute__((aligned(16))) bf16_t sK[RING][CH * DK];
-    __shared__ __attribute__((aligned(16))) bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
-    __shared__ __attribute__((aligned(16))) bf16x8 sBt[RING][NBF][64];    // K_{c+1} K_c^T W_c
-    __shared__ __attribute__((aligned(16))) bf16_t sV[RING][CH * SL];
-    __shared__ __attribute__((aligned(16))) float sG[RING][CH];           // gamma_r
-    // S_c and R'_c as MFMA operands, by chunk parity
-    __shared__ __attribute__((aligned(16))) bf16x8 sSf[2][NKD][64];
-    __shared__ __attribute__((aligned(16))) bf16x8 sRf[2][2][64];
-    __shared__ __attribute__((aligned(16))) bf16_t sQ[2][32 * DK];        // Q rows of each output wave
+    auto& sK = lds.sK;
+    auto& sW = lds.sW;
+    auto& sBt = lds.sBt;
+    auto& sV = lds.sV;
+    auto& sG = lds.sG;
+    auto& sSf = lds.sSf;
+    auto& sRf = lds.sRf;
+    auto& sQ = lds.sQ;
+    constexpr int AUX = FUSED ? 17 : 0;   // sc0 sc1: coherent with the writers' stores
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -664,6 +690,7 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
         // waves share the copies: K load groups, W and B fragments with index
         // = loader (mod 4), the two V loads on loaders 2 and 3, gamma on loader 0.
         const int li = wave - 4;
+        int spins = 1 << 22;   // ~0.2 s of sleeping in all; the chunk-terms workgroups never wait
         const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
         const bf16_t* wsB = reinterpret_cast<const bf16_t*>(p.wsB);
         int koff[NCH / 4];   // loop-invariant byte offsets of this lane's K loads within a chunk
@@ -676,17 +703,24 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
         auto issue = [&](int c, auto SLOT, auto LI) {
             constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
             const long sc = slot(c);
+            if constexpr (FUSED) {   // wait for the chunk's terms, within one budget for the whole call
+                while (__hip_atomic_load(&p.flags[sc], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != p.epoch &&
+                       spins > 0) {
+                    --spins;
+                    __builtin_amdgcn_s_sleep(2);
+                }
+            }
             const auto rk = crsrc(p.k, DK, c);
 #pragma unroll
             for (int j = 0; j < NCH / 4; ++j) bdma16(rk, &sK[sl][RPI * (L + 4 * j) * DK], koff[j]);
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
-            for (int f = L; f < NFRAG; f += 4) bdma16(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
+            for (int f = L; f < NFRAG; f += 4) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
             const auto rb = rsrc(wsB + sc * (NBF * 512), NBF * 512 * 2);
 #pragma unroll
-            for (int f = L; f < NBF; f += 4) bdma16(rb, &sBt[sl][f][0], (f * 64 + lane) * 16);
+            for (int f = L; f < NBF; f += 4) bdma16<AUX>(rb, &sBt[sl][f][0], (f * 64 + lane) * 16);
             if constexpr (L >= 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L & 1) * SL], voff);
-            if constexpr (L == 0) bdma4(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+            if constexpr (L == 0) bdma4<AUX>(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
         };
         // After barrier c every wave is done with chunk c-1, whose slot is
         // (c+3) % RING: chunk c+3 is loaded there, and the wait leaves only
@@ -896,7 +930,7 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
             auto load_p = [&](int c, bf16x8(&pa)[NPP]) {
                 const auto rp = rsrc(wsP + slot(c) * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
-                for (int k = 0; k < NPP; ++k) pa[k] = bload16(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
+                for (int k = 0; k < NPP; ++k) pa[k] = bload16<AUX>(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
             };
             auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
@@ -935,11 +969,11 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
                 load_q(min(c + 1, nc - 1));
             };
             bf16x8 pA[NPP], pB[NPP];
+            lds_barrier();   // prologue 1: the loaders have seen chunks 0..2's terms published
             if (nc > 0) {
                 load_p(0, pA);
                 load_q(0);
             }
-            lds_barrier();   // prologue 1
             lds_barrier();   // prologue 2
             for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
                 ostep(c, Ic<0>{}, pA, pB);
@@ -952,6 +986,12 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
         if (wave == 2) run(Ic<0>{});
         else run(Ic<1>{});
     }
+}
+
+template <int DK>
+__global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
+    __shared__ ChainLds<DK> lds;
+    state_chain_bf16<DK, false>(p, blockIdx.x, lds);
 }
 
 // ------------------------------------------------------------------ bf16 chunk terms
@@ -1060,17 +1100,33 @@ __device__ __forceinline__ void store_gram(float (*sA)[CH + 4], bf16_t (*sPb)[CH
         for (int e = 0; e < 4; ++e) sPb[16 * BI[QW + 4 * j] + 4 * lg + e][16 * BJ[QW + 4 * j] + l16] = from_f<bf16_t>(pblk[j][e]);
 }
 
-template <int DK>
-__global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
+// LDS of one chunk-terms work item: phase 1 holds the K, Q and K' tiles; phase
+// 2 reuses the space for A, T (fp32) and P (bf16), and T's bf16 copy over A
+template <int DK> struct TermsLds {
+    static constexpr int PA = CH + 4, PB = CH + 8;   // row pitches of the fp32 and bf16 64 x 64 matrices
+    static constexpr int SZ_TILES = 3 * CH * DK * 2;
+    static constexpr int SZ_MATS = 2 * CH * PA * 4 + CH * PB * 2;
+    __attribute__((aligned(16))) char r0[SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS];
+    double sGl[CH];
+    __attribute__((aligned(16))) float sB[CH];
+    __attribute__((aligned(16))) float sD[CH];
+};
+
+// Chunk terms of work item gi = chunk slot * H + head, by the 4 waves whose
+// threads are tid = 0..255.  store = false computes without writing (a
+// placeholder item that keeps a workgroup's two halves in step).  FUSED: every
+// result is stored with cache-bypassing stores, then the slot's flag is set to
+// the call's epoch.
+template <int DK, bool FUSED>
+__device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi, TermsLds<DK>& lds, const int tid,
+                                                 const bool store) {
     constexpr int NCH = DK / 8;     // 16-byte chunks per K/Q row
     constexpr int RPI = 64 / NCH;   // rows per 1 KB buffer load
     constexpr int TILE = CH * DK;
-    constexpr int PA = CH + 4, PB = CH + 8;   // row pitches of the fp32 and bf16 64 x 64 matrices
-    constexpr int SZ_TILES = 3 * TILE * 2;
-    constexpr int SZ_MATS = 2 * CH * PA * 4 + CH * PB * 2;
-    constexpr int R0 = SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS;
+    constexpr int PA = TermsLds<DK>::PA, PB = TermsLds<DK>::PB;
+    constexpr int AUX = FUSED ? 17 : 0;
     const int H = p.H;
-    const int gc = blockIdx.x / H, h = blockIdx.x % H;
+    const int gc = (int)(gi / H), h = (int)(gi % H);
     int s;
     if (p.ragged) {
         if (gc >= p.chunk_off[p.n_seq]) return;
@@ -1092,11 +1148,10 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     const int n1 = min(CH, len - (c + 1) * CH);   // rows of the next chunk (<= 0: none)
     const long slot = (long)gc * H + h;
 
-    __shared__ __attribute__((aligned(16))) char r0[R0];
-    __shared__ double sGl[CH];
-    __shared__ __attribute__((aligned(16))) float sB[CH];
-    __shared__ __attribute__((aligned(16))) float sD[CH];
-    // phase 1: the K, Q and K' tiles; phase 2: A, T (fp32) and P (bf16); T's bf16 copy over A
+    char* r0 = lds.r0;
+    double* sGl = lds.sGl;
+    float* sB = lds.sB;
+    float* sD = lds.sD;
     bf16_t* sK = reinterpret_cast<bf16_t*>(r0);
     bf16_t* sQ = sK + TILE;
     bf16_t* sKn = sQ + TILE;
@@ -1105,7 +1160,7 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     bf16_t(*sPb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0 + 2 * CH * PA * 4);
     bf16_t(*sTb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0);
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
 
@@ -1141,8 +1196,11 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
         sGl[lane] = x;
         sB[lane] = bv;
         sD[lane] = dec;
-        p.wsG[slot * 2 * CH + lane] = __builtin_amdgcn_exp2f((float)x);
-        p.wsG[slot * 2 * CH + CH + lane] = dec;
+        if (store) {
+            const auto rg = rsrc(p.wsG + slot * 2 * CH, 2 * CH * 4);
+            bstore4<AUX>(__builtin_amdgcn_exp2f((float)x), rg, lane * 4);
+            bstore4<AUX>(dec, rg, (CH + lane) * 4);
+        }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -1232,9 +1290,9 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
     }
     __syncthreads();
 
-    bf16_t* Wg = reinterpret_cast<bf16_t*>(p.wsT) + slot * tp_elems<bf16_t>();
-    bf16_t* Pg = reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>();
-    bf16_t* Bg = reinterpret_cast<bf16_t*>(p.wsB) + slot * (NBF * 64 * 8);
+    const auto rW = rsrc(reinterpret_cast<bf16_t*>(p.wsT) + slot * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
+    const auto rP = rsrc(reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
+    const auto rB = rsrc(reinterpret_cast<bf16_t*>(p.wsB) + slot * (NBF * 64 * 8), NBF * 64 * 8 * 2);
     for (int f = wave; f < NFRAG; f += 4) {
         const int mt = frag_mt(f), kk2 = frag_kk(f), r = 16 * mt + l16;
         // W fragment: D_r T[r][tau] beta_tau
@@ -1243,7 +1301,7 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
         const floatx4 b1 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 16 + 4 * lg]);
         const floatx4 w0 = dr * b0 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 4 * lg]);
         const floatx4 w1 = dr * b1 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 16 + 4 * lg]);
-        *reinterpret_cast<bf16x8*>(Wg + (f * 64 + lane) * 8) = pack_bf16(w0, w1);
+        if (store) bstore16<AUX>(pack_bf16(w0, w1), rW, (f * 64 + lane) * 16);
         // P' fragment from (T^T P^T) tiles (tau block 2 kk2 + hb, token block mt)
         floatx4 pt[2];
 #pragma unroll
@@ -1260,7 +1318,7 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
             }
             pt[hb] *= hb ? b1 : b0;
         }
-        *reinterpret_cast<bf16x8*>(Pg + (f * 64 + lane) * 8) = pack_bf16(pt[0], pt[1]);
+        if (store) bstore16<AUX>(pack_bf16(pt[0], pt[1]), rP, (f * 64 + lane) * 16);
     }
     {   // B fragments (row block mt = wave) from B^T = diag(beta) T^T (diag(D) E^T) tiles
         // (tau block bt, token block mt); T^T's contraction order matches def's
@@ -1278,7 +1336,43 @@ __global__ __launch_bounds__(NT, 2) void k_chunk_terms_bf16(Params p) {
         }
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
-            *reinterpret_cast<bf16x8*>(Bg + ((2 * wave + kk) * 64 + lane) * 8) = pack_bf16(bt4[2 * kk], bt4[2 * kk + 1]);
+            if (store) bstore16<AUX>(pack_bf16(bt4[2 * kk], bt4[2 * kk + 1]), rB, ((2 * wave + kk) * 64 + lane) * 16);
+    }
+    if constexpr (FUSED) {   // publish: every wave's stores are complete before the flag is set
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (tid == 0 && store) __hip_atomic_store(&p.flags[slot], p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+template <int DK>
+__global__ __launch_bounds__(NT, 3) void k_chunk_terms_bf16(Params p) {
+    __shared__ TermsLds<DK> lds;
+    chunk_terms_bf16<DK, false>(p, blockIdx.x, lds, threadIdx.x, true);
+}
+
+// One launch for the whole bf16 prefill: workgroups [0, npw) form chunk terms
+// (two work items per workgroup, one per half of its waves, walking the items
+// in chunk order), the rest are chain workgroups.  The chunk-terms workgroups
+// are dispatched first and never wait, so the chain workgroups' waits end
+// whatever number of workgroups the device holds at once.
+template <int DK>
+__global__ __launch_bounds__(NT_CHAIN) void k_prefill_fused_bf16(Params p) {
+    static_assert(NT_CHAIN == 2 * NT, "two work items per chunk-terms workgroup");
+    __shared__ union Lds {
+        ChainLds<DK> c;
+        TermsLds<DK> t[2];
+    } lds;
+    if ((int)blockIdx.x < p.npw) {
+        const int half = threadIdx.x / NT;
+        const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
+        for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
+            const long gi = min(k + half, items - 1);   // both halves run every step together
+            chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
+            __syncthreads();   // the next item reuses the LDS
+        }
+    } else {
+        state_chain_bf16<DK, true>(p, blockIdx.x - p.npw, lds.c);
     }
 }
 
@@ -1339,7 +1433,7 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
     long slots;          // chunk slots per head
-    size_t meta, G, T, P, B, total;
+    size_t meta, G, T, P, B, F, total;
 };
 
 // Workspace layout; returns false for arguments that are out of range.
@@ -1357,17 +1451,57 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
     L->B = L->P + round_up(per * tp * esz, 256);
-    L->total = L->B + (io == GDN_BF16 ? round_up(per * NBF * 512 * 2, 256) : 0);
+    L->F = L->B + (io == GDN_BF16 ? round_up(per * NBF * 512 * 2, 256) : 0);
+    L->total = L->F + (io == GDN_BF16 ? round_up(per * sizeof(uint64_t), 256) : 0);
     return true;
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+// Tag of one call's chunk-term flags: a per-process random high half and a call
+// counter, never 0 or all ones (what a cleared or 0xFF-filled workspace holds).
+uint64_t next_epoch() {
+    static uint64_t salt = 0;
+    static uint64_t counter = 0;
+    if (salt == 0) {
+        uint64_t x = (uint64_t)(uintptr_t)&counter ^ ((uint64_t)time(nullptr) << 20) ^ 0x9e3779b97f4a7c15ull;
+        x ^= x >> 33; x *= 0xff51afd7ed558ccdull; x ^= x >> 33;
+        salt = (x & 0x7ffffffeull) + 1;
+    }
+    return (salt << 32) | (uint32_t)(++counter);
+}
+
 template <typename IO, int DK>
-void launch_prefill(const Params& p, long slots, hipStream_t st) {
+void launch_prefill(Params p, long slots, hipStream_t st) {
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(64), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
                            p.seq_len, p.chunk_off);
+    if (sizeof(IO) == 2) {
+        // one launch with the chunk terms formed beside the chain when enough
+        // compute units are left over for them
+        const long nchain = (long)p.n_seq * p.H * (p.DV / SL);
+        const long items = slots * p.H;
+        const long spare = (long)device_cus() - nchain;
+        if (spare >= 8 && items > 0) {
+            p.npw = (int)std::min(spare, (items + 1) / 2);
+            p.epoch = next_epoch();
+            hipLaunchKernelGGL((k_prefill_fused_bf16<DK>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
+            return;
+        }
+    }
     if (slots > 0 && p.T > 0) {
         if (sizeof(IO) == 2)
             hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
@@ -1477,8 +1611,11 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
     p.wsB = ws + L.B;
+    p.flags = reinterpret_cast<uint64_t*>(ws + L.F);
+    p.epoch = 0;
+    p.npw = 0;
     p.scale = scale;
-    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsB = nullptr; }
+    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsB = nullptr; p.flags = nullptr; }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
