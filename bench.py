@@ -44,6 +44,24 @@ def algorithmic(w, lens, dk, dv, H, io, s0, decode=False):
     return byts, flops * H
 
 
+def measured_traffic(workload):
+    """HBM bytes per call from the committed rocprofv3 counter summary, if it was taken on this kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "%s_traffic.md" % workload)
+    src = os.path.join(ROOT, "paper_2607_14568_amd", "csrc", "gdn.hip")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get("kernel source sha256") != sha or "HBM bytes per call" not in fields:
+        return None
+    return float(fields["HBM bytes per call"])
+
+
 def cpu_baseline(w, x, budget_s):
     """The fp64 oracle, as it stands, on this host's cores, on the same inputs."""
     import oracle
@@ -87,6 +105,8 @@ def main():
     ap.add_argument("--sets", type=int, default=4, help="rotating resident input sets")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="run one plain device copy of MIB MiB before timing (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
@@ -143,6 +163,12 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    if args.copy_calibration > 0:   # a copy of known size: its FETCH_SIZE / WRITE_SIZE calibrate the counters
+        src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # per-call durations with HIP events on the stream the library launches on
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
@@ -170,7 +196,7 @@ def main():
         roof = {"bound": "mfma", "achieved": flops / avg_call_s / 1e12, "peak": PEAK[w.io] / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = None if w.decode else measured_traffic(w.name)
     roof["kernel"] = "one gdn_decode_step call" if w.decode else \
         "one gdn_chunk_prefill call (k_prefill_fused_bf16 for bf16 io)"
     roof["alg_bytes"] = byts

@@ -203,3 +203,18 @@ def test_invalid_ragged_offsets_are_clamped_not_faulting():
                                      None, cu_seqlens=[0, 150, 150, 200])
     assert oracle.max_rel_err(f64(o), ref_o) < 2e-4
     assert oracle.max_rel_err(f64(ST), ref_S) < 2e-4
+
+
+def test_workspace_reused_across_calls_with_different_inputs():
+    """One workspace, three calls with different inputs and shapes: no call may read another call's chunk matrices."""
+    need = max(gdn.gdn_chunk_prefill_workspace_bytes(1, T, 4, 128, 128, 64, 0, gdn.GDN_BF16) for T in (300, 200))
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    for i, (T, seed) in enumerate([(300, 51), (300, 52), (200, 53)]):
+        x = inputs.make_prefill(B=1, T=T, H=4, dk=128, dv=128, io="bf16", seed=seed, s0_std=0.05)
+        print("case: call %d T=%d seed=%d" % (i, T, seed), flush=True)
+        d = _dev(x)
+        o, ST = gdn.gdn_chunk_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], workspace=ws)
+        torch.cuda.synchronize()
+        o_ref, ST_ref = _ref(x)
+        assert oracle.max_rel_err(f64(o), o_ref) < TOL["bf16"], i
+        assert oracle.max_rel_err(f64(ST), ST_ref) < TOL["bf16"], i
