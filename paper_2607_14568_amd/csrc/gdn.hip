@@ -134,6 +134,9 @@ struct Params {
     int32_t* seq_start;
     int32_t* seq_len;
     int32_t* chunk_off;  // [n_seq + 1], first chunk slot of each sequence
+    int32_t* seq_perm;   // ragged: sequences by chunk count, longest first
+    int32_t* cprefix;    // ragged: [cpt + 1] (sequence, chunk index < c) pair counts
+    int cpt;             // chunks of the longest possible sequence
     float* wsG;          // [slot][H][128]: gamma_r = exp(G_r), then exp(G_n - G_r)
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
@@ -143,6 +146,29 @@ struct Params {
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
     float scale;
 };
+
+// Sequence at rank r when sequences are taken longest first (ragged), else r.
+__device__ __forceinline__ int seq_at_rank(const Params& p, int r) { return p.ragged ? p.seq_perm[r] : r; }
+
+// Work item k of the chunk terms in the order the chains consume them: chunk
+// index within its sequence, then sequence rank, then head.
+__device__ __forceinline__ long item_slot(const Params& p, long k) {
+    const int H = p.H;
+    int c, r;
+    if (p.ragged) {
+        int lo = 0, hi = p.cpt;   // largest c with cprefix[c] * H <= k
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if ((long)p.cprefix[mid] * H <= k) lo = mid; else hi = mid;
+        }
+        c = lo;
+        r = (int)((k - (long)p.cprefix[c] * H) / H);
+        return ((long)p.chunk_off[p.seq_perm[r]] + c) * H + (int)(k % H);
+    }
+    c = (int)(k / ((long)p.n_seq * H));
+    r = (int)((k / H) % p.n_seq);
+    return ((long)r * p.NC + c) * H + (int)(k % H);
+}
 
 __device__ __forceinline__ void seq_info(const Params& p, int s, long& start, int& len, int& cbase) {
     if (p.ragged) {
@@ -158,20 +184,77 @@ __device__ __forceinline__ void seq_info(const Params& p, int s, long& start, in
 
 // Sanitises the ragged offsets into a nondecreasing partition of [0, T] and
 // lays out one workspace slot per chunk of every sequence.
-__global__ void k_ragged_setup(const int32_t* cu, int n_seq, int T, int32_t* seq_start,
-                               int32_t* seq_len, int32_t* chunk_off) {
-    if (blockIdx.x != 0 || threadIdx.x != 0) return;
-    int b = min(max(cu[0], 0), T);
-    int acc = 0;
-    chunk_off[0] = 0;
-    for (int s = 0; s < n_seq; ++s) {
-        int e = min(max(cu[s + 1], b), T);
-        seq_start[s] = b;
-        seq_len[s] = e - b;
-        acc += (e - b + CH - 1) / CH;
-        chunk_off[s + 1] = acc;
-        b = e;
+// Exclusive scan of x[0..n) in place by one workgroup of NSET threads (each
+// thread scans a contiguous segment; the segment totals by wave shuffles).
+// reverse: the sum runs from the top index down.
+constexpr int NSET = 1024;
+__device__ void block_scan(int32_t* x, int n, bool reverse, int* part) {
+    const int t = threadIdx.x, seg = (n + NSET - 1) / NSET;
+    const int lo = t * seg, hi = min(n, lo + seg);
+    auto at = [&](int i) -> int32_t& { return x[reverse ? n - 1 - i : i]; };
+    int sum = 0;
+    for (int i = lo; i < hi; ++i) sum += at(i);
+    // exclusive scan of the segment totals: within each wave by shuffles, then over the wave totals
+    const int lane = t & 63, wv = t >> 6;
+    int inc = sum;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(inc, off, 64);
+        if (lane >= off) inc += y;
     }
+    if (lane == 63) part[wv] = inc;
+    __syncthreads();
+    if (t == 0) {
+        int acc = 0;
+        for (int i = 0; i < NSET / 64; ++i) {
+            const int v = part[i];
+            part[i] = acc;
+            acc += v;
+        }
+    }
+    __syncthreads();
+    int acc = part[wv] + inc - sum;
+    for (int i = lo; i < hi; ++i) {
+        const int v = at(i);
+        at(i) = acc;
+        acc += v;
+    }
+    __syncthreads();
+}
+
+// Ragged sequence table: clamped starts and lengths, first chunk slot of each
+// sequence; the sequences ordered by chunk count, longest first (perm); and
+// prefix[c] = number of (sequence, chunk index c' < c) pairs, i.e. the sum over
+// c' < c of the number of sequences with more than c' chunks.  hist: cpt + 2
+// ints of scratch.  One workgroup of NSET threads.
+__global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_seq, int T, int32_t* seq_start,
+                                                      int32_t* seq_len, int32_t* chunk_off, int32_t* perm,
+                                                      int32_t* prefix, int32_t* hist, int cpt) {
+    __shared__ int part[NSET];
+    const int t = threadIdx.x;
+    if (t == 0) {   // offsets clamped into a partition of [0, T]
+        int b = min(max(cu[0], 0), T);
+        int acc = 0;
+        chunk_off[0] = 0;
+        for (int s = 0; s < n_seq; ++s) {
+            const int e = min(max(cu[s + 1], b), T);
+            seq_start[s] = b;
+            seq_len[s] = e - b;
+            acc += (e - b + CH - 1) / CH;
+            chunk_off[s + 1] = acc;
+            b = e;
+        }
+    }
+    for (int c = t; c <= cpt + 1; c += NSET) hist[c] = 0;
+    __syncthreads();
+    for (int s = t; s < n_seq; s += NSET) atomicAdd(&hist[(seq_len[s] + CH - 1) / CH], 1);   // counts <= cpt
+    __syncthreads();
+    // first rank of each chunk count, longest first: hist[n] <- #sequences with more than n chunks
+    block_scan(hist, cpt + 1, true, part);
+    for (int c = t; c <= cpt; c += NSET) prefix[c] = hist[c];
+    __syncthreads();
+    for (int s = t; s < n_seq; s += NSET) perm[atomicAdd(&hist[(seq_len[s] + CH - 1) / CH], 1)] = s;
+    block_scan(prefix, cpt + 1, false, part);
 }
 
 // Stage rows [t0, t0+n) of a [*, H, D] io tensor (head h) into an LDS tile
@@ -647,14 +730,14 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     constexpr int NCH = DK / 8;         // 16-byte chunks per K row
     constexpr int RPI = 64 / NCH;       // rows per 1 KB direct load
     const int H = p.H, DV = p.DV;
-    // Slices of one (sequence, head) are blockIdx values congruent modulo the
-    // number of (sequence, head) pairs, so with 8 | n_seq*H they share an XCD
-    // (dispatch is round-robin over the 8 XCDs) and its L2 copy of K, Q and the
-    // chunk matrices.
-    const int G = p.n_seq * H;
-    const int js = bid / G;
-    const int h = (bid % G) % H;
-    const int s = (bid % G) / H;
+    // Workgroups go longest sequence first (ragged), and within a sequence
+    // slice-major, so the slices of one (sequence, head) are congruent modulo H:
+    // with 8 | H they share an XCD (dispatch is round-robin over the 8 XCDs) and
+    // its L2 copy of K, Q and the chunk matrices.
+    const int per = H * (DV / SL);
+    const int s = seq_at_rank(p, bid / per);
+    const int js = (bid % per) / H;
+    const int h = bid % H;
     long start;
     int len, cbase;
     seq_info(p, s, start, len, cbase);
@@ -1367,7 +1450,7 @@ __global__ __launch_bounds__(NT_CHAIN) void k_prefill_fused_bf16(Params p) {
         const int half = threadIdx.x / NT;
         const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
         for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
-            const long gi = min(k + half, items - 1);   // both halves run every step together
+            const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
             chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
             __syncthreads();   // the next item reuses the LDS
         }
@@ -1446,7 +1529,7 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     if (L->slots * (long)H > (1L << 24)) return false;
     const size_t per = (size_t)L->slots * H;
     L->meta = 0;
-    L->G = n_seqs > 0 ? round_up((size_t)3 * (n_seqs + 1) * sizeof(int32_t), 256) : 0;
+    L->G = n_seqs > 0 ? round_up(((size_t)4 * (n_seqs + 1) + 2 * (size_t)(cpt + 2)) * sizeof(int32_t), 256) : 0;
     L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
@@ -1487,15 +1570,17 @@ uint64_t next_epoch() {
 template <typename IO, int DK>
 void launch_prefill(Params p, long slots, hipStream_t st) {
     if (p.ragged)
-        hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(64), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
-                           p.seq_len, p.chunk_off);
+        hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
+                           p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
     if (sizeof(IO) == 2) {
-        // one launch with the chunk terms formed beside the chain when enough
-        // compute units are left over for them
+        // one launch with the chunk terms formed beside the chain when it leaves
+        // a quarter of the compute units free; otherwise the chunk terms first
+        // (three workgroups per CU) and the chain after, longest sequence first
         const long nchain = (long)p.n_seq * p.H * (p.DV / SL);
         const long items = slots * p.H;
-        const long spare = (long)device_cus() - nchain;
-        if (spare >= 8 && items > 0) {
+        const long cus = device_cus();
+        const long spare = cus - nchain;   // CUs the chain leaves free (one chain workgroup per CU)
+        if (spare >= 8 && 4 * spare >= cus && items > 0) {
             p.npw = (int)std::min(spare, (items + 1) / 2);
             p.epoch = next_epoch();
             hipLaunchKernelGGL((k_prefill_fused_bf16<DK>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
@@ -1607,6 +1692,9 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.seq_start = p.ragged ? reinterpret_cast<int32_t*>(ws) : nullptr;
     p.seq_len = p.ragged ? p.seq_start + (n_seqs + 1) : nullptr;
     p.chunk_off = p.ragged ? p.seq_len + (n_seqs + 1) : nullptr;
+    p.seq_perm = p.ragged ? p.chunk_off + (n_seqs + 1) : nullptr;
+    p.cprefix = p.ragged ? p.seq_perm + (n_seqs + 1) : nullptr;
+    p.cpt = (T + CH - 1) / CH;
     p.wsG = reinterpret_cast<float*>(ws + L.G);
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
