@@ -144,6 +144,7 @@ struct Params {
     uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
     uint64_t epoch;      // per-call tag of those flags
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
+    int xcd_items;       // fused bf16 launch: chunk-terms items assigned by XCD (dense, 8 | H, 8 | npw)
     float scale;
 };
 
@@ -1005,7 +1006,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 const int r = RPI * j + lane / NCH;
                 qoff[j] = ((32 * ow + r) * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             }
-            auto load_q = [&](int c) {   // last global load of a step: the next step waits for all
+            auto load_q = [&](int c) {
                 const auto rq = crsrc(p.q, DK, c);
 #pragma unroll
                 for (int j = 0; j < 32 / RPI; ++j) bdma16(rq, sq + RPI * j * DK, qoff[j]);
@@ -1015,11 +1016,15 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int k = 0; k < NPP; ++k) pa[k] = bload16<AUX>(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
             };
+            // Per chunk this wave issues, in order: the next chunk's Q copy, its P'
+            // loads, then two output stores (buffer stores, so tokens past the
+            // chunk end are dropped by the descriptor and the count is fixed).
+            // Global memory operations complete in issue order, so at the next
+            // chunk's start waiting until NPP remain covers the Q copy.
             auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
-                const int n = rows(c);
                 lds_barrier();   // barrier c: S_c and R'_c visible
-                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // Q_c staged, P'_c loaded
+                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NPP) : "memory");   // Q_c staged
                 bf16x8 qa[2][NKD];
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
@@ -1027,8 +1032,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     for (int kk = 0; kk < NKD; ++kk)
                         qa[i][kk] = *reinterpret_cast<const bf16x8*>(sq + kq(16 * i + l16, 32 * kk + 8 * lg));
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // staging area read: free for Q_{c+1}
+                load_q(min(c + 1, nc - 1));
                 load_p(min(c + 1, nc - 1), pn);
                 const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
+                const auto ro = crsrc(p.o, DV, c);
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int mt = 2 * ow + i, tok = 16 * mt + l16;
@@ -1045,17 +1052,16 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                         op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pa[2 * i + 1], op, 0, 0, 0);
                     }
                     const floatx4 ov = p.scale * (gm * oq + op);   // value channels 4 lg .. 4 lg + 3 of token tok
-                    if (tok < n)
-                        *reinterpret_cast<bf16x4*>(go + ((tok0(c) + tok) * H + h) * (long)DV + js * SL + 4 * lg) =
-                            __builtin_convertvector(ov, bf16x4);
+                    typedef int int2v __attribute__((ext_vector_type(2)));
+                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, __builtin_convertvector(ov, bf16x4)), ro,
+                                                          (tok * H * DV + js * SL + 4 * lg) * 2, 0, 0);
                 }
-                load_q(min(c + 1, nc - 1));
             };
             bf16x8 pA[NPP], pB[NPP];
             lds_barrier();   // prologue 1: the loaders have seen chunks 0..2's terms published
             if (nc > 0) {
-                load_p(0, pA);
                 load_q(0);
+                load_p(0, pA);
             }
             lds_barrier();   // prologue 2
             for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
@@ -1448,11 +1454,28 @@ __global__ __launch_bounds__(NT_CHAIN) void k_prefill_fused_bf16(Params p) {
     } lds;
     if ((int)blockIdx.x < p.npw) {
         const int half = threadIdx.x / NT;
-        const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
-        for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
-            const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
-            chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
-            __syncthreads();   // the next item reuses the LDS
+        if (p.xcd_items) {
+            // Dispatch deals workgroups to the 8 XCDs round-robin, so chain
+            // workgroups of head h sit on XCD (npw + h) % 8.  Workgroup b forms
+            // the items of heads h = (b - npw) mod 8 (+ 8 u), in chunk order, on
+            // the XCD whose L2 then serves those chains.
+            const int H = p.H, hu = H / 8, q = blockIdx.x / 8, nq = p.npw / 8;
+            const int h0 = ((int)(blockIdx.x % 8) - p.npw % 8 + 8) % 8;
+            const long items = (long)p.NC * p.n_seq * hu;   // per XCD
+            for (long k = 2L * q; k < items; k += 2L * nq) {
+                const long j = min(k + half, items - 1);
+                const int c = (int)(j / ((long)p.n_seq * hu)), r = (int)((j / hu) % p.n_seq), u = (int)(j % hu);
+                const long gi = ((long)r * p.NC + c) * H + h0 + 8 * u;
+                chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
+                __syncthreads();   // the next item reuses the LDS
+            }
+        } else {
+            const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
+            for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
+                const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
+                chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
+                __syncthreads();   // the next item reuses the LDS
+            }
         }
     } else {
         state_chain_bf16<DK, true>(p, blockIdx.x - p.npw, lds.c);
@@ -1582,6 +1605,8 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         const long spare = cus - nchain;   // CUs the chain leaves free (one chain workgroup per CU)
         if (spare >= 8 && 4 * spare >= cus && items > 0) {
             p.npw = (int)std::min(spare, (items + 1) / 2);
+            p.xcd_items = !p.ragged && p.H % 8 == 0 && p.npw >= 8;
+            if (p.xcd_items) p.npw &= ~7;
             p.epoch = next_epoch();
             hipLaunchKernelGGL((k_prefill_fused_bf16<DK>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
             return;
@@ -1702,6 +1727,7 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.flags = reinterpret_cast<uint64_t*>(ws + L.F);
     p.epoch = 0;
     p.npw = 0;
+    p.xcd_items = 0;
     p.scale = scale;
     if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsB = nullptr; p.flags = nullptr; }
 
