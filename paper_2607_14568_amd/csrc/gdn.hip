@@ -458,7 +458,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 // ------------------------------------------------------------------ state chain
 // One workgroup per (sequence, head, 16-row slice of S); chunks in order.
 template <typename IO, int DK>
-__global__ __launch_bounds__(NT) void k_state_chain(Params p) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
     using M = Mma<IO>;
     constexpr int PAD = 16 / sizeof(IO);
     constexpr int NMT = DK / 16;          // 16-row tiles of S^T
@@ -487,35 +487,97 @@ __global__ __launch_bounds__(NT) void k_state_chain(Params p) {
     for (int i = tid; i < SL * DK; i += NT)
         sS[i / DK][i % DK] = p.S0 ? p.S0[srow0 + i] : 0.f;
 
-    const IO* gv = reinterpret_cast<const IO*>(p.v);
     IO* go = reinterpret_cast<IO*>(p.o);
 
-    for (int c = 0; c < nc; ++c) {
+    // One chunk's inputs, this thread's share, held in registers: the next
+    // chunk's loads are issued right after the current chunk is written to LDS,
+    // so their latency overlaps the current chunk's arithmetic.
+    constexpr int VE = 16 / sizeof(IO);             // elements per 16-byte load
+    constexpr int NKV = CH * (DK / VE) / NT;        // K (and Q) loads per thread
+    constexpr int NTV = CH * (CH / VE) / NT;        // T (and P) loads per thread
+    constexpr int VPV = SL / VE;                    // loads per V row slice
+    constexpr int NVV = (CH * VPV + NT - 1) / NT;   // V loads per thread
+    static_assert(CH * (DK / VE) % NT == 0 && CH * (CH / VE) % NT == 0, "loads per thread");
+    struct Pre {
+        uint4 k[NKV], q[NKV], t[NTV], pp[NTV], v[NVV];
+        float gam, dec, beta;
+    };
+    // buffer loads: one lane offset per tensor, rows past the chunk end read as zeros
+    auto rs = [](const void* base, long bytes) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (uint32_t)bytes, 0x00020000);
+    };
+    auto ld = [](__amdgpu_buffer_rsrc_t r, int voff) {   // the whole offset in voff: it is what the range check sees
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+    };
+    const int kvo = ((tid / (DK / VE)) * H * DK + (tid % (DK / VE)) * VE) * (int)sizeof(IO);
+    const int vvo = ((tid / VPV) * H * DV + js * SL + (tid % VPV) * VE) * (int)sizeof(IO);
+    auto load = [&](int c, Pre& x) {
         const long t0 = start + (long)c * CH;
         const int n = min(CH, len - c * CH);
         const long slot = (long)(cbase + c) * H + h;
-        __syncthreads();   // previous chunk done with every tile
-        stage_rows<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), t0, n, H, h);
-        stage_rows<IO, DK, DK + PAD>(sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
-        {
-            constexpr int VE = 16 / sizeof(IO), VPR = CH / VE;
-            const IO* Tg = reinterpret_cast<const IO*>(p.wsT) + slot * tp_elems<IO>();
-            const IO* Pg = reinterpret_cast<const IO*>(p.wsP) + slot * tp_elems<IO>();
-            for (int i = tid; i < CH * VPR; i += NT) {
-                const int r = i / VPR, cv = i % VPR;
-                *reinterpret_cast<uint4*>(&sT[r][cv * VE]) = *reinterpret_cast<const uint4*>(Tg + r * CH + cv * VE);
-                *reinterpret_cast<uint4*>(&sP[r][cv * VE]) = *reinterpret_cast<const uint4*>(Pg + r * CH + cv * VE);
+        const long rb = (long)(n - 1) * H + 1;   // rows of the head's chunk, in [T][H] rows
+        const auto rk = rs(reinterpret_cast<const IO*>(p.k) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
+        const auto rq = rs(reinterpret_cast<const IO*>(p.q) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
+#pragma unroll
+        for (int j = 0; j < NKV; ++j) {
+            const int so = (NT / (DK / VE)) * j * H * DK * (int)sizeof(IO);
+            x.k[j] = ld(rk, kvo + so);
+            x.q[j] = ld(rq, kvo + so);
+        }
+        const auto rt = rs(reinterpret_cast<const IO*>(p.wsT) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
+        const auto rp = rs(reinterpret_cast<const IO*>(p.wsP) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
+#pragma unroll
+        for (int j = 0; j < NTV; ++j) {
+            x.t[j] = ld(rt, tid * 16 + NT * 16 * j);
+            x.pp[j] = ld(rp, tid * 16 + NT * 16 * j);
+        }
+        const auto rv = rs(reinterpret_cast<const IO*>(p.v) + (t0 * H + h) * DV, rb * DV * sizeof(IO));
+#pragma unroll
+        for (int j = 0; j < NVV; ++j)
+            x.v[j] = tid + NT * j < CH * VPV ? ld(rv, vvo + (NT / VPV) * j * H * DV * (int)sizeof(IO)) : make_uint4(0, 0, 0, 0);
+        if (tid < CH) {
+            x.gam = p.wsG[slot * 2 * CH + tid];
+            x.dec = p.wsG[slot * 2 * CH + CH + tid];
+            x.beta = tid < n ? p.beta[(t0 + tid) * H + h] : 0.f;
+        }
+    };
+    auto store = [&](const Pre& x) {
+#pragma unroll
+        for (int j = 0; j < NKV; ++j) {
+            const int i = tid + NT * j, r = i / (DK / VE), cv = i % (DK / VE);
+            *reinterpret_cast<uint4*>(&sK[r][cv * VE]) = x.k[j];
+            *reinterpret_cast<uint4*>(&sQ[r][cv * VE]) = x.q[j];
+        }
+#pragma unroll
+        for (int j = 0; j < NTV; ++j) {
+            const int i = tid + NT * j, r = i / (CH / VE), cv = i % (CH / VE);
+            *reinterpret_cast<uint4*>(&sT[r][cv * VE]) = x.t[j];
+            *reinterpret_cast<uint4*>(&sP[r][cv * VE]) = x.pp[j];
+        }
+#pragma unroll
+        for (int j = 0; j < NVV; ++j) {
+            const int i = tid + NT * j, r = i / VPV, cv = i % VPV;
+            if (i < CH * VPV) {
+                const IO* e = reinterpret_cast<const IO*>(&x.v[j]);
+#pragma unroll
+                for (int u = 0; u < VE; ++u) sV[r][cv * VE + u] = to_f(e[u]);
             }
         }
-        for (int i = tid; i < CH * SL; i += NT) {
-            const int r = i / SL, j = i % SL;
-            sV[r][j] = (r < n) ? to_f(gv[((t0 + r) * H + h) * (long)DV + js * SL + j]) : 0.f;
-        }
         if (tid < CH) {
-            sGam[tid] = p.wsG[slot * 2 * CH + tid];
-            sDec[tid] = p.wsG[slot * 2 * CH + CH + tid];
-            sBeta[tid] = (tid < n) ? p.beta[(t0 + tid) * H + h] : 0.f;
+            sGam[tid] = x.gam;
+            sDec[tid] = x.dec;
+            sBeta[tid] = x.beta;
         }
+    };
+
+    Pre pre;
+    if (nc > 0) load(0, pre);
+    for (int c = 0; c < nc; ++c) {
+        const long t0 = start + (long)c * CH;
+        const int n = min(CH, len - c * CH);
+        __syncthreads();   // previous chunk done with every tile
+        store(pre);
+        if (c + 1 < nc) load(c + 1, pre);
         __syncthreads();
 
         // X = K S^T (tokens of tile `wave` x 16 value channels)
