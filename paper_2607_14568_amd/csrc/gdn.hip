@@ -60,41 +60,11 @@ template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float f) {
 }
 
 // ------------------------------------------------------------------ MFMA 16x16
-// Output layout of both instructions: lane l holds D[4*(l/16) + e][l % 16], e = 0..3.
-// Operand layout: lane l feeds row (A) / column (B) l % 16 and KL contraction
-// elements; which contraction indices a lane's elements stand for is a free
-// choice as long as A and B agree.  Here element e of lane group lg = l/16 in
-// step kk is contraction index kk*KS + lg*KL + e.
-template <typename IO> struct Mma;
-
-template <> struct Mma<bf16_t> {
-    static constexpr int KS = 32;  // contraction length per instruction
-    static constexpr int KL = 8;   // contraction elements per lane
-    typedef bf16x8 frag;
-    __device__ static __forceinline__ floatx4 mma(frag a, frag b, floatx4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-    }
-    __device__ static __forceinline__ frag load(const bf16_t* p) {   // 16-byte aligned
-        return __builtin_bit_cast(frag, *reinterpret_cast<const short8*>(p));
-    }
-    __device__ static __forceinline__ frag pack(const float* x) {
-        short8 s;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s[e] = (short)from_f<bf16_t>(x[e]);
-        return __builtin_bit_cast(frag, s);
-    }
-};
-
-template <> struct Mma<float> {
-    static constexpr int KS = 4;
-    static constexpr int KL = 1;
-    typedef float frag;
-    __device__ static __forceinline__ floatx4 mma(frag a, frag b, floatx4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-    }
-    __device__ static __forceinline__ frag load(const float* p) { return *p; }
-    __device__ static __forceinline__ frag pack(const float* x) { return x[0]; }
-};
+// Output layout of the 16x16 instructions (fp32 16x16x4, bf16 16x16x32): lane l
+// holds D[4*(l/16) + e][l % 16], e = 0..3.  Lane l feeds row (A) / column (B)
+// l % 16 and 1 (fp32) or 8 (bf16) contraction elements; which contraction
+// indices a lane's elements stand for is a free choice as long as A and B agree.
+__device__ __forceinline__ floatx4 f4(const void* ptr) { return *reinterpret_cast<const floatx4*>(ptr); }
 
 // Fragment order of the lower-triangular 64x64 matrices T and P for bf16 io.
 // A 16x16x32 MFMA over a 64-long token contraction needs, for output row tile
@@ -258,25 +228,41 @@ __global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_
     block_scan(prefix, cpt + 1, false, part);
 }
 
-// Stage rows [t0, t0+n) of a [*, H, D] io tensor (head h) into an LDS tile
-// [64][LD]; rows n..63 are zero.
+// Stage rows [t0, t0+n) of two [*, H, D] io tensors (head h) into LDS tiles
+// [64][LD]; rows n..63 are zero.  Every load is issued before the first LDS
+// store, so the tiles cost one memory latency rather than one per pass.
 template <typename IO, int D, int LD>
-__device__ __forceinline__ void stage_rows(IO (*dst)[LD], const IO* src, long t0, int n, int H, int h) {
+__device__ __forceinline__ void stage_rows2(IO (*dA)[LD], const IO* sA, IO (*dB)[LD], const IO* sB, long t0, int n,
+                                            int H, int h) {
     constexpr int VE = 16 / sizeof(IO);
     constexpr int VPR = D / VE;
-    for (int i = threadIdx.x; i < CH * VPR; i += NT) {
-        const int r = i / VPR, cv = i % VPR;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (r < n) val = *reinterpret_cast<const uint4*>(src + ((t0 + r) * H + h) * (long)D + cv * VE);
-        *reinterpret_cast<uint4*>(&dst[r][cv * VE]) = val;
+    constexpr int NPT = (CH * VPR + NT - 1) / NT;
+    uint4 a[NPT], b[NPT];
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+        const int i = threadIdx.x + NT * j, r = i / VPR, cv = i % VPR;
+        a[j] = b[j] = make_uint4(0, 0, 0, 0);
+        if (i < CH * VPR && r < n) {
+            const long off = ((t0 + r) * H + h) * (long)D + cv * VE;
+            a[j] = *reinterpret_cast<const uint4*>(sA + off);
+            b[j] = *reinterpret_cast<const uint4*>(sB + off);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+        const int i = threadIdx.x + NT * j, r = i / VPR, cv = i % VPR;
+        if (i < CH * VPR) {
+            *reinterpret_cast<uint4*>(&dA[r][cv * VE]) = a[j];
+            *reinterpret_cast<uint4*>(&dB[r][cv * VE]) = b[j];
+        }
     }
 }
 
-// ------------------------------------------------------------------ chunk terms
-// One workgroup per (chunk slot, head): G, T = (I+A)^{-1} and P for one chunk.
-template <typename IO, int DK>
+// ------------------------------------------------------------------ fp32 chunk terms
+// One workgroup per (chunk slot, head), fp32 io: G, T = (I+A)^{-1} and P for one chunk.
+template <int DK>
 __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
-    using M = Mma<IO>;
+    using IO = float;
     constexpr int PAD = 16 / sizeof(IO);
     const int H = p.H;
     const int slot_x = blockIdx.x;
@@ -335,8 +321,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         p.wsG[slot * 2 * CH + lane] = expf((float)x);
         p.wsG[slot * 2 * CH + CH + lane] = expf((float)(xn - x));
     }
-    stage_rows<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), t0, n, H, h);
-    stage_rows<IO, DK, DK + PAD>(sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
+    stage_rows2<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
     __syncthreads();
 
     // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P)
@@ -346,12 +331,13 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         while (t > bi) { t -= bi + 1; ++bi; }
         const int bj = t;
         const IO(*X)[DK + PAD] = which ? sQ : sK;
+        // instruction 4 j + e: lane group lg carries contraction index 16 j + 4 lg + e
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < DK / M::KS; ++kk) {
-            const auto a = M::load(&X[bi * 16 + l16][kk * M::KS + lg * M::KL]);
-            const auto b = M::load(&sK[bj * 16 + l16][kk * M::KS + lg * M::KL]);
-            acc = M::mma(a, b, acc);
+        for (int j = 0; j < DK / 16; ++j) {
+            const floatx4 a4 = f4(&X[bi * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sK[bj * 16 + l16][16 * j + 4 * lg]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], acc, 0, 0, 0);
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -407,59 +393,20 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
         __syncthreads();
     }
-    if (sizeof(IO) == 4) {
-        // fp32 io: T and P as row-major squares, zero above the diagonal blocks
-        for (int i = tid; i < CH * CH; i += NT) {
-            const int r = i / CH, cc = i % CH;
-            const bool up = (cc >> 4) > (r >> 4);
-            Tg[i] = from_f<IO>(up ? 0.f : sTi[r][cc]);
-            Pg[i] = from_f<IO>(up ? 0.f : sP[r][cc]);
-        }
-        return;
-    }
-    // bf16 io: beta and the decay to the chunk end are folded into the two
-    // matrices the state chain applies to R' = V - diag(gamma) K S0^T:
-    //   D U   = (diag(D) T diag(beta)) R'     (input of the state update)
-    //   P U   = (P T diag(beta)) R'           (output correction)
-    // Both are lower triangular; P T is formed here with fp32 MFMA over the
-    // needed 16-blocks (sA is free once the solve is done).
-    float(*sPT)[CH + 4] = sA;
-    for (int job = wave; job < 10; job += 4) {
-        int t = job, bi = 0;
-        while (t > bi) { t -= bi + 1; ++bi; }
-        const int bj = t;
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int m = bj; m <= bi; ++m) {
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sP[16 * bi + l16][16 * m + 4 * kk + lg],
-                                                           sTi[16 * m + 4 * kk + lg][16 * bj + l16], acc, 0, 0, 0);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sPT[16 * bi + 4 * lg + e][16 * bj + l16] = acc[e];
-    }
-    __syncthreads();
-    // fragment order (frag_row / frag_col); blocks above the diagonal are zero
-    for (int i = tid; i < 2 * NFRAG * 64; i += NT) {
-        const int which = i / (NFRAG * 64), f = (i / 64) % NFRAG, l = i % 64;
-        IO* dst = (which ? Pg : Tg) + (f * 64 + l) * 8;
-        const int r = frag_row(f, l);
-        bf16_t v[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int cc = frag_col(f, l, e);
-            const float val = which ? sPT[r][cc] * sB[cc] : sD[r] * sTi[r][cc] * sB[cc];
-            v[e] = from_f<bf16_t>((cc >> 4) > (r >> 4) ? 0.f : val);
-        }
-        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
+    // T and P as row-major squares, zero above the diagonal blocks
+    for (int i = tid; i < CH * CH; i += NT) {
+        const int r = i / CH, cc = i % CH;
+        const bool up = (cc >> 4) > (r >> 4);
+        Tg[i] = up ? 0.f : sTi[r][cc];
+        Pg[i] = up ? 0.f : sP[r][cc];
     }
 }
 
-// ------------------------------------------------------------------ state chain
+// ------------------------------------------------------------------ fp32 state chain
 // One workgroup per (sequence, head, 16-row slice of S); chunks in order.
-template <typename IO, int DK>
+template <int DK>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
-    using M = Mma<IO>;
+    using IO = float;
     constexpr int PAD = 16 / sizeof(IO);
     constexpr int NMT = DK / 16;          // 16-row tiles of S^T
     const int H = p.H, DV = p.DV, nsl = DV / SL;
@@ -472,26 +419,28 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
 
-    __shared__ __attribute__((aligned(16))) float sS[SL][DK + 4];   // rows js*16.. of S
+    __shared__ __attribute__((aligned(16))) float sS[2][SL][DK + 4];   // rows js*16.. of S, by chunk parity
     __shared__ __attribute__((aligned(16))) IO sK[CH][DK + PAD];
     __shared__ __attribute__((aligned(16))) IO sQ[CH][DK + PAD];
     __shared__ __attribute__((aligned(16))) IO sT[CH][CH + PAD];
     __shared__ __attribute__((aligned(16))) IO sP[CH][CH + PAD];
-    __shared__ float sV[CH][SL + 1], sR[CH][SL + 1], sU[CH][SL + 1];
-    __shared__ float sGam[CH], sDec[CH], sBeta[CH];
+    __shared__ float sV[CH][SL + 1];
+    __shared__ __attribute__((aligned(16))) float sRt[SL][CH + 4], sUt[SL][CH + 4];   // R, U transposed
+    __shared__ __attribute__((aligned(16))) float sGam[CH], sDec[CH], sBeta[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
 
     for (int i = tid; i < SL * DK; i += NT)
-        sS[i / DK][i % DK] = p.S0 ? p.S0[srow0 + i] : 0.f;
+        sS[0][i / DK][i % DK] = p.S0 ? p.S0[srow0 + i] : 0.f;
 
     IO* go = reinterpret_cast<IO*>(p.o);
 
     // One chunk's inputs, this thread's share, held in registers: the next
-    // chunk's loads are issued right after the current chunk is written to LDS,
-    // so their latency overlaps the current chunk's arithmetic.
+    // chunk's loads are issued while the current chunk computes (K and Q after
+    // its first product, the rest after its second), so their latency and the
+    // issue of 100 KB of loads per workgroup overlap the arithmetic.
     constexpr int VE = 16 / sizeof(IO);             // elements per 16-byte load
     constexpr int NKV = CH * (DK / VE) / NT;        // K (and Q) loads per thread
     constexpr int NTV = CH * (CH / VE) / NT;        // T (and P) loads per thread
@@ -511,11 +460,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     };
     const int kvo = ((tid / (DK / VE)) * H * DK + (tid % (DK / VE)) * VE) * (int)sizeof(IO);
     const int vvo = ((tid / VPV) * H * DV + js * SL + (tid % VPV) * VE) * (int)sizeof(IO);
-    auto load = [&](int c, Pre& x) {
+    auto load_kq = [&](int c, Pre& x) {
         const long t0 = start + (long)c * CH;
-        const int n = min(CH, len - c * CH);
-        const long slot = (long)(cbase + c) * H + h;
-        const long rb = (long)(n - 1) * H + 1;   // rows of the head's chunk, in [T][H] rows
+        const long rb = (long)(min(CH, len - c * CH) - 1) * H + 1;   // rows of the head's chunk, in [T][H] rows
         const auto rk = rs(reinterpret_cast<const IO*>(p.k) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
         const auto rq = rs(reinterpret_cast<const IO*>(p.q) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
 #pragma unroll
@@ -524,6 +471,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
             x.k[j] = ld(rk, kvo + so);
             x.q[j] = ld(rq, kvo + so);
         }
+    };
+    auto load_rest = [&](int c, Pre& x) {
+        const long t0 = start + (long)c * CH;
+        const int n = min(CH, len - c * CH);
+        const long slot = (long)(cbase + c) * H + h;
+        const long rb = (long)(n - 1) * H + 1;
         const auto rt = rs(reinterpret_cast<const IO*>(p.wsT) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
         const auto rp = rs(reinterpret_cast<const IO*>(p.wsP) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
 #pragma unroll
@@ -571,60 +524,67 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     };
 
     Pre pre;
-    if (nc > 0) load(0, pre);
+    if (nc > 0) {
+        load_kq(0, pre);
+        load_rest(0, pre);
+    }
     for (int c = 0; c < nc; ++c) {
         const long t0 = start + (long)c * CH;
         const int n = min(CH, len - c * CH);
+        const float(*sSc)[DK + 4] = sS[c & 1];
         __syncthreads();   // previous chunk done with every tile
         store(pre);
-        if (c + 1 < nc) load(c + 1, pre);
         __syncthreads();
 
+        // fp32 MFMA (contraction 4 per instruction): in instruction 4 j + e, lane
+        // group lg carries contraction index 16 j + 4 lg + e, so a lane reads its
+        // operands for four instructions with one 16-byte LDS read.
         // X = K S^T (tokens of tile `wave` x 16 value channels)
         floatx4 x = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < DK / M::KS; ++kk) {
-            float sb[M::KL];
+        for (int j = 0; j < DK / 16; ++j) {
+            const floatx4 a4 = f4(&sK[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sSc[l16][16 * j + 4 * lg]);
 #pragma unroll
-            for (int e = 0; e < M::KL; ++e) sb[e] = sS[l16][kk * M::KS + lg * M::KL + e];
-            x = M::mma(M::load(&sK[wave * 16 + l16][kk * M::KS + lg * M::KL]), M::pack(sb), x);
+            for (int e = 0; e < 4; ++e) x = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], x, 0, 0, 0);
         }
-        // R = diag(beta) (V - diag(gamma) X)
+        // R = diag(beta) (V - diag(gamma) X), stored transposed
+        {
+            floatx4 rv;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = wave * 16 + 4 * lg + e;
-            sR[r][l16] = sBeta[r] * (sV[r][l16] - sGam[r] * x[e]);
+            for (int e = 0; e < 4; ++e) {
+                const int r = wave * 16 + 4 * lg + e;
+                rv[e] = sBeta[r] * (sV[r][l16] - sGam[r] * x[e]);
+            }
+            *reinterpret_cast<floatx4*>(&sRt[l16][wave * 16 + 4 * lg]) = rv;
         }
         __syncthreads();
 
+        if (c + 1 < nc) load_kq(c + 1, pre);
         // U = T R
         floatx4 u = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < CH / M::KS; ++kk) {
-            float rb[M::KL];
+        for (int j = 0; j < CH / 16; ++j) {
+            const floatx4 a4 = f4(&sT[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sRt[l16][16 * j + 4 * lg]);
 #pragma unroll
-            for (int e = 0; e < M::KL; ++e) rb[e] = sR[kk * M::KS + lg * M::KL + e][l16];
-            u = M::mma(M::load(&sT[wave * 16 + l16][kk * M::KS + lg * M::KL]), M::pack(rb), u);
+            for (int e = 0; e < 4; ++e) u = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], u, 0, 0, 0);
         }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sU[wave * 16 + 4 * lg + e][l16] = u[e];
+        *reinterpret_cast<floatx4*>(&sUt[l16][wave * 16 + 4 * lg]) = u;
         __syncthreads();
 
+        if (c + 1 < nc) load_rest(c + 1, pre);
         // O = scale (diag(gamma) Q S^T + P U)
         floatx4 oq = {0.f, 0.f, 0.f, 0.f}, op = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < DK / M::KS; ++kk) {
-            float sb[M::KL];
+        for (int j = 0; j < DK / 16; ++j) {
+            const floatx4 a4 = f4(&sQ[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sSc[l16][16 * j + 4 * lg]);
 #pragma unroll
-            for (int e = 0; e < M::KL; ++e) sb[e] = sS[l16][kk * M::KS + lg * M::KL + e];
-            oq = M::mma(M::load(&sQ[wave * 16 + l16][kk * M::KS + lg * M::KL]), M::pack(sb), oq);
+            for (int e = 0; e < 4; ++e) oq = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], oq, 0, 0, 0);
         }
 #pragma unroll
-        for (int kk = 0; kk < CH / M::KS; ++kk) {
-            float ub[M::KL];
+        for (int j = 0; j < CH / 16; ++j) {
+            const floatx4 a4 = f4(&sP[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sUt[l16][16 * j + 4 * lg]);
 #pragma unroll
-            for (int e = 0; e < M::KL; ++e) ub[e] = sU[kk * M::KS + lg * M::KL + e][l16];
-            op = M::mma(M::load(&sP[wave * 16 + l16][kk * M::KS + lg * M::KL]), M::pack(ub), op);
+            for (int e = 0; e < 4; ++e) op = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], op, 0, 0, 0);
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -643,33 +603,30 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
             acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
             if (mt < NMT) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[m][e] = gn * sS[l16][mt * 16 + 4 * lg + e];
+                for (int e = 0; e < 4; ++e) acc[m][e] = gn * sSc[l16][mt * 16 + 4 * lg + e];
 #pragma unroll
-                for (int kk = 0; kk < CH / M::KS; ++kk) {
-                    float ka[M::KL], ub[M::KL];
+                for (int j = 0; j < CH / 16; ++j) {
+                    const floatx4 u4 = f4(&sUt[l16][16 * j + 4 * lg]), d4 = f4(&sDec[16 * j + 4 * lg]);
 #pragma unroll
-                    for (int e = 0; e < M::KL; ++e) {
-                        const int r = kk * M::KS + lg * M::KL + e;
-                        ka[e] = to_f(sK[r][mt * 16 + l16]);
-                        ub[e] = sDec[r] * sU[r][l16];
-                    }
-                    acc[m] = M::mma(M::pack(ka), M::pack(ub), acc[m]);
+                    for (int e = 0; e < 4; ++e)
+                        acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(to_f(sK[16 * j + 4 * lg + e][mt * 16 + l16]),
+                                                                      d4[e] * u4[e], acc[m], 0, 0, 0);
                 }
             }
         }
-        __syncthreads();   // every read of the old state is done
+        // the new state into the other buffer: the old one may still be read
 #pragma unroll
         for (int m = 0; m < (NMT + 3) / 4; ++m) {
             const int mt = wave + 4 * m;
             if (mt < NMT) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) sS[l16][mt * 16 + 4 * lg + e] = acc[m][e];
+                for (int e = 0; e < 4; ++e) sS[(c + 1) & 1][l16][mt * 16 + 4 * lg + e] = acc[m][e];
             }
         }
     }
     __syncthreads();
     if (p.ST)
-        for (int i = tid; i < SL * DK; i += NT) p.ST[srow0 + i] = sS[i / DK][i % DK];
+        for (int i = tid; i < SL * DK; i += NT) p.ST[srow0 + i] = sS[nc & 1][i / DK][i % DK];
 }
 
 // ------------------------------------------------------------------ bf16 state chain
@@ -1657,7 +1614,7 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
                            p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
-    if (sizeof(IO) == 2) {
+    if constexpr (sizeof(IO) == 2) {
         // one launch with the chunk terms formed beside the chain when it leaves
         // a quarter of the compute units free; otherwise the chunk terms first
         // (three workgroups per CU) and the chain after, longest sequence first
@@ -1675,16 +1632,16 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         }
     }
     if (slots > 0 && p.T > 0) {
-        if (sizeof(IO) == 2)
+        if constexpr (sizeof(IO) == 2)
             hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
         else
-            hipLaunchKernelGGL((k_chunk_terms<IO, DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+            hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     }
     const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
-    if (sizeof(IO) == 2)
+    if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_state_chain_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p);
     else
-        hipLaunchKernelGGL((k_state_chain<IO, DK>), grid, dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain<DK>), grid, dim3(NT), 0, st, p);
 }
 
 template <typename IO, int DK>
