@@ -74,7 +74,6 @@ __device__ __forceinline__ floatx4 f4(const void* ptr) { return *reinterpret_cas
 // element e of lane group l/16 is token 32*kk + 16*(e/4) + 4*(l/16) + e%4 --
 // exactly the rows an MFMA accumulator tile pair holds in that lane.
 constexpr int NFRAG = 6;
-constexpr int NBF = 8;    // fragments of the full 64x64 cross-chunk matrix (4 row tiles x 2 blocks)
 __host__ __device__ constexpr int frag_id(int mt, int kk) { return mt < 2 ? mt : 2 + 2 * (mt - 2) + kk; }
 __device__ __forceinline__ int frag_mt(int f) { return f < 2 ? f : 2 + ((f - 2) >> 1); }
 __device__ __forceinline__ int frag_kk(int f) { return f < 2 ? 0 : ((f - 2) & 1); }
@@ -110,7 +109,6 @@ struct Params {
     float* wsG;          // [slot][H][128]: gamma_r = exp(G_r), then exp(G_n - G_r)
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
-    void* wsB;           // bf16 io: [slot][H][NBF fragments] of K_{c+1} K_c^T W_c
     uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
     uint64_t epoch;      // per-call tag of those flags
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
@@ -632,18 +630,18 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 // ------------------------------------------------------------------ bf16 state chain
 // One workgroup of 8 waves per (sequence, head, 16-row slice of S), bf16 io.
 // Write S_c for the state entering chunk c, X_c = K_c S_c^T and
-// R'_c = V_c - diag(gamma_c) X_c.  The chunk recurrence
-// S_{c+1}^T = gamma_n S_c^T + K_c^T W_c R'_c (W_c = diag(D) T diag(beta)) gives
-//     X_{c+1} = gamma_n K_{c+1} S_c^T + B_c R'_c,     B_c = K_{c+1} K_c^T W_c,
-// so the next chunk's R' needs only S_c and R'_c, and its product runs beside
-// the state update instead of after it.
+// R'_c = V_c - diag(gamma_c) X_c (section 3.2: V - diag(gamma) K S0^T).  Per chunk:
+// D U = W_c R'_c (W_c = diag(D) T diag(beta)), S_{c+1}^T = gamma_n S_c^T + K_c^T D U,
+// and X_{c+1} = K_{c+1} S_{c+1}^T for the next chunk's R'.
 //  waves 0,1 ("chain"): wave w keeps the S^T rows of key-channel tiles
 //    [NMD/2 w, NMD/2 (w+1)) as fp32 MFMA accumulators and the R' rows of token
-//    tiles 2w, 2w+1.  At barrier c the two waves swap their halves of S_c and
-//    R'_c (bf16 MFMA operands); then each forms X_{c+1} and R'_{c+1} for its
-//    token tiles, D U = W_c R'_c, and S^T <- gamma_n S^T + K_c^T (D U) for its
-//    key tiles.  Every B operand (S, R', D U) is packed from accumulators; the
-//    A operands are read in the matching contraction order:
+//    tiles 2w, 2w+1.  After barrier A_c (R'_c complete) each forms D U from both
+//    waves' R' tiles and updates its key tiles; it publishes its half of S_{c+1}
+//    and forms its keys' share of X_{c+1} for all four token tiles.  At barrier
+//    B_c the two waves swap the shares of each other's token tiles; each then
+//    completes X_{c+1} and R'_{c+1} for its own tiles.  Every B operand (S, R',
+//    D U) is packed from accumulators; the A operands are read in the matching
+//    contraction order:
 //      - token contractions: element e of lane group g in block kk is token
 //        32 kk + 16 (e/4) + 4 g + e%4 (the rows an accumulator tile pair holds);
 //      - key contractions: accumulator tile md, lane group g, element e holds
@@ -652,25 +650,25 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 //        the K (and Q) operands are single 16-byte reads.  K^T comes from the
 //        row-major K tile through LDS transpose reads.
 //  waves 2,3 ("output"): O_c^T = scale (S_c Q_c^T diag(gamma_c) + R'_c^T P'_c^T)
-//    for one half of the chunk's tokens, from the same exchanged S_c and R'_c --
+//    for one half of the chunk's tokens, from the published S_c and R'_c --
 //    the operands swapped, so a lane ends up with 4 consecutive value channels
 //    of one token and writes them with one 8-byte store.  Each stages its Q rows
 //    in LDS one chunk ahead (buffer loads of whole cache lines: register loads
 //    in the MFMA layout would read 64-byte halves) and loads its P' fragments
 //    straight into registers.
-//  waves 4..7 ("loaders"): copy chunk c+3 (K, W, B, the V slice, gamma) into a
+//  waves 4..7 ("loaders"): copy chunk c+3 (K, W, the V slice, gamma) into a
 //    4-deep LDS ring with buffer loads to LDS, each a quarter of the loads (one
 //    wave alone issues global loads at about a third of a CU's rate).
 // Global loads use per-chunk buffer descriptors that end at row n-1 of the
 // head, so the rows of a partial chunk read as zeros.  K rows sit in LDS with
 // their 16-byte chunks XOR-swizzled by row, which keeps the transpose reads
 // (4 rows, 4 chunks) free of bank conflicts.
-// One barrier per chunk, at its start: S_c and R'_c are complete (exchange
-// buffers alternate by chunk parity); every wave is done with chunk c-1, so
-// the loader refills that slot; chunk c+1, read during chunk c, was waited for
-// before it.  Barriers order LDS traffic only, so global loads and stores stay
-// in flight across them.  The chunk loop is unrolled by the ring depth so ring
-// slots are constants.
+// Two barriers per chunk.  At A_c, S_c and R'_c are complete (exchange buffers
+// alternate by chunk parity) and every wave is done with chunk c-1, so the
+// loaders refill that slot; chunk c+1, read during chunk c, was waited for
+// before it.  B_c orders the chain waves' exchange of X_{c+1}.  Barriers order
+// LDS traffic only, so global loads and stores stay in flight across them.
+// The chunk loop is unrolled by the ring depth so ring slots are constants.
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short short4v __attribute__((ext_vector_type(4)));
@@ -731,11 +729,11 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 template <int DK> struct ChainLds {
     bf16_t sK[RING][CH * DK];     // ring of chunk inputs (slot = chunk % RING)
     bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
-    bf16x8 sBt[RING][NBF][64];    // K_{c+1} K_c^T W_c
     bf16_t sV[RING][CH * SL];
     float sG[RING][CH];           // gamma_r
     bf16x8 sSf[2][DK / 32][64];   // S_c and R'_c as MFMA operands, by chunk parity
     bf16x8 sRf[2][2][64];
+    floatx4 sY[2][2][64];         // each chain wave's share of X_{c+1} for the other wave's token tiles
     bf16_t sQ[2][32 * DK];        // Q rows of each output wave
 };
 
@@ -764,7 +762,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     const int nc = (len + CH - 1) / CH;
     auto& sK = lds.sK;
     auto& sW = lds.sW;
-    auto& sBt = lds.sBt;
+    auto& sY = lds.sY;
     auto& sV = lds.sV;
     auto& sG = lds.sG;
     auto& sSf = lds.sSf;
@@ -790,12 +788,11 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     if (wave >= 4) {
         // ------------------------------------------------ loaders
         // One wave issues global loads at about a third of a CU's rate, so four
-        // waves share the copies: K load groups, W and B fragments with index
-        // = loader (mod 4), the two V loads on loaders 2 and 3, gamma on loader 0.
+        // waves share the copies: K load groups, W fragments with index =
+        // loader (mod 4), the two V loads on loaders 2 and 3, gamma on loader 0.
         const int li = wave - 4;
         int spins = 1 << 22;   // ~0.2 s of sleeping in all; the chunk-terms workgroups never wait
         const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
-        const bf16_t* wsB = reinterpret_cast<const bf16_t*>(p.wsB);
         int koff[NCH / 4];   // loop-invariant byte offsets of this lane's K loads within a chunk
 #pragma unroll
         for (int j = 0; j < NCH / 4; ++j) {
@@ -819,22 +816,20 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
             for (int f = L; f < NFRAG; f += 4) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
-            const auto rb = rsrc(wsB + sc * (NBF * 512), NBF * 512 * 2);
-#pragma unroll
-            for (int f = L; f < NBF; f += 4) bdma16<AUX>(rb, &sBt[sl][f][0], (f * 64 + lane) * 16);
             if constexpr (L >= 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L & 1) * SL], voff);
             if constexpr (L == 0) bdma4<AUX>(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
         };
-        // After barrier c every wave is done with chunk c-1, whose slot is
+        // After barrier A_c every wave is done with chunk c-1, whose slot is
         // (c+3) % RING: chunk c+3 is loaded there, and the wait leaves only
-        // those loads in flight, so chunk c+2 has landed before barrier c+1.
+        // those loads in flight, so chunk c+2 has landed before barrier A_{c+1}.
         auto run = [&](auto LI) {
             constexpr int L = decltype(LI)::value;
-            constexpr int NI = NCH / 4 + (NFRAG - L + 3) / 4 + (NBF - L + 3) / 4 + (L >= 2) + (L == 0);
+            constexpr int NI = NCH / 4 + (NFRAG - L + 3) / 4 + (L >= 2) + (L == 0);
             auto lstep = [&](int c, auto SLOT) {
                 constexpr int bn = (decltype(SLOT)::value + 3) % RING;
-                lds_barrier();
+                lds_barrier();   // A_c
                 issue(min(c + 3, nc - 1), Ic<bn>{}, LI);
+                lds_barrier();   // B_c
                 asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
             };
             if (nc > 0) {
@@ -871,16 +866,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         }
         // loop-invariant LDS offsets of this lane's operands
         int offT[HMD][2][2];      // K^T fragments of this wave's key tiles (transpose reads)
-        int offX[2][2][HKD];      // K rows of this wave's token tiles: [tile][own / other key half][block]
         int offV[2];              // V rows of this wave's token tiles (transpose reads)
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int mt = 2 * w + i;
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) {
-                offX[i][0][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
-                offX[i][1][k2] = kq(16 * mt + l16, 32 * ((1 - w) * HKD + k2) + 8 * lg);
-            }
             offV[i] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
         }
 #pragma unroll
@@ -927,36 +916,30 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 z[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int k2 = 0; k2 < HKD; ++k2) {
+                    const int r = 16 * (2 * w + i) + l16;
                     y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(&sK[0][offX[i][0][k2]]), sfo[k2], y[i], 0, 0, 0);
+                        *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * (w * HKD + k2) + 8 * lg)]), sfo[k2], y[i], 0, 0, 0);
                     y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(&sK[0][offX[i][1][k2]]), sfx[k2], y[i], 0, 0, 0);
+                        *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * ((1 - w) * HKD + k2) + 8 * lg)]), sfx[k2], y[i],
+                        0, 0, 0);
                 }
             }
             rfo = rprime(y, z, 1.f, 0);
             sRf[0][w][lane] = rfo;
         }
+        // K_{c+1} rows of all four token tiles over this wave's key blocks (the
+        // partial products X_{c+1} = K_{c+1} S_{c+1}^T the waves exchange)
+        int offY[4][HKD];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int k2 = 0; k2 < HKD; ++k2) offY[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
         auto cstep = [&](int c, auto SLOT) {
             constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
-            lds_barrier();   // barrier c: both halves of S_c and R'_c visible
-            // the other wave's halves, then chunk c's operands and chunk c+1's K rows
-            bf16x8 sfx[HKD];
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) sfx[k2] = sSf[x2][(1 - w) * HKD + k2][lane];
+            lds_barrier();   // barrier A_c: S_c halves and R'_c visible
             const bf16x8 rfx = sRf[x2][1 - w][lane];
             const bf16x8 rf0 = sel(w == 0, rfo, rfx), rf1 = sel(w == 0, rfx, rfo);
-            bf16x8 xo[2][HKD], xx[2][HKD], bo[2], bx[2], wf[NFRAG], ka[HMD][2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-#pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2) {
-                    xo[i][k2] = *reinterpret_cast<const bf16x8*>(&sK[bn][offX[i][0][k2]]);
-                    xx[i][k2] = *reinterpret_cast<const bf16x8*>(&sK[bn][offX[i][1][k2]]);
-                }
-                bo[i] = sBt[b][2 * (2 * w + i) + w][lane];
-                bx[i] = sBt[b][2 * (2 * w + i) + 1 - w][lane];
-            }
-            const float gn = sG[b][CH - 1];
+            bf16x8 wf[NFRAG], ka[HMD][2];
 #pragma unroll
             for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
 #pragma unroll
@@ -964,19 +947,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk)
                     ka[m][kk] = join4(lds_tr8(&sK[b][offT[m][kk][0]]), lds_tr8(&sK[b][offT[m][kk][1]]));
-            // X_{c+1} for this wave's token tiles: gn (K_{c+1} S_c^T) + B_c R'_c
-            floatx4 y[2], z[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                z[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bo[i], rfo, floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                z[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bx[i], rfx, z[i], 0, 0, 0);
-                y[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2) {
-                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xo[i][k2], sfo[k2], y[i], 0, 0, 0);
-                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xx[i][k2], sfx[k2], y[i], 0, 0, 0);
-                }
-            }
+            const float gn = sG[b][CH - 1];
             // D U = W R' (lower triangular: tile mt needs blocks 0..mt/2); S^T <- gn S^T + K^T (D U)
             floatx4 du[4];
 #pragma unroll
@@ -992,10 +963,33 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
                 acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
             }
-            // R'_{c+1} and S_{c+1}, published for chunk c+1
-            rfo = rprime(y, z, gn, bn);
-            sRf[1 - x2][w][lane] = rfo;
+            // S_{c+1}: this wave's half for the output waves, and its share of X_{c+1}
             publish_s(1 - x2);
+            floatx4 yp[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                yp[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2)
+                    yp[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(&sK[bn][offY[mt][k2]]), sfo[k2], yp[mt], 0, 0, 0);
+            }
+            // (whole-value selects: a runtime index into a register array would go to scratch)
+            floatx4 own[2], oth[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                own[i] = w == 0 ? yp[i] : yp[2 + i];
+                oth[i] = w == 0 ? yp[2 + i] : yp[i];
+                sY[w][i][lane] = oth[i];   // the other wave's token tiles
+            }
+            lds_barrier();   // barrier B_c: both waves' shares of X_{c+1} visible
+            floatx4 y[2];
+            const floatx4 z[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+            for (int i = 0; i < 2; ++i) y[i] = own[i] + sY[1 - w][i][lane];
+            // R'_{c+1}, published for chunk c+1
+            rfo = rprime(y, z, 1.f, bn);
+            sRf[1 - x2][w][lane] = rfo;
         };
         for (int c = 0; c < nc; c += RING) {
             cstep(c, Ic<0>{});
@@ -1042,7 +1036,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             // chunk's start waiting until NPP remain covers the Q copy.
             auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
-                lds_barrier();   // barrier c: S_c and R'_c visible
+                lds_barrier();   // barrier A_c: S_c and R'_c visible
                 asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NPP) : "memory");   // Q_c staged
                 bf16x8 qa[2][NKD];
 #pragma unroll
@@ -1075,6 +1069,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, __builtin_convertvector(ov, bf16x4)), ro,
                                                           (tok * H * DV + js * SL + 4 * lg) * 2, 0, 0);
                 }
+                lds_barrier();   // B_c (the chain waves' exchange of X_{c+1}); S_c and R'_c are no longer read
             };
             bf16x8 pA[NPP], pB[NPP];
             lds_barrier();   // prologue 1: the loaders have seen chunks 0..2's terms published
@@ -1096,8 +1091,9 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     }
 }
 
+// One workgroup per CU (its LDS), so two waves per SIMD: the register budget is that of two waves.
 template <int DK>
-__global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
+__global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_bf16(Params p) {
     __shared__ ChainLds<DK> lds;
     state_chain_bf16<DK, false>(p, blockIdx.x, lds);
 }
@@ -1107,23 +1103,18 @@ __global__ __launch_bounds__(NT_CHAIN) void k_state_chain_bf16(Params p) {
 // state chain gamma_r and exp(G_n - G_r), and in MFMA fragment order
 //     W  = diag(D) T diag(beta)     lower triangular, 6 fragments
 //     P' = P T diag(beta)           lower triangular, 6 fragments
-//     B  = K' K^T W                 64 x 64, 8 fragments
-// with T = (I + A)^{-1} and K' the key tile of the sequence's next chunk (B is
-// zero for a sequence's last chunk).  B carries a chunk's contribution to the
-// state into the next chunk's product K' S^T, so the chain can form that
-// product from the state it already has.
-// Stages: K, Q and K' arrive by buffer loads to LDS (rows past a chunk read as
+// with T = (I + A)^{-1}.
+// Stages: K and Q arrive by buffer loads to LDS (rows past a chunk read as
 // zero); prefix sums of g in fp64 log2 units (every decay factor is one exp2
-// of an fp64 difference); each wave forms its share of the 16x16 blocks of
-// K K^T and Q K^T (lower) and K K'^T (all) with all its operands in registers,
-// so the tiles' LDS space holds A, P and T afterwards; T's diagonal blocks by
-// forward substitution with the rows of A in registers; its off-diagonal
-// blocks one block diagonal at a time by fp32 MFMA block products; the
-// fragments of W, P' and B from a bf16 copy of T.
+// of an fp64 difference); each wave forms its share of the lower 16x16 blocks
+// of K K^T and Q K^T with all its operands in registers, so the tiles' LDS
+// space holds A, P and T afterwards; T's diagonal blocks by forward
+// substitution with the rows of A in registers; its off-diagonal blocks one
+// block diagonal at a time by fp32 MFMA block products; the fragments of W and
+// P' from a bf16 copy of T.
 template <int DK, int W>
-__device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, const bf16_t* sKn,
-                                            const double* sGl, const float* sB, const float* sD, int l16, int lg,
-                                            floatx4 (&ablk)[3], floatx4 (&pblk)[3], bf16x8 (&def)[2]) {
+__device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, const double* sGl, const float* sB,
+                                            int l16, int lg, floatx4 (&ablk)[3], floatx4 (&pblk)[3]) {
     constexpr int NCH = DK / 8, NKD = DK / 32;
     // lower 16x16 blocks (bi, bj): KK^T takes entries W, W+4, ..; QK^T entries (W+2)%4, ..
     constexpr int BI[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
@@ -1132,27 +1123,17 @@ __device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, 
     constexpr int NA = W < 2 ? 3 : 2, NP = QW < 2 ? 3 : 2;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
     auto kq = [&](int r, int cc) { return r * DK + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
-    bf16x8 kf[4][NKD], kn[NKD];
+    bf16x8 kf[4][NKD];
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
         for (int kk = 0; kk < NKD; ++kk) kf[rb][kk] = *reinterpret_cast<const bf16x8*>(sK + kq(16 * rb + l16, 32 * kk + 8 * lg));
-#pragma unroll
-    for (int kk = 0; kk < NKD; ++kk) kn[kk] = *reinterpret_cast<const bf16x8*>(sKn + kq(16 * W + l16, 32 * kk + 8 * lg));
     bf16x8 qf[NP][NKD];
 #pragma unroll
     for (int j = 0; j < NP; ++j)
 #pragma unroll
         for (int kk = 0; kk < NKD; ++kk)
             qf[j][kk] = *reinterpret_cast<const bf16x8*>(sQ + kq(16 * BI[QW + 4 * j] + l16, 32 * kk + 8 * lg));
-    // K K'^T transposed, tiles (ib, W): lane holds E^T[16 ib + 4 lg + e][16 W + l16]
-    floatx4 et[4];
-#pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-        et[ib] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < NKD; ++kk) et[ib] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ib][kk], kn[kk], et[ib], 0, 0, 0);
-    }
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
         const int bi = BI[W + 4 * j], bj = BJ[W + 4 * j];
@@ -1183,12 +1164,6 @@ __device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, 
             pblk[j][e] = r >= i ? gam * acc[e] : 0.f;
         }
     }
-    // diag(D) E^T, packed as B operands over the chunk's tokens (contraction order
-    // 32 kk + 16 (e/4) + 4 lg + e%4 -- the rows an accumulator tile pair holds)
-#pragma unroll
-    for (int ib = 0; ib < 4; ++ib) et[ib] *= *reinterpret_cast<const floatx4*>(&sD[16 * ib + 4 * lg]);
-    def[0] = pack_bf16(et[0], et[1]);
-    def[1] = pack_bf16(et[2], et[3]);
 }
 
 template <int DK, int W>
@@ -1208,11 +1183,11 @@ __device__ __forceinline__ void store_gram(float (*sA)[CH + 4], bf16_t (*sPb)[CH
         for (int e = 0; e < 4; ++e) sPb[16 * BI[QW + 4 * j] + 4 * lg + e][16 * BJ[QW + 4 * j] + l16] = from_f<bf16_t>(pblk[j][e]);
 }
 
-// LDS of one chunk-terms work item: phase 1 holds the K, Q and K' tiles; phase
+// LDS of one chunk-terms work item: phase 1 holds the K and Q tiles; phase
 // 2 reuses the space for A, T (fp32) and P (bf16), and T's bf16 copy over A
 template <int DK> struct TermsLds {
     static constexpr int PA = CH + 4, PB = CH + 8;   // row pitches of the fp32 and bf16 64 x 64 matrices
-    static constexpr int SZ_TILES = 3 * CH * DK * 2;
+    static constexpr int SZ_TILES = 2 * CH * DK * 2;
     static constexpr int SZ_MATS = 2 * CH * PA * 4 + CH * PB * 2;
     __attribute__((aligned(16))) char r0[SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS];
     double sGl[CH];
@@ -1253,7 +1228,6 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     const int c = gc - cbase;
     const long t0 = start + (long)c * CH;
     const int n = min(CH, len - c * CH);
-    const int n1 = min(CH, len - (c + 1) * CH);   // rows of the next chunk (<= 0: none)
     const long slot = (long)gc * H + h;
 
     char* r0 = lds.r0;
@@ -1262,7 +1236,6 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     float* sD = lds.sD;
     bf16_t* sK = reinterpret_cast<bf16_t*>(r0);
     bf16_t* sQ = sK + TILE;
-    bf16_t* sKn = sQ + TILE;
     float(*sA)[PA] = reinterpret_cast<float(*)[PA]>(r0);
     float(*sTi)[PA] = reinterpret_cast<float(*)[PA]>(r0 + CH * PA * 4);
     bf16_t(*sPb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0 + 2 * CH * PA * 4);
@@ -1272,21 +1245,18 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     const int l16 = lane & 15, lg = lane >> 4;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
 
-    {   // K, Q and K' tiles straight into LDS; loads i = wave, wave + 4, ...
+    {   // K and Q tiles straight into LDS; loads i = wave, wave + 4, ...
         const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
         const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
         const long row0 = t0 * H + h;
         const uint32_t bytes = (uint32_t)(((long)(n - 1) * H + 1) * DK * 2);
         const auto rk = rsrc(gk + row0 * DK, bytes);
         const auto rq = rsrc(gq + row0 * DK, bytes);
-        const auto rn = n1 > 0 ? rsrc(gk + (row0 + (long)CH * H) * DK, (uint32_t)(((long)(n1 - 1) * H + 1) * DK * 2))
-                               : rsrc(gk, 0);   // empty: the tile reads as zeros
         for (int i = wave; i < NCH; i += 4) {
             const int r = RPI * i + lane / NCH;
             const int off = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             bdma16(rk, sK + RPI * i * DK, off);
             bdma16(rq, sQ + RPI * i * DK, off);
-            bdma16(rn, sKn + RPI * i * DK, off);
         }
     }
     if (wave == 0) {
@@ -1315,12 +1285,11 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
 
     // token-token blocks, all operands in registers
     floatx4 ablk[3], pblk[3];
-    bf16x8 def[2];
     switch (wave) {
-        case 0: gram_blocks<DK, 0>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
-        case 1: gram_blocks<DK, 1>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
-        case 2: gram_blocks<DK, 2>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
-        default: gram_blocks<DK, 3>(sK, sQ, sKn, sGl, sB, sD, l16, lg, ablk, pblk, def); break;
+        case 0: gram_blocks<DK, 0>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
+        case 1: gram_blocks<DK, 1>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
+        case 2: gram_blocks<DK, 2>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
+        default: gram_blocks<DK, 3>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
     }
     __syncthreads();   // every tile read done: A, P and T take the space over
     switch (wave) {
@@ -1400,7 +1369,6 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
 
     const auto rW = rsrc(reinterpret_cast<bf16_t*>(p.wsT) + slot * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
     const auto rP = rsrc(reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
-    const auto rB = rsrc(reinterpret_cast<bf16_t*>(p.wsB) + slot * (NBF * 64 * 8), NBF * 64 * 8 * 2);
     for (int f = wave; f < NFRAG; f += 4) {
         const int mt = frag_mt(f), kk2 = frag_kk(f), r = 16 * mt + l16;
         // W fragment: D_r T[r][tau] beta_tau
@@ -1428,24 +1396,6 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
         }
         if (store) bstore16<AUX>(pack_bf16(pt[0], pt[1]), rP, (f * 64 + lane) * 16);
     }
-    {   // B fragments (row block mt = wave) from B^T = diag(beta) T^T (diag(D) E^T) tiles
-        // (tau block bt, token block mt); T^T's contraction order matches def's
-        floatx4 bt4[4];
-#pragma unroll
-        for (int bt = 0; bt < 4; ++bt) {
-            bt4[bt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kk = bt < 2 ? 0 : 1; kk < 2; ++kk) {   // T^T[tau][i] = 0 for i < tau
-                const bf16_t* t0p = &sTb[32 * kk + 4 * lg + (l16 >> 2)][16 * bt + 4 * (l16 & 3)];
-                const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 16 * PB));
-                bt4[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, def[kk], bt4[bt], 0, 0, 0);
-            }
-            bt4[bt] *= *reinterpret_cast<const floatx4*>(&sB[16 * bt + 4 * lg]);
-        }
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-            if (store) bstore16<AUX>(pack_bf16(bt4[2 * kk], bt4[2 * kk + 1]), rB, ((2 * wave + kk) * 64 + lane) * 16);
-    }
     if constexpr (FUSED) {   // publish: every wave's stores are complete before the flag is set
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
@@ -1465,7 +1415,7 @@ __global__ __launch_bounds__(NT, 3) void k_chunk_terms_bf16(Params p) {
 // are dispatched first and never wait, so the chain workgroups' waits end
 // whatever number of workgroups the device holds at once.
 template <int DK>
-__global__ __launch_bounds__(NT_CHAIN) void k_prefill_fused_bf16(Params p) {
+__global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_prefill_fused_bf16(Params p) {
     static_assert(NT_CHAIN == 2 * NT, "two work items per chunk-terms workgroup");
     __shared__ union Lds {
         ChainLds<DK> c;
@@ -1558,7 +1508,7 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
     long slots;          // chunk slots per head
-    size_t meta, G, T, P, B, F, total;
+    size_t meta, G, T, P, F, total;
 };
 
 // Workspace layout; returns false for arguments that are out of range.
@@ -1575,8 +1525,7 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
-    L->B = L->P + round_up(per * tp * esz, 256);
-    L->F = L->B + (io == GDN_BF16 ? round_up(per * NBF * 512 * 2, 256) : 0);
+    L->F = L->P + round_up(per * tp * esz, 256);
     L->total = L->F + (io == GDN_BF16 ? round_up(per * sizeof(uint64_t), 256) : 0);
     return true;
 }
@@ -1742,13 +1691,12 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.wsG = reinterpret_cast<float*>(ws + L.G);
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
-    p.wsB = ws + L.B;
     p.flags = reinterpret_cast<uint64_t*>(ws + L.F);
     p.epoch = 0;
     p.npw = 0;
     p.xcd_items = 0;
     p.scale = scale;
-    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsB = nullptr; p.flags = nullptr; }
+    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.flags = nullptr; }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
