@@ -66,21 +66,17 @@ template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float f) {
 // indices a lane's elements stand for is a free choice as long as A and B agree.
 __device__ __forceinline__ floatx4 f4(const void* ptr) { return *reinterpret_cast<const floatx4*>(ptr); }
 
-// Fragment order of the lower-triangular 64x64 matrices T and P for bf16 io.
+// Fragment order of the lower-triangular 64x64 matrices W and P' for bf16 io.
 // A 16x16x32 MFMA over a 64-long token contraction needs, for output row tile
 // mt, contraction blocks kk = 0..mt/2 (the rest is zero): six fragments
 // f = (mt, kk) = (0,0) (1,0) (2,0) (2,1) (3,0) (3,1).  Lane l, element e of
-// fragment f holds M[frag_row(f, l)][frag_col(f, l, e)], so that contraction
-// element e of lane group l/16 is token 32*kk + 16*(e/4) + 4*(l/16) + e%4 --
-// exactly the rows an MFMA accumulator tile pair holds in that lane.
+// fragment f holds M[16 mt + l%16][32 kk + 16 (e/4) + 4 (l/16) + e%4], so that
+// contraction element e of lane group l/16 is token 32 kk + 16 (e/4) + 4 (l/16)
+// + e%4 -- exactly the rows an MFMA accumulator tile pair holds in that lane.
 constexpr int NFRAG = 6;
 __host__ __device__ constexpr int frag_id(int mt, int kk) { return mt < 2 ? mt : 2 + 2 * (mt - 2) + kk; }
 __device__ __forceinline__ int frag_mt(int f) { return f < 2 ? f : 2 + ((f - 2) >> 1); }
 __device__ __forceinline__ int frag_kk(int f) { return f < 2 ? 0 : ((f - 2) & 1); }
-__device__ __forceinline__ int frag_row(int f, int l) { return 16 * frag_mt(f) + (l & 15); }
-__device__ __forceinline__ int frag_col(int f, int l, int e) {
-    return 32 * frag_kk(f) + 16 * (e >> 2) + 4 * (l >> 4) + (e & 3);
-}
 
 // Elements per (chunk, head) slot of T and of P in the workspace.
 template <typename IO> __host__ __device__ constexpr int tp_elems() { return sizeof(IO) == 2 ? NFRAG * 64 * 8 : CH * CH; }
@@ -934,7 +930,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
             for (int k2 = 0; k2 < HKD; ++k2) offY[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
-        auto cstep = [&](int c, auto SLOT) {
+        auto cstep = [&](auto SLOT) {   // chunk c = SLOT (mod RING)
             constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
             lds_barrier();   // barrier A_c: S_c halves and R'_c visible
             const bf16x8 rfx = sRf[x2][1 - w][lane];
@@ -992,10 +988,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             sRf[1 - x2][w][lane] = rfo;
         };
         for (int c = 0; c < nc; c += RING) {
-            cstep(c, Ic<0>{});
-            if (c + 1 < nc) cstep(c + 1, Ic<1>{});
-            if (c + 2 < nc) cstep(c + 2, Ic<2>{});
-            if (c + 3 < nc) cstep(c + 3, Ic<3>{});
+            cstep(Ic<0>{});
+            if (c + 1 < nc) cstep(Ic<1>{});
+            if (c + 2 < nc) cstep(Ic<2>{});
+            if (c + 3 < nc) cstep(Ic<3>{});
         }
         if (p.ST) {
 #pragma unroll
@@ -1008,7 +1004,6 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         // rows are staged in LDS by buffer loads (whole 128-byte lines, XOR-swizzled
         // like K), one chunk ahead.  P' token tile mt needs fragments (mt, 0..mt/2):
         // wave 2 fragments 0, 1; wave 3 fragments 2, 3, 4, 5.
-        bf16_t* go = reinterpret_cast<bf16_t*>(p.o);
         auto run = [&](auto OW) {
             constexpr int ow = decltype(OW)::value, NPP = ow ? 4 : 2;
             const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);

@@ -218,3 +218,11 @@ def test_workspace_reused_across_calls_with_different_inputs():
         o_ref, ST_ref = _ref(x)
         assert oracle.max_rel_err(f64(o), o_ref) < TOL["bf16"], i
         assert oracle.max_rel_err(f64(ST), ST_ref) < TOL["bf16"], i
+
+
+@pytest.mark.parametrize("T", [200, 700])
+def test_dense_batch_through_two_launches(T):
+    """B=2, H=16, dv=128 gives 256 chain workgroups: no CUs are left beside the
+    chain, so the chunk terms run as their own launch before it."""
+    x = inputs.make_prefill(B=2, T=T, H=16, dk=128, dv=128, io="bf16", seed=T + 5, s0_std=0.05)
+    _check(x, "bf16", "B=2 T=%d H=16 bf16 (two launches)" % T)
