@@ -730,7 +730,7 @@ template <int DK> struct ChainLds {
     bf16x8 sSf[2][DK / 32][64];   // S_c and R'_c as MFMA operands, by chunk parity
     bf16x8 sRf[2][2][64];
     floatx4 sY[2][2][64];         // each chain wave's share of X_{c+1} for the other wave's token tiles
-    bf16_t sQ[2][32 * DK];        // Q rows of each output wave
+    bf16_t sQ[2][2][32 * DK];     // Q rows of each output wave, by chunk parity
 };
 
 // Chain workgroup `bid`.  FUSED: the chunk terms come from workgroups of the
@@ -852,169 +852,188 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         }
     } else if (wave < 2) {
         // ------------------------------------------------ chain waves
-        const int w = wave;
-        auto chan = [&](int md) { return 32 * (md >> 1) + 8 * lg + 4 * (md & 1); };   // + e
-        floatx4 acc[HMD];
-#pragma unroll
-        for (int m = 0; m < HMD; ++m) {
-            acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
-            if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(w * HMD + m));
-        }
-        // loop-invariant LDS offsets of this lane's operands
-        int offT[HMD][2][2];      // K^T fragments of this wave's key tiles (transpose reads)
-        int offV[2];              // V rows of this wave's token tiles (transpose reads)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int mt = 2 * w + i;
-            offV[i] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
-        }
-#pragma unroll
-        for (int m = 0; m < HMD; ++m) {
-            const int md = w * HMD + m;
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2)
-                    offT[m][kk][h2] = kq(32 * kk + 16 * h2 + 4 * lg + (l16 >> 2),
-                                         32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1));
-        }
-        bf16x8 sfo[HKD], rfo;   // this wave's halves of S_c and R'_c
-        auto publish_s = [&](int par) {
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) {
-                sfo[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
-                sSf[par][w * HKD + k2][lane] = sfo[k2];
-            }
-        };
-        // R' rows of this wave's token tiles from X = gn y + z: V - diag(gamma) X
-        auto rprime = [&](const floatx4 (&y)[2], const floatx4 (&z)[2], float gn, int bn) {
-            floatx4 rr[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const short4v vv = lds_tr8(&sV[bn][offV[i]]);
-                const floatx4 gm = *reinterpret_cast<const floatx4*>(&sG[bn][16 * (2 * w + i) + 4 * lg]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) rr[i][e] = bf(vv[e]) - gm[e] * (gn * y[i][e] + z[i][e]);
-            }
-            return pack_bf16(rr[0], rr[1]);
-        };
-        lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
-        if (nc > 0) publish_s(0);
-        lds_barrier();   // prologue 2: S_0 halves visible
-        if (nc > 0) {    // R'_0 = V_0 - diag(gamma_0) K_0 S_0^T for this wave's token tiles
-            bf16x8 sfx[HKD];
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) sfx[k2] = sSf[0][(1 - w) * HKD + k2][lane];
-            floatx4 y[2], z[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                y[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-                z[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2) {
-                    const int r = 16 * (2 * w + i) + l16;
-                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * (w * HKD + k2) + 8 * lg)]), sfo[k2], y[i], 0, 0, 0);
-                    y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * ((1 - w) * HKD + k2) + 8 * lg)]), sfx[k2], y[i],
-                        0, 0, 0);
-                }
-            }
-            rfo = rprime(y, z, 1.f, 0);
-            sRf[0][w][lane] = rfo;
-        }
-        // K_{c+1} rows of all four token tiles over this wave's key blocks (the
-        // partial products X_{c+1} = K_{c+1} S_{c+1}^T the waves exchange)
-        int offY[4][HKD];
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int k2 = 0; k2 < HKD; ++k2) offY[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
-        auto cstep = [&](auto SLOT) {   // chunk c = SLOT (mod RING)
-            constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
-            lds_barrier();   // barrier A_c: S_c halves and R'_c visible
-            const bf16x8 rfx = sRf[x2][1 - w][lane];
-            const bf16x8 rf0 = sel(w == 0, rfo, rfx), rf1 = sel(w == 0, rfx, rfo);
-            bf16x8 wf[NFRAG], ka[HMD][2];
-#pragma unroll
-            for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
-#pragma unroll
-            for (int m = 0; m < HMD; ++m)
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk)
-                    ka[m][kk] = join4(lds_tr8(&sK[b][offT[m][kk][0]]), lds_tr8(&sK[b][offT[m][kk][1]]));
-            const float gn = sG[b][CH - 1];
-            // D U = W R' (lower triangular: tile mt needs blocks 0..mt/2); S^T <- gn S^T + K^T (D U)
-            floatx4 du[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 0)], rf0, floatx4{0.f, 0.f, 0.f, 0.f},
-                                                                 0, 0, 0);
-                if (mt >= 2) du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 1)], rf1, du[mt], 0, 0, 0);
-            }
-            const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
+        // (one instance per wave, so the wave's half is a constant: no selects)
+        auto chain = [&](auto WI) {
+            constexpr int w = decltype(WI)::value;
+            auto chan = [&](int md) { return 32 * (md >> 1) + 8 * lg + 4 * (md & 1); };   // + e
+            floatx4 acc[HMD];
 #pragma unroll
             for (int m = 0; m < HMD; ++m) {
-                acc[m] *= gn;
-                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
-                acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
+                acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+                if (p.S0) acc[m] = *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(w * HMD + m));
             }
-            // S_{c+1}: this wave's half for the output waves, and its share of X_{c+1}
-            publish_s(1 - x2);
-            floatx4 yp[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                yp[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int k2 = 0; k2 < HKD; ++k2)
-                    yp[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(&sK[bn][offY[mt][k2]]), sfo[k2], yp[mt], 0, 0, 0);
-            }
-            // (whole-value selects: a runtime index into a register array would go to scratch)
-            floatx4 own[2], oth[2];
+            // loop-invariant LDS offsets of this lane's operands
+            int offT[HMD][2][2];      // K^T fragments of this wave's key tiles (transpose reads)
+            int offV[2];              // V rows of this wave's token tiles (transpose reads)
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-                own[i] = w == 0 ? yp[i] : yp[2 + i];
-                oth[i] = w == 0 ? yp[2 + i] : yp[i];
-                sY[w][i][lane] = oth[i];   // the other wave's token tiles
+                const int mt = 2 * w + i;
+                offV[i] = (16 * mt + 4 * lg + (l16 >> 2)) * SL + 4 * (l16 & 3);
             }
-            lds_barrier();   // barrier B_c: both waves' shares of X_{c+1} visible
-            floatx4 y[2];
-            const floatx4 z[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-            for (int i = 0; i < 2; ++i) y[i] = own[i] + sY[1 - w][i][lane];
-            // R'_{c+1}, published for chunk c+1
-            rfo = rprime(y, z, 1.f, bn);
-            sRf[1 - x2][w][lane] = rfo;
+            for (int m = 0; m < HMD; ++m) {
+                const int md = w * HMD + m;
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2)
+                        offT[m][kk][h2] = kq(32 * kk + 16 * h2 + 4 * lg + (l16 >> 2),
+                                             32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1));
+            }
+            bf16x8 sfo[HKD], rfo;   // this wave's halves of S_c and R'_c
+            auto publish_s = [&](int par) {
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) {
+                    sfo[k2] = pack_bf16(acc[2 * k2], acc[2 * k2 + 1]);
+                    sSf[par][w * HKD + k2][lane] = sfo[k2];
+                }
+            };
+            // R' rows of this wave's token tiles from X = K S^T: V - diag(gamma) X
+            struct VG {
+                short4v vv[2];
+                floatx4 gm[2];
+            };
+            auto load_vg = [&](int bn) {
+                VG r;
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    r.vv[i] = lds_tr8(&sV[bn][offV[i]]);
+                    r.gm[i] = *reinterpret_cast<const floatx4*>(&sG[bn][16 * (2 * w + i) + 4 * lg]);
+                }
+                return r;
+            };
+            auto rprime = [&](const floatx4 (&y)[2], const VG& vg) {
+                floatx4 rr[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) rr[i][e] = bf(vg.vv[i][e]) - vg.gm[i][e] * y[i][e];
+                return pack_bf16(rr[0], rr[1]);
+            };
+            lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
+            if (nc > 0) publish_s(0);
+            lds_barrier();   // prologue 2: S_0 halves visible
+            if (nc > 0) {    // R'_0 = V_0 - diag(gamma_0) K_0 S_0^T for this wave's token tiles
+                bf16x8 sfx[HKD];
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) sfx[k2] = sSf[0][(1 - w) * HKD + k2][lane];
+                floatx4 y[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    y[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int k2 = 0; k2 < HKD; ++k2) {
+                        const int r = 16 * (2 * w + i) + l16;
+                        y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * (w * HKD + k2) + 8 * lg)]), sfo[k2], y[i], 0, 0, 0);
+                        y[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            *reinterpret_cast<const bf16x8*>(&sK[0][kq(r, 32 * ((1 - w) * HKD + k2) + 8 * lg)]), sfx[k2], y[i],
+                            0, 0, 0);
+                    }
+                }
+                rfo = rprime(y, load_vg(0));
+                sRf[0][w][lane] = rfo;
+            }
+            // K_{c+1} rows of all four token tiles over this wave's key blocks (the
+            // partial products X_{c+1} = K_{c+1} S_{c+1}^T the waves exchange)
+            int offY[4][HKD];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int k2 = 0; k2 < HKD; ++k2) offY[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
+            auto cstep = [&](auto SLOT) {   // chunk c = SLOT (mod RING)
+                constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
+                lds_barrier();   // barrier A_c: S_c halves and R'_c visible
+                const bf16x8 rfx = sRf[x2][1 - w][lane];
+                const bf16x8 rf0 = sel(w == 0, rfo, rfx), rf1 = sel(w == 0, rfx, rfo);
+                const float gn = sG[b][CH - 1];
+                bf16x8 wf[NFRAG], ka[HMD][2], ky[4][HKD];
+#pragma unroll
+                for (int f = 0; f < NFRAG; ++f) wf[f] = sW[b][f][lane];
+#pragma unroll
+                for (int m = 0; m < HMD; ++m)
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk)
+                        ka[m][kk] = join4(lds_tr8(&sK[b][offT[m][kk][0]]), lds_tr8(&sK[b][offT[m][kk][1]]));
+                // chunk c+1's operands are resident since barrier A_c: read them ahead of
+                // the products that need them
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int k2 = 0; k2 < HKD; ++k2) ky[mt][k2] = *reinterpret_cast<const bf16x8*>(&sK[bn][offY[mt][k2]]);
+                const VG vg = load_vg(bn);
+                // D U = W R' (lower triangular: tile mt needs blocks 0..mt/2); S^T <- gn S^T + K^T (D U)
+                floatx4 du[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 0)], rf0, floatx4{0.f, 0.f, 0.f, 0.f},
+                                                                     0, 0, 0);
+                    if (mt >= 2) du[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[frag_id(mt, 1)], rf1, du[mt], 0, 0, 0);
+                }
+                const bf16x8 df0 = pack_bf16(du[0], du[1]), df1 = pack_bf16(du[2], du[3]);
+#pragma unroll
+                for (int m = 0; m < HMD; ++m) {
+                    acc[m] *= gn;
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
+                }
+                // S_{c+1}: this wave's half for the output waves, and its share of X_{c+1}
+                publish_s(1 - x2);
+                floatx4 yp[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    yp[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int k2 = 0; k2 < HKD; ++k2)
+                        yp[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ky[mt][k2], sfo[k2], yp[mt], 0, 0, 0);
+                }
+                // (whole-value selects: a runtime index into a register array would go to scratch)
+                floatx4 own[2], oth[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    own[i] = w == 0 ? yp[i] : yp[2 + i];
+                    oth[i] = w == 0 ? yp[2 + i] : yp[i];
+                    sY[w][i][lane] = oth[i];   // the other wave's token tiles
+                }
+                lds_barrier();   // barrier B_c: both waves' shares of X_{c+1} visible
+                floatx4 y[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) y[i] = own[i] + sY[1 - w][i][lane];
+                // R'_{c+1}, published for chunk c+1
+                rfo = rprime(y, vg);
+                sRf[1 - x2][w][lane] = rfo;
+            };
+            for (int c = 0; c < nc; c += RING) {
+                cstep(Ic<0>{});
+                if (c + 1 < nc) cstep(Ic<1>{});
+                if (c + 2 < nc) cstep(Ic<2>{});
+                if (c + 3 < nc) cstep(Ic<3>{});
+            }
+            if (p.ST) {
+#pragma unroll
+                for (int m = 0; m < HMD; ++m)
+                    *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
+            }
         };
-        for (int c = 0; c < nc; c += RING) {
-            cstep(Ic<0>{});
-            if (c + 1 < nc) cstep(Ic<1>{});
-            if (c + 2 < nc) cstep(Ic<2>{});
-            if (c + 3 < nc) cstep(Ic<3>{});
-        }
-        if (p.ST) {
-#pragma unroll
-            for (int m = 0; m < HMD; ++m)
-                *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
-        }
+        if (wave == 0) chain(Ic<0>{});
+        else chain(Ic<1>{});
     } else {
         // ------------------------------------------------ output waves
         // Wave 2 + o handles token tiles 2o, 2o + 1 (rows 32o .. 32o + 31).  Its Q
         // rows are staged in LDS by buffer loads (whole 128-byte lines, XOR-swizzled
-        // like K), one chunk ahead.  P' token tile mt needs fragments (mt, 0..mt/2):
-        // wave 2 fragments 0, 1; wave 3 fragments 2, 3, 4, 5.
+        // like K), two chunks ahead in two buffers.  P' token tile mt needs fragments
+        // (mt, 0..mt/2): wave 2 fragments 0, 1; wave 3 fragments 2, 3, 4, 5.
         auto run = [&](auto OW) {
             constexpr int ow = decltype(OW)::value, NPP = ow ? 4 : 2;
             const bf16_t* wsP = reinterpret_cast<const bf16_t*>(p.wsP);
-            bf16_t* sq = sQ[ow];
+
             int qoff[32 / RPI];   // byte offsets of this lane's Q row loads within a chunk
 #pragma unroll
             for (int j = 0; j < 32 / RPI; ++j) {
                 const int r = RPI * j + lane / NCH;
                 qoff[j] = ((32 * ow + r) * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             }
-            auto load_q = [&](int c) {
+            auto load_q = [&](int c, bf16_t* sq) {
                 const auto rq = crsrc(p.q, DK, c);
 #pragma unroll
                 for (int j = 0; j < 32 / RPI; ++j) bdma16(rq, sq + RPI * j * DK, qoff[j]);
@@ -1024,24 +1043,28 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int k = 0; k < NPP; ++k) pa[k] = bload16<AUX>(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
             };
-            // Per chunk this wave issues, in order: the next chunk's Q copy, its P'
-            // loads, then two output stores (buffer stores, so tokens past the
-            // chunk end are dropped by the descriptor and the count is fixed).
-            // Global memory operations complete in issue order, so at the next
-            // chunk's start waiting until NPP remain covers the Q copy.
+            // Per chunk c this wave issues, in order: the P' loads of chunk c+1, the
+            // Q copy of chunk c+2 (into the buffer chunk c's rows leave), then two
+            // output stores (buffer stores, so tokens past the chunk end are
+            // dropped by the descriptor and the count is fixed).  Global memory
+            // operations complete in issue order, so at a chunk's start waiting
+            // until 32 / RPI remain covers its P' loads and its Q copy.  (Chunk c+2's
+            // terms are published: a loader saw its flag before barrier A_c.)
+            constexpr int NQ = 32 / RPI;
             auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
+                bf16_t* sq = sQ[x2][ow];
                 lds_barrier();   // barrier A_c: S_c and R'_c visible
-                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NPP) : "memory");   // Q_c staged
+                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NQ) : "memory");   // Q_c staged, P'_c loaded
                 bf16x8 qa[2][NKD];
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
 #pragma unroll
                     for (int kk = 0; kk < NKD; ++kk)
                         qa[i][kk] = *reinterpret_cast<const bf16x8*>(sq + kq(16 * i + l16, 32 * kk + 8 * lg));
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // staging area read: free for Q_{c+1}
-                load_q(min(c + 1, nc - 1));
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // staging buffer read: free for Q_{c+2}
                 load_p(min(c + 1, nc - 1), pn);
+                load_q(min(c + 2, nc - 1), sq);
                 const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
                 const auto ro = crsrc(p.o, DV, c);
 #pragma unroll
@@ -1069,8 +1092,9 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             bf16x8 pA[NPP], pB[NPP];
             lds_barrier();   // prologue 1: the loaders have seen chunks 0..2's terms published
             if (nc > 0) {
-                load_q(0);
                 load_p(0, pA);
+                load_q(0, sQ[0][ow]);
+                load_q(min(1, nc - 1), sQ[1][ow]);
             }
             lds_barrier();   // prologue 2
             for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
@@ -1293,17 +1317,11 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
         case 2: store_gram<DK, 2>(sA, sPb, l16, lg, ablk, pblk); break;
         default: store_gram<DK, 3>(sA, sPb, l16, lg, ablk, pblk); break;
     }
-    for (int i = tid; i < 6 * 256; i += NT) {   // P's six upper blocks are zero
-        int t = i / 256, bj = 1;
-        while (t >= bj) { t -= bj; ++bj; }
-        const int e = i % 256;
-        sPb[16 * t + e / 16][16 * bj + e % 16] = 0;
-    }
     __syncthreads();
 
     // T = (I + A)^{-1}: diagonal blocks by forward substitution, one wave, lane =
-    // 16 * block + column, A's block rows in registers; meanwhile the other
-    // waves clear T's upper blocks
+    // 16 * block + column, A's block rows in registers.  The upper blocks of P
+    // and T are never stored: their readers take them as zero.
     if (wave == 0) {
         const int b = lg;
         float a[16][16];
@@ -1324,13 +1342,6 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
             for (int r = i + 1; r < 16; ++r) x[r] -= a[r][i] * x[i];
 #pragma unroll
         for (int r = 0; r < 16; ++r) sTi[16 * b + r][16 * b + l16] = x[r];
-    } else {
-        for (int i = tid - 64; i < 6 * 256; i += NT - 64) {
-            int t = i / 256, bj = 1;
-            while (t >= bj) { t -= bj; ++bj; }
-            const int e = i % 256;
-            sTi[16 * t + e / 16][16 * bj + e % 16] = 0.f;
-        }
     }
     __syncthreads();
     // off-diagonal blocks, diagonal d: T_{b,b-d} = -T_bb sum_{m} A_bm T_{m,b-d}.
@@ -1355,9 +1366,10 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
         }
         __syncthreads();
     }
-    for (int i = tid; i < CH * CH / 4; i += NT) {   // bf16 copy of T (A is no longer read)
+    for (int i = tid; i < CH * CH / 4; i += NT) {   // bf16 copy of T, zero above the diagonal blocks (A is no longer read)
         const int r = i / (CH / 4), c4 = 4 * (i % (CH / 4));
-        const floatx4 v = *reinterpret_cast<const floatx4*>(&sTi[r][c4]);
+        floatx4 v = *reinterpret_cast<const floatx4*>(&sTi[r][c4]);
+        if ((c4 >> 4) > (r >> 4)) v = floatx4{0.f, 0.f, 0.f, 0.f};
         *reinterpret_cast<bf16x4*>(&sTb[r][c4]) = __builtin_convertvector(v, bf16x4);
     }
     __syncthreads();
@@ -1370,8 +1382,10 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
         const float dr = sD[r];
         const floatx4 b0 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 4 * lg]);
         const floatx4 b1 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 16 + 4 * lg]);
-        const floatx4 w0 = dr * b0 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 4 * lg]);
-        const floatx4 w1 = dr * b1 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 16 + 4 * lg]);
+        const floatx4 zero = {0.f, 0.f, 0.f, 0.f};   // blocks of T above the diagonal
+        const floatx4 w0 = 2 * kk2 > mt ? zero : dr * b0 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 4 * lg]);
+        const floatx4 w1 =
+            2 * kk2 + 1 > mt ? zero : dr * b1 * *reinterpret_cast<const floatx4*>(&sTi[r][32 * kk2 + 16 + 4 * lg]);
         if (store) bstore16<AUX>(pack_bf16(w0, w1), rW, (f * 64 + lane) * 16);
         // P' fragment from (T^T P^T) tiles (tau block 2 kk2 + hb, token block mt)
         floatx4 pt[2];
@@ -1384,7 +1398,8 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
             for (int kk = 0; kk < 2; ++kk) {
                 const bf16_t* t0p = &sTb[32 * kk + 8 * lg + (l16 >> 2)][16 * bt + 4 * (l16 & 3)];
                 const bf16x8 a = join4(lds_tr8(t0p), lds_tr8(t0p + 4 * PB));
-                const bf16x8 bb = *reinterpret_cast<const bf16x8*>(&sPb[16 * mt + l16][32 * kk + 8 * lg]);
+                bf16x8 bb = *reinterpret_cast<const bf16x8*>(&sPb[16 * mt + l16][32 * kk + 8 * lg]);
+                if (2 * kk + (lg >> 1) > mt) bb = bf16x8{};   // blocks of P above the diagonal
                 pt[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb, pt[hb], 0, 0, 0);
             }
             pt[hb] *= hb ? b1 : b0;
