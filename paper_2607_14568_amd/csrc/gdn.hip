@@ -190,25 +190,39 @@ __device__ void block_scan(int32_t* x, int n, bool reverse, int* part) {
 // Ragged sequence table: clamped starts and lengths, first chunk slot of each
 // sequence; the sequences ordered by chunk count, longest first (perm); and
 // prefix[c] = number of (sequence, chunk index c' < c) pairs, i.e. the sum over
-// c' < c of the number of sequences with more than c' chunks.  hist: cpt + 2
-// ints of scratch.  One workgroup of NSET threads.
+// c' < c of the number of sequences with more than c' chunks.  ghist: cpt + 2
+// ints of scratch, used when the histogram does not fit in LDS.  One workgroup
+// of NSET threads.
 __global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_seq, int T, int32_t* seq_start,
                                                       int32_t* seq_len, int32_t* chunk_off, int32_t* perm,
-                                                      int32_t* prefix, int32_t* hist, int cpt) {
+                                                      int32_t* prefix, int32_t* ghist, int cpt) {
     __shared__ int part[NSET];
+    __shared__ int scu[NSET + 1];
+    __shared__ int shist[8192];
+    int32_t* hist = cpt + 2 <= 8192 ? shist : ghist;   // the histogram in LDS when it fits
     const int t = threadIdx.x;
-    if (t == 0) {   // offsets clamped into a partition of [0, T]
-        int b = min(max(cu[0], 0), T);
-        int acc = 0;
-        chunk_off[0] = 0;
-        for (int s = 0; s < n_seq; ++s) {
-            const int e = min(max(cu[s + 1], b), T);
-            seq_start[s] = b;
-            seq_len[s] = e - b;
-            acc += (e - b + CH - 1) / CH;
-            chunk_off[s + 1] = acc;
-            b = e;
+    // offsets clamped into a partition of [0, T]: a serial walk by thread 0 over
+    // blocks of offsets that all threads fetch at once
+    int b = 0, acc = 0;
+    for (int s0 = 0; s0 < n_seq; s0 += NSET) {
+        const int m = min(NSET, n_seq - s0);
+        for (int i = t; i <= m; i += NSET) scu[i] = cu[s0 + i];
+        __syncthreads();
+        if (t == 0) {
+            if (s0 == 0) {
+                b = min(max(scu[0], 0), T);
+                chunk_off[0] = 0;
+            }
+            for (int i = 0; i < m; ++i) {
+                const int e = min(max(scu[i + 1], b), T);
+                seq_start[s0 + i] = b;
+                seq_len[s0 + i] = e - b;
+                acc += (e - b + CH - 1) / CH;
+                chunk_off[s0 + i + 1] = acc;
+                b = e;
+            }
         }
+        __syncthreads();
     }
     for (int c = t; c <= cpt + 1; c += NSET) hist[c] = 0;
     __syncthreads();
