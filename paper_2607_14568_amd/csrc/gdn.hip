@@ -1232,10 +1232,11 @@ template <int DK> struct TermsLds {
 // threads are tid = 0..255.  store = false computes without writing (a
 // placeholder item that keeps a workgroup's two halves in step).  FUSED: every
 // result is stored with cache-bypassing stores, then the slot's flag is set to
-// the call's epoch.
+// the call's epoch; and the item's V rows, which only the chain reads, are
+// copied into vsink (LDS nobody reads) so that they wait in L2 for the chain.
 template <int DK, bool FUSED>
 __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi, TermsLds<DK>& lds, const int tid,
-                                                 const bool store) {
+                                                 const bool store, bf16_t* vsink = nullptr) {
     constexpr int NCH = DK / 8;     // 16-byte chunks per K/Q row
     constexpr int RPI = 64 / NCH;   // rows per 1 KB buffer load
     constexpr int TILE = CH * DK;
@@ -1315,6 +1316,13 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if constexpr (FUSED) {   // V rows of the item into L2 (waited for before the flag is set)
+        const int DV = p.DV, vch = DV / 8, vrpi = 64 / vch;
+        const auto rv = rsrc(reinterpret_cast<const bf16_t*>(p.v) + (t0 * H + h) * DV,
+                             (uint32_t)(((long)(n - 1) * H + 1) * DV * 2));
+        for (int i = wave; i < CH / vrpi; i += 4)
+            bdma16(rv, vsink + i * 512, ((vrpi * i + lane / vch) * H * DV + (lane % vch) * 8) * 2);
+    }
 
     // token-token blocks, all operands in registers
     floatx4 ablk[3], pblk[3];
@@ -1443,7 +1451,10 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
     static_assert(NT_CHAIN == 2 * NT, "two work items per chunk-terms workgroup");
     __shared__ union Lds {
         ChainLds<DK> c;
-        TermsLds<DK> t[2];
+        struct {
+            TermsLds<DK> t;
+            bf16_t vsink[CH * 128];
+        } t[2];
     } lds;
     if ((int)blockIdx.x < p.npw) {
         const int half = threadIdx.x / NT;
@@ -1459,14 +1470,14 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
                 const long j = min(k + half, items - 1);
                 const int c = (int)(j / ((long)p.n_seq * hu)), r = (int)((j / hu) % p.n_seq), u = (int)(j % hu);
                 const long gi = ((long)r * p.NC + c) * H + h0 + 8 * u;
-                chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
+                chunk_terms_bf16<DK, true>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items, lds.t[half].vsink);
                 __syncthreads();   // the next item reuses the LDS
             }
         } else {
             const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
             for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
                 const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
-                chunk_terms_bf16<DK, true>(p, gi, lds.t[half], threadIdx.x % NT, k + half < items);
+                chunk_terms_bf16<DK, true>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items, lds.t[half].vsink);
                 __syncthreads();   // the next item reuses the LDS
             }
         }
