@@ -795,38 +795,62 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     (uint32_t)(((long)(rows(c) - 1) * H + 1) * width * 2));
     };
 
-    if (wave >= 4) {
-        // ------------------------------------------------ loaders
-        // One wave issues global loads at about a third of a CU's rate, so four
-        // waves share the copies: K load groups, W fragments with index =
-        // loader (mod 4), the two V loads on loaders 2 and 3, gamma on loader 0.
-        const int li = wave - 4;
+    if (FUSED && wave == 7) {
+        // ------------------------------------------------ flag poller (one launch only)
+        // Observes each chunk's flag one chunk before the loaders copy its terms
+        // (the flag's memory round trip then overlaps a chunk's work, and the
+        // loaders wait on their own copies only): chunks 0..2 before barrier P,
+        // chunk 3 before the first chunk, chunk c+4 during chunk c.  The loaders'
+        // copies of a chunk follow its observation through the barriers.
         int spins = 1 << 22;   // ~0.2 s of sleeping in all; the chunk-terms workgroups never wait
+        auto seen = [&](int c) {
+            return __hip_atomic_load(&p.flags[slot(c)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == p.epoch;
+        };
+        auto wait_flag = [&](int c, bool ok) {
+            while (!ok && spins > 0) {
+                --spins;
+                __builtin_amdgcn_s_sleep(2);
+                ok = seen(c);
+            }
+        };
+        if (FUSED && nc > 0)
+            for (int c = 0; c < 3; ++c) wait_flag(min(c, nc - 1), seen(min(c, nc - 1)));
+        lds_barrier();   // prologue P: chunks 0..2's terms published
+        if (FUSED && nc > 0) wait_flag(min(3, nc - 1), seen(min(3, nc - 1)));
+        lds_barrier();   // prologue 1
+        lds_barrier();   // prologue 2
+        for (int c = 0; c < nc; ++c) {
+            lds_barrier();   // A_c
+            const bool ok = FUSED ? seen(min(c + 4, nc - 1)) : true;
+            lds_barrier();   // B_c
+            if (FUSED) wait_flag(min(c + 4, nc - 1), ok);
+        }
+    } else if (wave >= 4) {
+        // ------------------------------------------------ loaders
+        // One wave issues global loads at about a third of a CU's rate, so NL
+        // waves share the copies (four, or three beside the flag poller): K load
+        // groups and W fragments with index = loader (mod NL), the two V loads on
+        // loaders NL-2 and NL-1, gamma on loader 0.
+        constexpr int NL = FUSED ? 3 : 4;
+        const int li = wave - 4;
         const bf16_t* wsT = reinterpret_cast<const bf16_t*>(p.wsT);
-        int koff[NCH / 4];   // loop-invariant byte offsets of this lane's K loads within a chunk
+        int koff[(NCH + NL - 1) / NL];   // loop-invariant byte offsets of this lane's K loads within a chunk
 #pragma unroll
-        for (int j = 0; j < NCH / 4; ++j) {
-            const int r = RPI * (li + 4 * j) + lane / NCH;
+        for (int j = 0; j < (NCH + NL - 1) / NL; ++j) {
+            const int r = RPI * (li + NL * j) + lane / NCH;
             koff[j] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
         }
-        const int voff = ((32 * (li & 1) + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
+        const int voff = ((32 * (li == NL - 1) + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
         auto issue = [&](int c, auto SLOT, auto LI) {
             constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
             const long sc = slot(c);
-            if constexpr (FUSED) {   // wait for the chunk's terms, within one budget for the whole call
-                while (__hip_atomic_load(&p.flags[sc], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != p.epoch &&
-                       spins > 0) {
-                    --spins;
-                    __builtin_amdgcn_s_sleep(2);
-                }
-            }
             const auto rk = crsrc(p.k, DK, c);
 #pragma unroll
-            for (int j = 0; j < NCH / 4; ++j) bdma16(rk, &sK[sl][RPI * (L + 4 * j) * DK], koff[j]);
+            for (int i = L; i < NCH; i += NL) bdma16(rk, &sK[sl][RPI * i * DK], koff[i / NL]);
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
-            for (int f = L; f < NFRAG; f += 4) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
-            if constexpr (L >= 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L & 1) * SL], voff);
+            for (int f = L; f < NFRAG; f += NL) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
+            if constexpr (L >= NL - 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L == NL - 1) * SL], voff);
             if constexpr (L == 0) bdma4<AUX>(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
         };
         // After barrier A_c every wave is done with chunk c-1, whose slot is
@@ -834,7 +858,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         // those loads in flight, so chunk c+2 has landed before barrier A_{c+1}.
         auto run = [&](auto LI) {
             constexpr int L = decltype(LI)::value;
-            constexpr int NI = NCH / 4 + (NFRAG - L + 3) / 4 + (L >= 2) + (L == 0);
+            constexpr int NI = (NCH - L + NL - 1) / NL + (NFRAG - L + NL - 1) / NL + (L >= NL - 2) + (L == 0);
             auto lstep = [&](int c, auto SLOT) {
                 constexpr int bn = (decltype(SLOT)::value + 3) % RING;
                 lds_barrier();   // A_c
@@ -842,6 +866,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 lds_barrier();   // B_c
                 asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
             };
+            lds_barrier();   // prologue P
             if (nc > 0) {
                 issue(0, Ic<0>{}, LI);
                 issue(min(1, nc - 1), Ic<1>{}, LI);
@@ -862,7 +887,9 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             case 0: run(Ic<0>{}); break;
             case 1: run(Ic<1>{}); break;
             case 2: run(Ic<2>{}); break;
-            default: run(Ic<3>{}); break;
+            default:
+                if constexpr (NL > 3) run(Ic<3>{});
+                break;
         }
     } else if (wave < 2) {
         // ------------------------------------------------ chain waves
@@ -924,6 +951,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     for (int e = 0; e < 4; ++e) rr[i][e] = bf(vg.vv[i][e]) - vg.gm[i][e] * y[i][e];
                 return pack_bf16(rr[0], rr[1]);
             };
+            lds_barrier();   // prologue P: chunks 0..2's terms published
             lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
             if (nc > 0) publish_s(0);
             lds_barrier();   // prologue 2: S_0 halves visible
@@ -1104,7 +1132,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 lds_barrier();   // B_c (the chain waves' exchange of X_{c+1}); S_c and R'_c are no longer read
             };
             bf16x8 pA[NPP], pB[NPP];
-            lds_barrier();   // prologue 1: the loaders have seen chunks 0..2's terms published
+            lds_barrier();   // prologue P: chunks 0..2's terms published
+            lds_barrier();   // prologue 1
             if (nc > 0) {
                 load_p(0, pA);
                 load_q(0, sQ[0][ow]);
