@@ -841,17 +841,25 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             koff[j] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
         }
         const int voff = ((32 * (li == NL - 1) + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
-        auto issue = [&](int c, auto SLOT, auto LI) {
+        // a chunk's copies of the inputs (K, V) and of its chunk terms (W, gamma)
+        auto issue_in = [&](int c, auto SLOT, auto LI) {
             constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
-            const long sc = slot(c);
             const auto rk = crsrc(p.k, DK, c);
 #pragma unroll
             for (int i = L; i < NCH; i += NL) bdma16(rk, &sK[sl][RPI * i * DK], koff[i / NL]);
+            if constexpr (L >= NL - 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L == NL - 1) * SL], voff);
+        };
+        auto issue_terms = [&](int c, auto SLOT, auto LI) {
+            constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
+            const long sc = slot(c);
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
             for (int f = L; f < NFRAG; f += NL) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
-            if constexpr (L >= NL - 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L == NL - 1) * SL], voff);
             if constexpr (L == 0) bdma4<AUX>(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+        };
+        auto issue = [&](int c, auto SLOT, auto LI) {
+            issue_in(c, SLOT, LI);
+            issue_terms(c, SLOT, LI);
         };
         // After barrier A_c every wave is done with chunk c-1, whose slot is
         // (c+3) % RING: chunk c+3 is loaded there, and the wait leaves only
@@ -866,11 +874,16 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 lds_barrier();   // B_c
                 asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI) : "memory");
             };
+            if (nc > 0) {   // the inputs need no chunk terms: copied while those are formed
+                issue_in(0, Ic<0>{}, LI);
+                issue_in(min(1, nc - 1), Ic<1>{}, LI);
+                issue_in(min(2, nc - 1), Ic<2>{}, LI);
+            }
             lds_barrier();   // prologue P
             if (nc > 0) {
-                issue(0, Ic<0>{}, LI);
-                issue(min(1, nc - 1), Ic<1>{}, LI);
-                issue(min(2, nc - 1), Ic<2>{}, LI);
+                issue_terms(0, Ic<0>{}, LI);
+                issue_terms(min(1, nc - 1), Ic<1>{}, LI);
+                issue_terms(min(2, nc - 1), Ic<2>{}, LI);
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             lds_barrier();   // prologue 1: chunks 0, 1 and 2 resident
@@ -1090,8 +1103,9 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             // output stores (buffer stores, so tokens past the chunk end are
             // dropped by the descriptor and the count is fixed).  Global memory
             // operations complete in issue order, so at a chunk's start waiting
-            // until 32 / RPI remain covers its P' loads and its Q copy.  (Chunk c+2's
-            // terms are published: a loader saw its flag before barrier A_c.)
+            // until 32 / RPI remain covers its P' loads and its Q copy.  (Chunk c+1's
+            // terms are published: in one launch the flag poller saw its flag three
+            // chunks earlier; with two launches the chunk terms came first.)
             constexpr int NQ = 32 / RPI;
             auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
@@ -1132,13 +1146,14 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 lds_barrier();   // B_c (the chain waves' exchange of X_{c+1}); S_c and R'_c are no longer read
             };
             bf16x8 pA[NPP], pB[NPP];
-            lds_barrier();   // prologue P: chunks 0..2's terms published
-            lds_barrier();   // prologue 1
-            if (nc > 0) {
-                load_p(0, pA);
+            if (nc > 0) {   // Q is an input: staged while the first chunk terms are formed
                 load_q(0, sQ[0][ow]);
                 load_q(min(1, nc - 1), sQ[1][ow]);
             }
+            lds_barrier();   // prologue P: chunks 0..2's terms published
+            lds_barrier();   // prologue 1
+            if (nc > 0) load_p(0, pA);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // (the first chunk's wait assumes the steady-state order)
             lds_barrier();   // prologue 2
             for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
                 ostep(c, Ic<0>{}, pA, pB);
