@@ -1098,20 +1098,23 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int k = 0; k < NPP; ++k) pa[k] = bload16<AUX>(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
             };
-            // Per chunk c this wave issues, in order: the P' loads of chunk c+1, the
-            // Q copy of chunk c+2 (into the buffer chunk c's rows leave), then two
-            // output stores (buffer stores, so tokens past the chunk end are
-            // dropped by the descriptor and the count is fixed).  Global memory
-            // operations complete in issue order, so at a chunk's start waiting
-            // until 32 / RPI remain covers its P' loads and its Q copy.  (Chunk c+1's
-            // terms are published: in one launch the flag poller saw its flag three
-            // chunks earlier; with two launches the chunk terms came first.)
+            // In chunk c this wave issues the P' loads of chunk c+2, into register
+            // set (c+2) % 4, and the Q copy of chunk c+2, into the buffer chunk c's
+            // rows leave: in one launch after barrier B_c (the loader waves' copies
+            // go out between A_c and B_c), with two launches as soon as chunk c's
+            // rows are read.  Loads complete in issue order, so at a chunk's start
+            // waiting until NPP + NQ remain covers its P' loads and its Q copy.
+            // (Chunk c+2's terms are published: in one launch the flag poller saw
+            // its flag two chunks earlier; with two launches the chunk terms came
+            // first.)
             constexpr int NQ = 32 / RPI;
-            auto ostep = [&](int c, auto SLOT, bf16x8(&pa)[NPP], bf16x8(&pn)[NPP]) {
+            bf16x8 pS[RING][NPP];   // P' fragments by ring slot
+            auto ostep = [&](int c, auto SLOT) {
                 constexpr int b = decltype(SLOT)::value, x2 = b & 1;
+                const bf16x8(&pa)[NPP] = pS[b];
                 bf16_t* sq = sQ[x2][ow];
                 lds_barrier();   // barrier A_c: S_c and R'_c visible
-                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NQ) : "memory");   // Q_c staged, P'_c loaded
+                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NPP + NQ) : "memory");   // Q_c staged, P'_c loaded
                 bf16x8 qa[2][NKD];
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
@@ -1119,8 +1122,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     for (int kk = 0; kk < NKD; ++kk)
                         qa[i][kk] = *reinterpret_cast<const bf16x8*>(sq + kq(16 * i + l16, 32 * kk + 8 * lg));
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // staging buffer read: free for Q_{c+2}
-                load_p(min(c + 1, nc - 1), pn);
-                load_q(min(c + 2, nc - 1), sq);
+                if constexpr (!FUSED) {
+                    load_p(min(c + 2, nc - 1), pS[(b + 2) % RING]);
+                    load_q(min(c + 2, nc - 1), sq);
+                }
                 const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
                 const auto ro = crsrc(p.o, DV, c);
 #pragma unroll
@@ -1144,22 +1149,28 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                                                           (tok * H * DV + js * SL + 4 * lg) * 2, 0, 0);
                 }
                 lds_barrier();   // B_c (the chain waves' exchange of X_{c+1}); S_c and R'_c are no longer read
+                if constexpr (FUSED) {
+                    load_p(min(c + 2, nc - 1), pS[(b + 2) % RING]);
+                    load_q(min(c + 2, nc - 1), sq);
+                }
             };
-            bf16x8 pA[NPP], pB[NPP];
             if (nc > 0) {   // Q is an input: staged while the first chunk terms are formed
                 load_q(0, sQ[0][ow]);
                 load_q(min(1, nc - 1), sQ[1][ow]);
             }
             lds_barrier();   // prologue P: chunks 0..2's terms published
             lds_barrier();   // prologue 1
-            if (nc > 0) load_p(0, pA);
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // (the first chunk's wait assumes the steady-state order)
+            if (nc > 0) {
+                load_p(0, pS[0]);
+                load_p(min(1, nc - 1), pS[1]);
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // (the first chunks' waits assume the steady-state order)
             lds_barrier();   // prologue 2
-            for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment buffers are constants
-                ostep(c, Ic<0>{}, pA, pB);
-                if (c + 1 < nc) ostep(c + 1, Ic<1>{}, pB, pA);
-                if (c + 2 < nc) ostep(c + 2, Ic<2>{}, pA, pB);
-                if (c + 3 < nc) ostep(c + 3, Ic<3>{}, pB, pA);
+            for (int c = 0; c < nc; c += RING) {   // unrolled so ring slot and fragment set are constants
+                ostep(c, Ic<0>{});
+                if (c + 1 < nc) ostep(c + 1, Ic<1>{});
+                if (c + 2 < nc) ostep(c + 2, Ic<2>{});
+                if (c + 3 < nc) ostep(c + 3, Ic<3>{});
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         };
