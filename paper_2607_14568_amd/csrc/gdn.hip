@@ -1099,10 +1099,11 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 for (int k = 0; k < NPP; ++k) pa[k] = bload16<AUX>(rp, ((ow ? 2 + k : k) * 64 + lane) * 16);
             };
             // In chunk c this wave issues the P' loads of chunk c+2, into register
-            // set (c+2) % 4, and the Q copy of chunk c+2, into the buffer chunk c's
-            // rows leave: in one launch after barrier B_c (the loader waves' copies
-            // go out between A_c and B_c), with two launches as soon as chunk c's
-            // rows are read.  Loads complete in issue order, so at a chunk's start
+            // set (c+2) % 4, the Q copy of chunk c+2, into the buffer chunk c's rows
+            // leave, and chunk c's output stores: in one launch all after barrier
+            // B_c (the loader waves' copies go out between A_c and B_c), with two
+            // launches the loads as soon as chunk c's rows are read and the stores
+            // as the outputs are formed.  Loads complete in issue order, so at a chunk's start
             // waiting until NPP + NQ remain covers its P' loads and its Q copy.
             // (Chunk c+2's terms are published: in one launch the flag poller saw
             // its flag two chunks earlier; with two launches the chunk terms came
@@ -1128,6 +1129,12 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 }
                 const bf16x8 rf0 = sRf[x2][0][lane], rf1 = sRf[x2][1][lane];
                 const auto ro = crsrc(p.o, DV, c);
+                typedef int int2v __attribute__((ext_vector_type(2)));
+                int2v ovs[2];
+                auto store_o = [&](int i) {   // 4 value channels of token 16 (2 ow + i) + l16
+                    __builtin_amdgcn_raw_buffer_store_b64(ovs[i], ro, ((16 * (2 * ow + i) + l16) * H * DV + js * SL + 4 * lg) * 2,
+                                                          0, 0);
+                };
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int mt = 2 * ow + i, tok = 16 * mt + l16;
@@ -1144,14 +1151,15 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                         op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pa[2 * i + 1], op, 0, 0, 0);
                     }
                     const floatx4 ov = p.scale * (gm * oq + op);   // value channels 4 lg .. 4 lg + 3 of token tok
-                    typedef int int2v __attribute__((ext_vector_type(2)));
-                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, __builtin_convertvector(ov, bf16x4)), ro,
-                                                          (tok * H * DV + js * SL + 4 * lg) * 2, 0, 0);
+                    ovs[i] = __builtin_bit_cast(int2v, __builtin_convertvector(ov, bf16x4));
+                    if constexpr (!FUSED) store_o(i);
                 }
                 lds_barrier();   // B_c (the chain waves' exchange of X_{c+1}); S_c and R'_c are no longer read
                 if constexpr (FUSED) {
                     load_p(min(c + 2, nc - 1), pS[(b + 2) % RING]);
                     load_q(min(c + 2, nc - 1), sq);
+                    store_o(0);
+                    store_o(1);
                 }
             };
             if (nc > 0) {   // Q is an input: staged while the first chunk terms are formed
