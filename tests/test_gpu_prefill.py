@@ -226,3 +226,11 @@ def test_dense_batch_through_two_launches(T):
     chain, so the chunk terms run as their own launch before it."""
     x = inputs.make_prefill(B=2, T=T, H=16, dk=128, dv=128, io="bf16", seed=T + 5, s0_std=0.05)
     _check(x, "bf16", "B=2 T=%d H=16 bf16 (two launches)" % T)
+
+
+@pytest.mark.parametrize("B,H,T", [(1, 8, 700), (2, 8, 600), (1, 24, 450)])
+def test_one_launch_item_order_per_xcd(B, H, T):
+    """One launch with 8 | H (chunk-terms items walked per XCD, several sequences and heads per
+    workgroup) and with the poller observing flags ahead of the loaders through the tail chunks."""
+    x = inputs.make_prefill(B=B, T=T, H=H, dk=128, dv=128, io="bf16", seed=B * 100 + H + T, s0_std=0.05)
+    _check(x, "bf16", "B=%d T=%d H=%d bf16 (one launch, per-XCD item order)" % (B, T, H))
