@@ -663,12 +663,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 //    for one half of the chunk's tokens, from the published S_c and R'_c --
 //    the operands swapped, so a lane ends up with 4 consecutive value channels
 //    of one token and writes them with one 8-byte store.  Each stages its Q rows
-//    in LDS one chunk ahead (buffer loads of whole cache lines: register loads
+//    in LDS two chunks ahead (buffer loads of whole cache lines: register loads
 //    in the MFMA layout would read 64-byte halves) and loads its P' fragments
-//    straight into registers.
+//    straight into registers, also two chunks ahead.
 //  waves 4..7 ("loaders"): copy chunk c+3 (K, W, the V slice, gamma) into a
-//    4-deep LDS ring with buffer loads to LDS, each a quarter of the loads (one
-//    wave alone issues global loads at about a third of a CU's rate).
+//    4-deep LDS ring with buffer loads to LDS, sharing the loads (one wave
+//    alone issues global loads at about a third of a CU's rate).  In the one-
+//    launch form wave 7 instead polls the chunk-terms flags a chunk ahead of
+//    the three others' copies.
 // Global loads use per-chunk buffer descriptors that end at row n-1 of the
 // head, so the rows of a partial chunk read as zeros.  K rows sit in LDS with
 // their 16-byte chunks XOR-swizzled by row, which keeps the transpose reads
@@ -676,8 +678,10 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 // Two barriers per chunk.  At A_c, S_c and R'_c are complete (exchange buffers
 // alternate by chunk parity) and every wave is done with chunk c-1, so the
 // loaders refill that slot; chunk c+1, read during chunk c, was waited for
-// before it.  B_c orders the chain waves' exchange of X_{c+1}.  Barriers order
-// LDS traffic only, so global loads and stores stay in flight across them.
+// before it.  B_c orders the chain waves' exchange of X_{c+1}; in the one-launch
+// form the output waves issue their loads and stores after it, the loaders
+// before it.  Barriers order LDS traffic only, so global loads and stores stay
+// in flight across them.
 // The chunk loop is unrolled by the ring depth so ring slots are constants.
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
