@@ -806,7 +806,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         // loaders wait on their own copies only): chunks 0..2 before barrier P,
         // chunk 3 before the first chunk, chunk c+4 during chunk c.  The loaders'
         // copies of a chunk follow its observation through the barriers.
-        int spins = 1 << 22;   // ~0.2 s of sleeping in all; the chunk-terms workgroups never wait
+        int spins = 1 << 22;   // one bound on the polls of the whole call (each a memory round trip and a short
+                               // sleep: seconds in all); the chunk-terms workgroups never wait, so it is not reached
         auto seen = [&](int c) {
             return __hip_atomic_load(&p.flags[slot(c)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == p.epoch;
         };
