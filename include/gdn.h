@@ -108,6 +108,31 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
                              void* stream);
 
 /*
+ * Segment-parallel prefill (section 3.2: the chunk map is affine in the state,
+ * S_{c+1}^T = M_c S_c^T + N_c, so a sequence's chunks can be grouped into
+ * segments whose maps compose).  Dense input can be cut at chunk boundaries
+ * into `segments` segments per sequence.  All segments' chains then run at once,
+ * twice: on the values from a zero state (segment 0: from S0), and on zero
+ * values from the identity, which gives each segment's transition and how the
+ * state entering it reaches its outputs.  A scan over the segments composes
+ * the entering states, and a last pass adds each segment's entering-state term
+ * to its outputs.  This pays off when the sequential chain would leave most
+ * compute units idle: few sequences times heads and many chunks.
+ *   segments = 0  automatic (the default): from the device's compute-unit count,
+ *                 B, H, dk, dv and T; the sequential form when splitting would
+ *                 not fill the device or leave segments shorter than 16 chunks
+ *   segments = 1  never split
+ *   segments > 1  that many segments (fewer when a sequence has fewer chunks)
+ * Ragged input is never split.  The setting is process-wide and read by both
+ * gdn_chunk_prefill_workspace_bytes (which sizes the automatic case for a
+ * 256-CU device) and gdn_chunk_prefill; a call whose workspace is too small for
+ * the split it would choose uses fewer segments, down to the sequential form.
+ * Results agree with the sequential form to rounding.  Returns the previous
+ * setting, or -1 (and changes nothing) when segments < 0 or segments > 64.
+ */
+int gdn_set_prefill_segments(int segments);
+
+/*
  * One decode step (the recurrence at T = 1; section 2.2, section 3.2): one
  * token for each of B sequences.
  *

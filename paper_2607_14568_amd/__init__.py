@@ -16,6 +16,7 @@ import torch
 __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
+    "gdn_set_prefill_segments",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -48,6 +49,8 @@ def lib():
         L.gdn_chunk_prefill_workspace_bytes.restype = S
         L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill.restype = I
+        L.gdn_set_prefill_segments.argtypes = [I]
+        L.gdn_set_prefill_segments.restype = I
         L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
         L.gdn_decode_step.restype = I
         _lib = L
@@ -69,6 +72,14 @@ def _check(status):
 
 def gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk=64, n_seqs=0, io_dtype=GDN_BF16) -> int:
     return int(lib().gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io_dtype))
+
+
+def gdn_set_prefill_segments(segments: int) -> int:
+    """Segments per sequence of the segment-parallel prefill (0 automatic, 1 never); returns the previous setting."""
+    prev = int(lib().gdn_set_prefill_segments(int(segments)))
+    if prev < 0:
+        raise ValueError("segments=%d out of range [0, 64]" % segments)
+    return prev
 
 
 def _dev(t, name, dtype=None):

@@ -32,6 +32,8 @@
 #include <string.h>
 #include <time.h>
 
+#include <type_traits>
+
 #include "gdn.h"
 
 namespace {
@@ -91,6 +93,7 @@ struct Params {
     const float* S0;
     void* o;
     float* ST;
+    int st_t;          // S_T stored transposed: [n, H, dk, DV] (key channel, then state row)
     int B, T, H, DV;
     int n_seq;         // dense: B; ragged: number of packed sequences
     int ragged;
@@ -413,14 +416,14 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 // ------------------------------------------------------------------ fp32 state chain
 // One workgroup per (sequence, head, 16-row slice of S); chunks in order.
 template <int DK>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
+__device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) {
     using IO = float;
     constexpr int PAD = 16 / sizeof(IO);
     constexpr int NMT = DK / 16;          // 16-row tiles of S^T
     const int H = p.H, DV = p.DV, nsl = DV / SL;
-    const int js = blockIdx.x % nsl;
-    const int h = (blockIdx.x / nsl) % H;
-    const int s = blockIdx.x / (nsl * H);
+    const int js = bid % nsl;
+    const int h = (bid / nsl) % H;
+    const int s = bid / (nsl * H);
 
     long start;
     int len, cbase;
@@ -492,7 +495,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
             x.t[j] = ld(rt, tid * 16 + NT * 16 * j);
             x.pp[j] = ld(rp, tid * 16 + NT * 16 * j);
         }
-        const auto rv = rs(reinterpret_cast<const IO*>(p.v) + (t0 * H + h) * DV, rb * DV * sizeof(IO));
+        // no value tensor reads as zeros (a descriptor of no bytes)
+        const auto rv = p.v ? rs(reinterpret_cast<const IO*>(p.v) + (t0 * H + h) * DV, rb * DV * sizeof(IO)) : rs(p.k, 0);
 #pragma unroll
         for (int j = 0; j < NVV; ++j)
             x.v[j] = tid + NT * j < CH * VPV ? ld(rv, vvo + (NT / VPV) * j * H * DV * (int)sizeof(IO)) : make_uint4(0, 0, 0, 0);
@@ -634,7 +638,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     }
     __syncthreads();
     if (p.ST)
-        for (int i = tid; i < SL * DK; i += NT) p.ST[srow0 + i] = sS[nc & 1][i / DK][i % DK];
+        for (int i = tid; i < SL * DK; i += NT) {
+            const long at = p.st_t ? srow0 - (long)js * SL * DK + (long)(i % DK) * DV + js * SL + i / DK : srow0 + i;
+            p.ST[at] = sS[nc & 1][i / DK][i % DK];
+        }
+}
+
+template <int DK>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
+    state_chain_f32<DK>(p, blockIdx.x);
 }
 
 // ------------------------------------------------------------------ bf16 state chain
@@ -798,6 +810,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         return rsrc(reinterpret_cast<const bf16_t*>(base) + (tok0(c) * H + h) * width,
                     (uint32_t)(((long)(rows(c) - 1) * H + 1) * width * 2));
     };
+    // values: no value tensor reads as zeros (a descriptor of no bytes)
+    auto vrsrc = [&](int c) { return p.v ? crsrc(p.v, DV, c) : rsrc(p.k, 0u); };
 
     if (FUSED && wave == 7) {
         // ------------------------------------------------ flag poller (one launch only)
@@ -852,7 +866,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             const auto rk = crsrc(p.k, DK, c);
 #pragma unroll
             for (int i = L; i < NCH; i += NL) bdma16(rk, &sK[sl][RPI * i * DK], koff[i / NL]);
-            if constexpr (L >= NL - 2) bdma16(crsrc(p.v, DV, c), &sV[sl][32 * (L == NL - 1) * SL], voff);
+            if constexpr (L >= NL - 2) bdma16(vrsrc(c), &sV[sl][32 * (L == NL - 1) * SL], voff);
         };
         auto issue_terms = [&](int c, auto SLOT, auto LI) {
             constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
@@ -1069,10 +1083,16 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 if (c + 2 < nc) cstep(Ic<2>{});
                 if (c + 3 < nc) cstep(Ic<3>{});
             }
-            if (p.ST) {
+            if (p.ST && !p.st_t) {
 #pragma unroll
                 for (int m = 0; m < HMD; ++m)
                     *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
+            } else if (p.ST) {
+                float* st = p.ST + srow0 - (long)js * SL * DK + js * SL + l16;
+#pragma unroll
+                for (int m = 0; m < HMD; ++m)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) st[(long)(chan(w * HMD + m) + e) * DV] = acc[m][e];
             }
         };
         if (wave == 0) chain(Ic<0>{});
@@ -1596,6 +1616,279 @@ __global__ __launch_bounds__(NT) void k_decode_step(const IO* __restrict__ q, co
     }
 }
 
+// ------------------------------------------------------------------ segment-parallel form
+// The chunk map of section 3.2 is affine in the state: S_{c+1}^T = M_c S_c^T + N_c.
+// With each sequence cut at chunk boundaries into P segments of L chunks, all
+// segments' chains run at once, twice, over the same chunk terms:
+//   run 1: the true values, from S0 for segment 0 and from zero for the others.
+//     It gives o for segment 0, for segment p the part o0 of o that leaves out
+//     the state entering it, and the segment's offset N_p (its final state);
+//   run 2: zero values from the identity (dk state rows).  Row i of its final
+//     state is row i of the segment's transition (S_end = S_start M_p + N_p in
+//     the S orientation), and its output Y_t[i] = (e_i M_{p,t}) (scale q_t) is
+//     what a unit state row i adds to o_t.
+// Rows of the state evolve independently of one another, so with X_p the state
+// entering segment p:
+//     X_1 = N_0,   X_{p+1} = X_p M_p + N_p,   o_t = o0_t + X_p Y_t  (t in segment p).
+// Segments are packed as the sequences of a ragged call, so the chains and the
+// chunk terms are the ragged kernels unchanged.
+struct SegParams {
+    int nseq, P, L, T, NC, H, DV, DK;   // sequences; segments per sequence; chunks per segment; tokens and chunks per sequence
+    int32_t* cu;         // [nseq P + 1] segment offsets into the nseq T packed tokens
+    const float* S0;     // [nseq, H, DV, DK] or null (zeros)
+    float* S0seg;        // [nseq P, H, DV, DK]: S0 for segment 0 of a sequence, zero for the others
+    float* Iseg;         // [nseq P, H, DK, DK]: identity
+    const float* N;      // run 1's final states [nseq P, H, DV, DK]
+    const float* M;      // run 2's final states, transposed [nseq P, H, DK, DK]
+    void* X;             // states entering each segment [nseq P, H, DV, DK], io (segment 0's unused)
+    float* ST;           // [nseq, H, DV, DK] or null
+    const void* Y;       // run 2's outputs [nseq T, H, DK] io
+    void* o;             // [nseq T, H, DV] io
+};
+
+// Segment table and the two runs' initial states: workgroup row y is segment
+// y (row nseq P only writes the table's end).
+template <int DK>
+__global__ __launch_bounds__(NT) void k_segment_prep(SegParams sp) {
+    const int seg = blockIdx.y, nseg = sp.nseq * sp.P;
+    const int i = blockIdx.x * NT + threadIdx.x;   // float4 within one segment's matrices
+    if (i == 0) {
+        const long off = (long)(seg % sp.P) * sp.L * CH;
+        sp.cu[seg] = (int32_t)((long)(seg / sp.P) * sp.T + (off < sp.T ? off : sp.T));
+    }
+    if (seg >= nseg) return;
+    const int mat4 = sp.H * sp.DV * (DK / 4), id4 = sp.H * DK * (DK / 4);
+    if (i < mat4) {
+        floatx4 x = {0.f, 0.f, 0.f, 0.f};
+        if (sp.S0 && seg % sp.P == 0) x = reinterpret_cast<const floatx4*>(sp.S0)[(long)(seg / sp.P) * mat4 + i];
+        reinterpret_cast<floatx4*>(sp.S0seg)[(long)seg * mat4 + i] = x;
+    }
+    if (i < id4) {
+        const int r = (i / (DK / 4)) % DK, c0 = (i % (DK / 4)) * 4;
+        floatx4 x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = c0 + e == r ? 1.f : 0.f;
+        reinterpret_cast<floatx4*>(sp.Iseg)[(long)seg * id4 + i] = x;
+    }
+}
+
+// The scan over segments: one workgroup per (sequence, head, 16 state rows);
+// rows of X never mix, so the workgroups are independent.  X (16 x DK, fp32)
+// sits in LDS; wave w forms column tile w of X M_p + N_p on MFMA (bf16
+// operands for bf16 io, fp32 for fp32 io) and writes X_p out in io precision
+// for the output pass.  M_p arrives transposed, so a lane's B fragment is one
+// contiguous run of a row of M_p^T.  M_p and N_p do not depend on X: a ring of R
+// register slots keeps the next R segments' fragments in flight, with the
+// segment loop unrolled by R so slots are never copied (a copy would wait for
+// its load), and the barriers order LDS only.
+template <typename IO, int DK>
+__global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
+    constexpr bool BF = sizeof(IO) == 2;
+    constexpr int NTH = DK * 4;   // DK / 16 waves
+    constexpr int NF = DK / 16;   // float4s of M_p^T per lane and segment
+    constexpr int R = 4;
+    __shared__ __attribute__((aligned(16))) float sX[2][SL][DK + 4];
+    const int H = sp.H, DV = sp.DV, nsl = DV / SL, P = sp.P;
+    const int js = blockIdx.x % nsl, h = (blockIdx.x / nsl) % H, b = blockIdx.x / (nsl * H);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int col = 16 * wave + l16;
+    const long mat = (long)DV * DK;
+    auto rows_at = [&](int seg) { return ((long)seg * H + h) * mat + (long)js * SL * DK; };
+    // contraction index of element e of lane group lg in step j: fp32: (DK/4) lg + 4 j + e;
+    // bf16 (steps of 8 = two float4s): 32 (j/2) + 8 lg + 4 (j%2) + e
+    auto koff = [&](int j) { return BF ? 32 * (j >> 1) + 8 * lg + 4 * (j & 1) : (DK / 4) * lg + 4 * j; };
+    floatx4 m[R][NF];
+    floatx4 nf[R];
+    {
+        const float* n0 = sp.N + rows_at(b * P);
+        for (int i = tid; i < SL * DK; i += NTH) sX[0][i / DK][i % DK] = n0[i];
+    }
+    // loads never branch (past the last segment they repeat it), so the
+    // compiler's wait counts stay exact across the unrolled loop
+    auto load = [&](int p, floatx4 (&mr)[NF], floatx4& n) {
+        p = min(p, P - 1);
+        const float* Mt = sp.M + ((long)(b * P + p) * H + h) * DK * DK + (long)col * DK;
+#pragma unroll
+        for (int j = 0; j < NF; ++j) mr[j] = *reinterpret_cast<const floatx4*>(Mt + koff(j));
+        const float* Np = sp.N + rows_at(b * P + p);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) n[e] = Np[(4 * lg + e) * DK + col];
+    };
+#pragma unroll
+    for (int d = 0; d < R; ++d) load(1 + d, m[d], nf[d]);
+    lds_barrier();
+    int cur = 0;
+    auto step = [&](int p, auto D) {
+        constexpr int d = decltype(D)::value;
+        {   // X_p out: one float4 per thread (a fixed count keeps the load counters exact)
+            static_assert(SL * DK == 4 * NTH, "one float4 of X per thread");
+            const int r = 4 * tid / DK, cc = 4 * tid % DK;
+            const floatx4 x = f4(&sX[cur][r][cc]);
+            IO* xo = reinterpret_cast<IO*>(sp.X) + rows_at(b * P + p) + 4 * tid;
+            if constexpr (BF) {
+                const uint2 u = {(uint32_t)from_f<bf16_t>(x[0]) | ((uint32_t)from_f<bf16_t>(x[1]) << 16),
+                                 (uint32_t)from_f<bf16_t>(x[2]) | ((uint32_t)from_f<bf16_t>(x[3]) << 16)};
+                *reinterpret_cast<uint2*>(xo) = u;
+            } else {
+                *reinterpret_cast<floatx4*>(xo) = x;
+            }
+        }
+        floatx4 acc = nf[d];
+        if constexpr (BF) {
+#pragma unroll
+            for (int kk = 0; kk < DK / 32; ++kk) {
+                const bf16x8 a = pack_bf16(f4(&sX[cur][l16][koff(2 * kk)]), f4(&sX[cur][l16][koff(2 * kk + 1)]));
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pack_bf16(m[d][2 * kk], m[d][2 * kk + 1]), acc, 0, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NF; ++j) {
+                const floatx4 a = f4(&sX[cur][l16][koff(j)]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], m[d][j][e], acc, 0, 0, 0);
+            }
+        }
+        // acc[e]: row 4 lg + e, column col of X_p M_p + N_p
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sX[cur ^ 1][4 * lg + e][col] = acc[e];
+        load(p + R, m[d], nf[d]);
+        lds_barrier();
+        cur ^= 1;
+    };
+    static_assert(R == 4, "the loop below is unrolled by 4");
+    int p0 = 1;
+    for (; p0 + R <= P; p0 += R) {
+        step(p0, Ic<0>{});
+        step(p0 + 1, Ic<1>{});
+        step(p0 + 2, Ic<2>{});
+        step(p0 + 3, Ic<3>{});
+    }
+    if (p0 < P) step(p0, Ic<0>{});
+    if (p0 + 1 < P) step(p0 + 1, Ic<1>{});
+    if (p0 + 2 < P) step(p0 + 2, Ic<2>{});
+    if (sp.ST) {
+        float* st = sp.ST + ((long)b * H + h) * mat + (long)js * SL * DK;
+        for (int i = tid; i < SL * DK; i += NTH) st[i] = sX[cur][i / DK][i % DK];
+    }
+}
+
+// o_t += X_p Y_t for the chunks of segments p >= 1: one workgroup of 8 waves
+// per (sequence, segment, pair of chunks, head), X_p (io precision) staged in
+// LDS.  Wave w takes tokens 16 (w%4)..+15 of the pair's chunk w/4 and forms
+// (X_p Y^T) tile by tile, so a lane ends up with 4 consecutive value channels
+// of one token.  Its Y fragments and the o values it updates are loaded
+// before the staging.
+constexpr int NT_CORR = 512;
+template <typename IO, int DK>
+__global__ __launch_bounds__(NT_CORR) void k_segment_correct(SegParams sp) {
+    constexpr bool BF = sizeof(IO) == 2;
+    constexpr int PADX = BF ? 8 : 4;
+    constexpr int DVM = 128;                     // largest value width
+    constexpr int NKB = BF ? DK / 32 : DK / 4;   // contraction steps
+    constexpr int VEC = 16 / sizeof(IO);         // elements per 16-byte load
+    __shared__ __attribute__((aligned(16))) IO sXp[DVM][DK + PADX];
+    const int H = sp.H, DV = sp.DV, npair = (sp.L + 1) / 2;
+    const int h = blockIdx.x % H;
+    const int q = (int)((blockIdx.x / H) % npair);
+    const int p = 1 + (int)((blockIdx.x / ((long)H * npair)) % (sp.P - 1));
+    const int b = (int)(blockIdx.x / ((long)H * npair * (sp.P - 1)));
+    const int seg = b * sp.P + p;
+    const int c_end = min((p + 1) * sp.L, sp.NC);   // one past the segment's last chunk
+    const int c0 = p * sp.L + 2 * q;
+    if (c0 >= c_end) return;                        // workgroup-uniform
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int c = c0 + wave / 4;
+    const long t_end = (long)b * sp.T + sp.T;       // one past the sequence's last token
+    const long t = (long)b * sp.T + (long)c * CH + 16 * (wave % 4) + l16;   // this lane's token
+    const bool live = c < c_end && t < t_end;
+    const long tb = live ? t : (long)b * sp.T;      // a valid row for the Y reads of idle lanes
+    const IO* y = reinterpret_cast<const IO*>(sp.Y) + (tb * H + h) * DK;
+    IO* o = reinterpret_cast<IO*>(sp.o) + (t * H + h) * DV + 4 * lg;
+    typedef typename std::conditional<BF, bf16x8, float>::type YF;
+    YF yb[NKB];
+#pragma unroll
+    for (int kk = 0; kk < NKB; ++kk) {
+        if constexpr (BF) yb[kk] = *reinterpret_cast<const bf16x8*>(y + 32 * kk + 8 * lg);
+        else yb[kk] = y[4 * kk + lg];
+    }
+    floatx4 ov[DVM / 16];
+#pragma unroll
+    for (int n = 0; n < DVM / 16; ++n) {
+        ov[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (live && n < DV / 16) {
+            if constexpr (BF) {
+                const uint2 u = *reinterpret_cast<const uint2*>(o + 16 * n);
+                ov[n] = floatx4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                                __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+            } else {
+                ov[n] = *reinterpret_cast<const floatx4*>(o + 16 * n);
+            }
+        }
+    }
+    const IO* xp = reinterpret_cast<const IO*>(sp.X) + ((long)seg * H + h) * DV * DK;
+#pragma unroll
+    for (int j = 0; j < DVM * DK / VEC / NT_CORR; ++j) {
+        const int i = tid + NT_CORR * j;
+        if (i < DV * DK / VEC) {
+            const int r = (VEC * i) / DK, cc = (VEC * i) % DK;
+            *reinterpret_cast<uint4*>(&sXp[r][cc]) = reinterpret_cast<const uint4*>(xp)[i];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int n = 0; n < DVM / 16; ++n) {
+        if (n >= DV / 16) break;
+        floatx4 acc = ov[n];
+#pragma unroll
+        for (int kk = 0; kk < NKB; ++kk) {
+            if constexpr (BF)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(&sXp[16 * n + l16][32 * kk + 8 * lg]), yb[kk], acc, 0, 0, 0);
+            else
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sXp[16 * n + l16][4 * kk + lg], yb[kk], acc, 0, 0, 0);
+        }
+        // acc[e]: value channel 16 n + 4 lg + e of this lane's token
+        if (live) {
+            if constexpr (BF) {
+                const uint2 u = {(uint32_t)from_f<bf16_t>(acc[0]) | ((uint32_t)from_f<bf16_t>(acc[1]) << 16),
+                                 (uint32_t)from_f<bf16_t>(acc[2]) | ((uint32_t)from_f<bf16_t>(acc[3]) << 16)};
+                *reinterpret_cast<uint2*>(o + 16 * n) = u;
+            } else {
+                *reinterpret_cast<floatx4*>(o + 16 * n) = acc;
+            }
+        }
+    }
+}
+
+// Paired chain launch: workgroups [0, first) run the problem in p, the rest the
+// same chunks with another value tensor, width, initial and final states and
+// output (the identity run of the segment-parallel form).
+struct ChainAlt {
+    const void* v;
+    const float* S0;
+    void* o;
+    float* ST;
+    int st_t;
+    int DV;
+    int first;
+};
+
+template <int DK>
+__global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_pair_bf16(Params p,
+                                                                                                         ChainAlt a) {
+    __shared__ ChainLds<DK> lds;
+    int bid = blockIdx.x;
+    if (bid >= a.first) { p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV; bid -= a.first; }
+    state_chain_bf16<DK, false>(p, bid, lds);
+}
+
+template <int DK>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain_pair(Params p, ChainAlt a) {
+    int bid = blockIdx.x;
+    if (bid >= a.first) { p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV; bid -= a.first; }
+    state_chain_f32<DK>(p, bid);
+}
+
 // ------------------------------------------------------------------ host side
 thread_local char g_err[512] = "";
 
@@ -1696,6 +1989,105 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         hipLaunchKernelGGL((k_state_chain<DK>), grid, dim3(NT), 0, st, p);
 }
 
+// ---- segment-parallel form: plan, workspace, launches
+constexpr int SEG_AUTO_MAX = 16;   // most segments per sequence chosen automatically
+constexpr int SEG_MAX = 64;        // most segments per sequence accepted
+constexpr int SEG_MIN_CHUNKS = 16; // fewest chunks per segment chosen automatically
+constexpr long PLAN_CUS = 256;     // compute units the workspace size assumes
+int g_segments = 0;                // 0: automatic, 1: never split, > 1: that many segments
+
+struct SegPlan {
+    int P = 1;   // segments per sequence (1: the sequential form)
+    int L = 0;   // chunks per segment
+};
+
+// Segments per sequence.  The chain walks a sequence's chunks one after another
+// on one workgroup per (sequence, head, 16 state rows), each holding a CU; when
+// those leave most CUs idle, P segments (each run twice) bring the chain's length
+// from NC to NC / P chunks for a scan over P states and one extra pass over o.
+// Ragged input keeps the sequential form.
+SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, long cus, int setting) {
+    SegPlan sp;
+    const int nc = (T + CH - 1) / CH;
+    if (n_seqs > 0 || nc < 2 || setting == 1) return sp;
+    int P;
+    if (setting > 1) {
+        P = setting;
+    } else {
+        const long per = (long)B * H * ((dv + dk) / SL);   // chain workgroups of one segment index
+        const long fit = cus / per;
+        P = (int)std::min<long>(std::min<long>(fit, SEG_AUTO_MAX), nc / SEG_MIN_CHUNKS);
+    }
+    P = std::min(P, nc);
+    if (P < 2) return sp;
+    sp.L = (nc + P - 1) / P;
+    sp.P = (nc + sp.L - 1) / sp.L;   // every segment non-empty
+    if (sp.P < 2) sp = SegPlan{};
+    return sp;
+}
+
+struct SegLayout {
+    Layout base;   // ragged layout over the nseq P segments
+    size_t cu, S0seg, Iseg, N, M, X, Y, total;
+};
+
+bool seg_layout(int B, int T, int H, int dk, int dv, int io, const SegPlan& sp, SegLayout* S) {
+    const long nseg = (long)B * sp.P;
+    if ((long)B * T >= (1L << 31) || nseg >= (1L << 30)) return false;
+    if (!ws_layout(1, B * T, H, dk, dv, (int)nseg, io, &S->base)) return false;
+    const size_t esz = io == GDN_BF16 ? 2 : 4;
+    const size_t sv = (size_t)nseg * H * dv * dk * sizeof(float), sk = (size_t)nseg * H * dk * dk * sizeof(float);
+    const size_t tk = (size_t)B * T * H * dk * esz;
+    size_t off = round_up(S->base.total, 256);
+    auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, 256); return at; };
+    S->cu = take((size_t)(nseg + 1) * sizeof(int32_t));
+    S->S0seg = take(sv);
+    S->Iseg = take(sk);
+    S->N = take(sv);
+    S->M = take(sk);
+    S->X = take(sv);
+    S->Y = take(tk);
+    S->total = off;
+    return true;
+}
+
+// Workspace bytes of the plan the setting and a device of `cus` CUs give
+// (the sequential form's when the plan does not split).
+size_t plan_bytes(int B, int T, int H, int dk, int dv, int n_seqs, int io, const SegPlan& sp) {
+    if (sp.P > 1) {
+        SegLayout S;
+        if (seg_layout(B, T, H, dk, dv, io, sp, &S)) return S.total;
+    }
+    Layout L;
+    return ws_layout(B, T, H, dk, dv, n_seqs, io, &L) ? L.total : 0;
+}
+
+template <typename IO, int DK>
+void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st) {
+    const long nseg = (long)sq.nseq * sq.P;
+    const long per_seg = (long)sq.H * std::max(sq.DV, DK) * DK / 4;   // float4s of one segment's initial states
+    hipLaunchKernelGGL((k_segment_prep<DK>), dim3((unsigned)((per_seg + NT - 1) / NT), (unsigned)(nseg + 1)), dim3(NT), 0,
+                       st, sq);
+    hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start, p.seq_len,
+                       p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
+    if constexpr (sizeof(IO) == 2)
+        hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+    else
+        hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+    ChainAlt a;
+    a.v = nullptr; a.S0 = sq.Iseg; a.st_t = 1; a.o = const_cast<void*>(sq.Y); a.ST = const_cast<float*>(sq.M); a.DV = DK;
+    a.first = (int)(nseg * p.H * (p.DV / SL));
+    const dim3 grid((unsigned)(a.first + nseg * p.H * (DK / SL)));
+    if constexpr (sizeof(IO) == 2)
+        hipLaunchKernelGGL((k_state_chain_pair_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p, a);
+    else
+        hipLaunchKernelGGL((k_state_chain_pair<DK>), grid, dim3(NT), 0, st, p, a);
+    hipLaunchKernelGGL((k_segment_scan<IO, DK>), dim3((unsigned)(sq.nseq * sq.H * (sq.DV / SL))), dim3(DK * 4), 0, st,
+                       sq);
+    hipLaunchKernelGGL((k_segment_correct<IO, DK>), dim3((unsigned)((long)sq.nseq * (sq.P - 1) * ((sq.L + 1) / 2) * sq.H)),
+                       dim3(NT_CORR), 0, st, sq);
+}
+
 template <typename IO, int DK>
 void launch_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
                    float* S, void* o, int B, int H, int dv, float scale, hipStream_t st) {
@@ -1736,7 +2128,13 @@ extern "C" size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk,
     if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return 0;
     Layout L;
     if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L)) return 0;
-    return L.total;
+    const SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, PLAN_CUS, __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    return std::max(L.total, plan_bytes(B, T, H, dk, dv, n_seqs, io_dtype, sp));
+}
+
+extern "C" int gdn_set_prefill_segments(int segments) {
+    if (segments < 0 || segments > SEG_MAX) return -1;
+    return __atomic_exchange_n(&g_segments, segments, __ATOMIC_RELAXED);
 }
 
 extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v, const float* g,
@@ -1778,7 +2176,7 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     if (workspace && !aligned(workspace, 256)) return fail(GDN_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
 
     Params p;
-    p.q = q; p.k = k; p.v = v; p.g = g; p.beta = beta; p.S0 = S0; p.o = o; p.ST = S_T;
+    p.q = q; p.k = k; p.v = v; p.g = g; p.beta = beta; p.S0 = S0; p.o = o; p.ST = S_T; p.st_t = 0;
     p.B = B; p.T = T; p.H = H; p.DV = dv;
     p.n_seq = n_seq;
     p.ragged = n_seqs > 0;
@@ -1803,6 +2201,52 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
+    // segment-parallel form when the plan splits and the workspace holds it
+    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, device_cus(), __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    SegLayout S;
+    while (sp.P > 1 && !(seg_layout(B, T, H, dk, dv, io_dtype, sp, &S) && S.total <= workspace_bytes &&
+                         (long)B * sp.P * H * ((dv + dk) / SL) < (1L << 31) && (long)B * p.NC * H < (1L << 31)))
+        sp = plan_segments(B, T, H, dk, dv, n_seqs, 0, sp.P - 1);
+    if (sp.P > 1) {
+        const int nseg = B * sp.P;
+        SegParams sq;
+        sq.nseq = B; sq.P = sp.P; sq.L = sp.L; sq.T = T; sq.NC = p.NC; sq.H = H; sq.DV = dv; sq.DK = dk;
+        sq.cu = reinterpret_cast<int32_t*>(ws + S.cu);
+        sq.S0 = S0;
+        sq.S0seg = reinterpret_cast<float*>(ws + S.S0seg);
+        sq.Iseg = reinterpret_cast<float*>(ws + S.Iseg);
+        sq.N = reinterpret_cast<float*>(ws + S.N);
+        sq.M = reinterpret_cast<float*>(ws + S.M);
+        sq.X = ws + S.X;
+        sq.ST = S_T;
+        sq.Y = ws + S.Y;
+        sq.o = o;
+        // run 1 as a ragged call over the segments
+        Params r = p;
+        r.B = 1; r.T = B * T; r.n_seq = nseg; r.ragged = 1;
+        r.cpt = (r.T + CH - 1) / CH; r.NC = r.cpt;
+        r.cu = sq.cu;
+        r.S0 = sq.S0seg; r.ST = const_cast<float*>(sq.N);
+        r.seq_start = reinterpret_cast<int32_t*>(ws);
+        r.seq_len = r.seq_start + (nseg + 1);
+        r.chunk_off = r.seq_len + (nseg + 1);
+        r.seq_perm = r.chunk_off + (nseg + 1);
+        r.cprefix = r.seq_perm + (nseg + 1);
+        r.wsG = reinterpret_cast<float*>(ws + S.base.G);
+        r.wsT = ws + S.base.T;
+        r.wsP = ws + S.base.P;
+        r.flags = reinterpret_cast<uint64_t*>(ws + S.base.F);
+        if (io_dtype == GDN_BF16) {
+            if (dk == 128) launch_segmented<bf16_t, 128>(r, sq, S.base.slots, hs);
+            else launch_segmented<bf16_t, 64>(r, sq, S.base.slots, hs);
+        } else {
+            if (dk == 128) launch_segmented<float, 128>(r, sq, S.base.slots, hs);
+            else launch_segmented<float, 64>(r, sq, S.base.slots, hs);
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+        return GDN_OK;
+    }
     if (io_dtype == GDN_BF16) {
         if (dk == 128) launch_prefill<bf16_t, 128>(p, L.slots, hs);
         else launch_prefill<bf16_t, 64>(p, L.slots, hs);

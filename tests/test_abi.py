@@ -59,6 +59,46 @@ def test_workspace_bytes():
         assert ws(*bad) == 0, bad
 
 
+def test_segment_setting_and_workspace():
+    """gdn_set_prefill_segments: range, previous value, and the workspace it implies
+    (pure host arithmetic; the automatic plan assumes a 256-CU device)."""
+    ws = gdn.gdn_chunk_prefill_workspace_bytes
+    set_ = gdn.gdn_set_prefill_segments
+    prev = set_(0)
+    try:
+        assert set_(0) == 0
+        with pytest.raises(ValueError):
+            set_(-1)
+        with pytest.raises(ValueError):
+            set_(65)
+        assert set_(1) == 0 and set_(0) == 1
+        bf = gdn.GDN_BF16
+        auto = {H: ws(1, 10240, H, 128, 128, 64, 0, bf) for H in (2, 4, 8, 16)}
+        set_(1)
+        seq = {H: ws(1, 10240, H, 128, 128, 64, 0, bf) for H in (2, 4, 8, 16)}
+        set_(0)
+        # few heads split (the chain would leave most of 256 CUs idle); H = 16 does not
+        for H in (2, 4, 8):
+            assert auto[H] > seq[H], H
+        assert auto[16] == seq[16]
+        # short prompts never split automatically (segments of at least 16 chunks)
+        set_(1)
+        short_seq = ws(1, 1000, 2, 128, 128, 64, 0, bf)
+        set_(0)
+        assert ws(1, 1000, 2, 128, 128, 64, 0, bf) == short_seq
+        # forced: more segments, more workspace; ragged input never splits
+        set_(2)
+        two = ws(1, 4096, 2, 128, 128, 64, 0, bf)
+        rag2 = ws(1, 4096, 2, 128, 128, 64, 3, bf)
+        set_(8)
+        assert ws(1, 4096, 2, 128, 128, 64, 0, bf) > two
+        assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
+        set_(1)
+        assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
+    finally:
+        set_(prev)
+
+
 def _prefill(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=2, dk=64, dv=64, chunk=64,
              cu=None, n_seqs=0, io=0, scale=1.0, ws=A, ws_bytes=1 << 40, stream=None)
