@@ -118,9 +118,10 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
  * the entering states, and a last pass adds each segment's entering-state term
  * to its outputs.  This pays off when the sequential chain would leave most
  * compute units idle: few sequences times heads and many chunks.
- *   segments = 0  automatic (the default): from the device's compute-unit count,
- *                 B, H, dk, dv and T; the sequential form when splitting would
- *                 not fill the device or leave segments shorter than 16 chunks
+ *   segments = 0  automatic (the default): the count (up to 16) that a time model
+ *                 of both forms, fitted on MI355X, gives for the device's
+ *                 compute-unit count, B, H, dk, dv, T and io_dtype; the sequential
+ *                 form unless splitting wins by 10 %
  *   segments = 1  never split
  *   segments > 1  that many segments (fewer when a sequence has fewer chunks)
  * Ragged input is never split.  The setting is process-wide and read by both

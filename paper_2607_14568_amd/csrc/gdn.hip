@@ -93,7 +93,8 @@ struct Params {
     const float* S0;
     void* o;
     float* ST;
-    int st_t;          // S_T stored transposed: [n, H, dk, DV] (key channel, then state row)
+    int st_t;          // S_T layout: 0 as declared; 1 transposed, [n, H, dk, DV] (key channel, then
+                       // state row); 2 transposed in bf16 (the bf16 chain's identity run)
     int B, T, H, DV;
     int n_seq;         // dense: B; ragged: number of packed sequences
     int ragged;
@@ -766,7 +767,9 @@ template <int DK> struct ChainLds {
 // Chain workgroup `bid`.  FUSED: the chunk terms come from workgroups of the
 // same launch; a chunk's terms are read only once its flag carries this call's
 // epoch, with loads that bypass the caches (their writers store the same way).
-template <int DK, bool FUSED>
+// IDENT: the identity run of the segment-parallel form -- values read as zeros
+// and S_T stored transposed in bf16 (layout 2 of Params::st_t).
+template <int DK, bool FUSED, bool IDENT = false>
 __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid, ChainLds<DK>& lds) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
     constexpr int HKD = NKD / 2;        // ... whose S^T rows one chain wave keeps
@@ -810,8 +813,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         return rsrc(reinterpret_cast<const bf16_t*>(base) + (tok0(c) * H + h) * width,
                     (uint32_t)(((long)(rows(c) - 1) * H + 1) * width * 2));
     };
-    // values: no value tensor reads as zeros (a descriptor of no bytes)
-    auto vrsrc = [&](int c) { return p.v ? crsrc(p.v, DV, c) : rsrc(p.k, 0u); };
+    // values; the identity run's read as zeros (a descriptor of no bytes)
+    auto vrsrc = [&](int c) { return IDENT ? rsrc(p.k, 0u) : crsrc(p.v, DV, c); };
 
     if (FUSED && wave == 7) {
         // ------------------------------------------------ flag poller (one launch only)
@@ -1083,16 +1086,16 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 if (c + 2 < nc) cstep(Ic<2>{});
                 if (c + 3 < nc) cstep(Ic<3>{});
             }
-            if (p.ST && !p.st_t) {
+            if constexpr (IDENT) {
+                bf16_t* st = reinterpret_cast<bf16_t*>(p.ST) + srow0 - (long)js * SL * DK + js * SL + l16;
+#pragma unroll
+                for (int m = 0; m < HMD; ++m)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) st[(long)(chan(w * HMD + m) + e) * DV] = from_f<bf16_t>(acc[m][e]);
+            } else if (p.ST) {
 #pragma unroll
                 for (int m = 0; m < HMD; ++m)
                     *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
-            } else if (p.ST) {
-                float* st = p.ST + srow0 - (long)js * SL * DK + js * SL + l16;
-#pragma unroll
-                for (int m = 0; m < HMD; ++m)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) st[(long)(chan(w * HMD + m) + e) * DV] = acc[m][e];
             }
         };
         if (wave == 0) chain(Ic<0>{});
@@ -1639,7 +1642,7 @@ struct SegParams {
     float* S0seg;        // [nseq P, H, DV, DK]: S0 for segment 0 of a sequence, zero for the others
     float* Iseg;         // [nseq P, H, DK, DK]: identity
     const float* N;      // run 1's final states [nseq P, H, DV, DK]
-    const float* M;      // run 2's final states, transposed [nseq P, H, DK, DK]
+    const float* M;      // run 2's final states, transposed [nseq P, H, DK, DK] (bf16 for bf16 io)
     void* X;             // states entering each segment [nseq P, H, DV, DK], io (segment 0's unused)
     float* ST;           // [nseq, H, DV, DK] or null
     const void* Y;       // run 2's outputs [nseq T, H, DK] io
@@ -1685,11 +1688,18 @@ template <typename IO, int DK>
 __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
     constexpr bool BF = sizeof(IO) == 2;
     constexpr int NTH = DK * 4;   // DK / 16 waves
-    constexpr int NF = DK / 16;   // float4s of M_p^T per lane and segment
+    constexpr int NF = DK / 16;   // 16-byte loads of M_p^T per lane and segment (bf16: DK / 32)
     constexpr int R = 4;
     __shared__ __attribute__((aligned(16))) float sX[2][SL][DK + 4];
     const int H = sp.H, DV = sp.DV, nsl = DV / SL, P = sp.P;
-    const int js = blockIdx.x % nsl, h = (blockIdx.x / nsl) % H, b = blockIdx.x / (nsl * H);
+    // Dispatch deals workgroups to the 8 XCDs round-robin: workgroup w runs on
+    // XCD w % 8.  All slices of one (sequence, head) go to one XCD, so its L2
+    // serves the M_p and N_p that every slice reads; the grid is padded to
+    // whole XCD rounds and the spare workgroups exit.
+    const int xcd = blockIdx.x % 8, k = blockIdx.x / 8;
+    const int unit = (k / nsl) * 8 + xcd, js = k % nsl;
+    if (unit >= sp.nseq * H) return;
+    const int h = unit % H, b = unit / H;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
     const int col = 16 * wave + l16;
     const long mat = (long)DV * DK;
@@ -1697,7 +1707,9 @@ __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
     // contraction index of element e of lane group lg in step j: fp32: (DK/4) lg + 4 j + e;
     // bf16 (steps of 8 = two float4s): 32 (j/2) + 8 lg + 4 (j%2) + e
     auto koff = [&](int j) { return BF ? 32 * (j >> 1) + 8 * lg + 4 * (j & 1) : (DK / 4) * lg + 4 * j; };
-    floatx4 m[R][NF];
+    typedef typename std::conditional<BF, bf16x8, floatx4>::type MF;
+    constexpr int NM = BF ? DK / 32 : NF;
+    MF m[R][NM];
     floatx4 nf[R];
     {
         const float* n0 = sp.N + rows_at(b * P);
@@ -1705,11 +1717,18 @@ __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
     }
     // loads never branch (past the last segment they repeat it), so the
     // compiler's wait counts stay exact across the unrolled loop
-    auto load = [&](int p, floatx4 (&mr)[NF], floatx4& n) {
+    auto load = [&](int p, MF (&mr)[NM], floatx4& n) {
         p = min(p, P - 1);
-        const float* Mt = sp.M + ((long)(b * P + p) * H + h) * DK * DK + (long)col * DK;
+        const long mt = ((long)(b * P + p) * H + h) * DK * DK + (long)col * DK;   // row col of M_p^T
+        if constexpr (BF) {
+            const bf16_t* Mt = reinterpret_cast<const bf16_t*>(sp.M) + mt;
 #pragma unroll
-        for (int j = 0; j < NF; ++j) mr[j] = *reinterpret_cast<const floatx4*>(Mt + koff(j));
+            for (int kk = 0; kk < NM; ++kk) mr[kk] = *reinterpret_cast<const bf16x8*>(Mt + koff(2 * kk));
+        } else {
+            const float* Mt = sp.M + mt;
+#pragma unroll
+            for (int j = 0; j < NF; ++j) mr[j] = *reinterpret_cast<const floatx4*>(Mt + koff(j));
+        }
         const float* Np = sp.N + rows_at(b * P + p);
 #pragma unroll
         for (int e = 0; e < 4; ++e) n[e] = Np[(4 * lg + e) * DK + col];
@@ -1738,7 +1757,7 @@ __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
 #pragma unroll
             for (int kk = 0; kk < DK / 32; ++kk) {
                 const bf16x8 a = pack_bf16(f4(&sX[cur][l16][koff(2 * kk)]), f4(&sX[cur][l16][koff(2 * kk + 1)]));
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pack_bf16(m[d][2 * kk], m[d][2 * kk + 1]), acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, m[d][kk], acc, 0, 0, 0);
             }
         } else {
 #pragma unroll
@@ -1773,7 +1792,7 @@ __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
 }
 
 // o_t += X_p Y_t for the chunks of segments p >= 1: one workgroup of 8 waves
-// per (sequence, segment, pair of chunks, head), X_p (io precision) staged in
+// per (sequence, segment, head, pair of chunks), X_p (io precision) staged in
 // LDS.  Wave w takes tokens 16 (w%4)..+15 of the pair's chunk w/4 and forms
 // (X_p Y^T) tile by tile, so a lane ends up with 4 consecutive value channels
 // of one token.  Its Y fragments and the o values it updates are loaded
@@ -1788,10 +1807,15 @@ __global__ __launch_bounds__(NT_CORR) void k_segment_correct(SegParams sp) {
     constexpr int VEC = 16 / sizeof(IO);         // elements per 16-byte load
     __shared__ __attribute__((aligned(16))) IO sXp[DVM][DK + PADX];
     const int H = sp.H, DV = sp.DV, npair = (sp.L + 1) / 2;
-    const int h = blockIdx.x % H;
-    const int q = (int)((blockIdx.x / H) % npair);
-    const int p = 1 + (int)((blockIdx.x / ((long)H * npair)) % (sp.P - 1));
-    const int b = (int)(blockIdx.x / ((long)H * npair * (sp.P - 1)));
+    // all workgroups of one (sequence, segment, head) on one XCD (workgroup w runs
+    // on XCD w % 8), whose L2 then serves their reads of X_p; spare ones exit
+    const int xcd = blockIdx.x % 8, k = blockIdx.x / 8;
+    const long unit = (long)(k / npair) * 8 + xcd;
+    if (unit >= (long)sp.nseq * (sp.P - 1) * H) return;
+    const int q = k % npair;
+    const int h = (int)(unit % H);
+    const int p = 1 + (int)((unit / H) % (sp.P - 1));
+    const int b = (int)(unit / ((long)H * (sp.P - 1)));
     const int seg = b * sp.P + p;
     const int c_end = min((p + 1) * sp.L, sp.NC);   // one past the segment's last chunk
     const int c0 = p * sp.L + 2 * q;
@@ -1877,9 +1901,13 @@ template <int DK>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_pair_bf16(Params p,
                                                                                                          ChainAlt a) {
     __shared__ ChainLds<DK> lds;
-    int bid = blockIdx.x;
-    if (bid >= a.first) { p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV; bid -= a.first; }
-    state_chain_bf16<DK, false>(p, bid, lds);
+    const int bid = blockIdx.x;
+    if (bid >= a.first) {
+        p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV;
+        state_chain_bf16<DK, false, true>(p, bid - a.first, lds);
+    } else {
+        state_chain_bf16<DK, false>(p, bid, lds);
+    }
 }
 
 template <int DK>
@@ -1992,7 +2020,6 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
 // ---- segment-parallel form: plan, workspace, launches
 constexpr int SEG_AUTO_MAX = 16;   // most segments per sequence chosen automatically
 constexpr int SEG_MAX = 64;        // most segments per sequence accepted
-constexpr int SEG_MIN_CHUNKS = 16; // fewest chunks per segment chosen automatically
 constexpr long PLAN_CUS = 256;     // compute units the workspace size assumes
 int g_segments = 0;                // 0: automatic, 1: never split, > 1: that many segments
 
@@ -2001,28 +2028,45 @@ struct SegPlan {
     int L = 0;   // chunks per segment
 };
 
-// Segments per sequence.  The chain walks a sequence's chunks one after another
-// on one workgroup per (sequence, head, 16 state rows), each holding a CU; when
-// those leave most CUs idle, P segments (each run twice) bring the chain's length
-// from NC to NC / P chunks for a scan over P states and one extra pass over o.
-// Ragged input keeps the sequential form.
-SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, long cus, int setting) {
+// Time model of both forms (microseconds), fitted to timings at dk = dv = 128 on
+// a 256-CU MI355X.  The sequential form costs a fixed start and one chain step per
+// chunk.  The segmented form costs a fixed part (its launches, the chunk terms'
+// start), a part per token and head (chunk terms, the output pass), one chain
+// step per chunk of a segment and one scan step per segment.  A chain that needs
+// more workgroups than CUs (one per CU: its LDS) runs in rounds.
+struct SegCost {
+    double seq_fixed, chunk, seg_fixed, per_token_head, per_segment;
+};
+constexpr SegCost COST_BF16 = {17.0, 0.73, 33.3, 3.6e-4, 1.4};
+constexpr SegCost COST_F32 = {12.0, 4.2, 40.0, 1.7e-3, 2.6};
+
+// Segments per sequence.  Ragged input keeps the sequential form.
+SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io, long cus, int setting) {
     SegPlan sp;
     const int nc = (T + CH - 1) / CH;
     if (n_seqs > 0 || nc < 2 || setting == 1) return sp;
-    int P;
+    auto split = [&](int P) {
+        SegPlan x;
+        x.L = (nc + P - 1) / P;
+        x.P = (nc + x.L - 1) / x.L;   // every segment non-empty
+        return x;
+    };
     if (setting > 1) {
-        P = setting;
-    } else {
-        const long per = (long)B * H * ((dv + dk) / SL);   // chain workgroups of one segment index
-        const long fit = cus / per;
-        P = (int)std::min<long>(std::min<long>(fit, SEG_AUTO_MAX), nc / SEG_MIN_CHUNKS);
+        const SegPlan x = split(std::min(setting, nc));
+        return x.P > 1 ? x : sp;
     }
-    P = std::min(P, nc);
-    if (P < 2) return sp;
-    sp.L = (nc + P - 1) / P;
-    sp.P = (nc + sp.L - 1) / sp.L;   // every segment non-empty
-    if (sp.P < 2) sp = SegPlan{};
+    if (cus <= 0) return sp;
+    const SegCost& k = io == GDN_BF16 ? COST_BF16 : COST_F32;
+    auto rounds = [&](long wgs) { return (double)((wgs + cus - 1) / cus); };
+    const double t_seq = k.seq_fixed + k.chunk * nc * rounds((long)B * H * (dv / SL));
+    double best = 0.9 * t_seq;   // splitting must win by a margin
+    for (int P = 2; P <= std::min(SEG_AUTO_MAX, nc); ++P) {
+        const SegPlan x = split(P);
+        if (x.P != P) continue;
+        const double t = k.seg_fixed + k.per_token_head * B * H * (double)T +
+                         k.chunk * x.L * rounds((long)B * P * H * ((dv + dk) / SL)) + k.per_segment * P;
+        if (t < best) { best = t; sp = x; }
+    }
     return sp;
 }
 
@@ -2075,16 +2119,18 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
     else
         hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     ChainAlt a;
-    a.v = nullptr; a.S0 = sq.Iseg; a.st_t = 1; a.o = const_cast<void*>(sq.Y); a.ST = const_cast<float*>(sq.M); a.DV = DK;
+    a.v = nullptr; a.S0 = sq.Iseg; a.st_t = sizeof(IO) == 2 ? 2 : 1; a.o = const_cast<void*>(sq.Y); a.ST = const_cast<float*>(sq.M); a.DV = DK;
     a.first = (int)(nseg * p.H * (p.DV / SL));
     const dim3 grid((unsigned)(a.first + nseg * p.H * (DK / SL)));
     if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_state_chain_pair_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p, a);
     else
         hipLaunchKernelGGL((k_state_chain_pair<DK>), grid, dim3(NT), 0, st, p, a);
-    hipLaunchKernelGGL((k_segment_scan<IO, DK>), dim3((unsigned)(sq.nseq * sq.H * (sq.DV / SL))), dim3(DK * 4), 0, st,
-                       sq);
-    hipLaunchKernelGGL((k_segment_correct<IO, DK>), dim3((unsigned)((long)sq.nseq * (sq.P - 1) * ((sq.L + 1) / 2) * sq.H)),
+    const long units = (long)sq.nseq * sq.H;   // (sequence, head) pairs, each on one XCD
+    hipLaunchKernelGGL((k_segment_scan<IO, DK>), dim3((unsigned)(8 * ((units + 7) / 8) * (sq.DV / SL))), dim3(DK * 4), 0,
+                       st, sq);
+    const long cunits = (long)sq.nseq * (sq.P - 1) * sq.H;   // (sequence, segment, head) triples, each on one XCD
+    hipLaunchKernelGGL((k_segment_correct<IO, DK>), dim3((unsigned)(8 * ((cunits + 7) / 8) * ((sq.L + 1) / 2))),
                        dim3(NT_CORR), 0, st, sq);
 }
 
@@ -2128,7 +2174,8 @@ extern "C" size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk,
     if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return 0;
     Layout L;
     if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L)) return 0;
-    const SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, PLAN_CUS, __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    const SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, PLAN_CUS,
+                                     __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
     return std::max(L.total, plan_bytes(B, T, H, dk, dv, n_seqs, io_dtype, sp));
 }
 
@@ -2202,11 +2249,12 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     // segment-parallel form when the plan splits and the workspace holds it
-    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, device_cus(), __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, device_cus(),
+                               __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
     SegLayout S;
     while (sp.P > 1 && !(seg_layout(B, T, H, dk, dv, io_dtype, sp, &S) && S.total <= workspace_bytes &&
                          (long)B * sp.P * H * ((dv + dk) / SL) < (1L << 31) && (long)B * p.NC * H < (1L << 31)))
-        sp = plan_segments(B, T, H, dk, dv, n_seqs, 0, sp.P - 1);
+        sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, 0, sp.P - 1);
     if (sp.P > 1) {
         const int nseg = B * sp.P;
         SegParams sq;

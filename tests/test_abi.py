@@ -72,20 +72,22 @@ def test_segment_setting_and_workspace():
         with pytest.raises(ValueError):
             set_(65)
         assert set_(1) == 0 and set_(0) == 1
-        bf = gdn.GDN_BF16
-        auto = {H: ws(1, 10240, H, 128, 128, 64, 0, bf) for H in (2, 4, 8, 16)}
+        bf, f32 = gdn.GDN_BF16, gdn.GDN_F32
+        auto = {(io, H): ws(1, 10240, H, 128, 128, 64, 0, io) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
         set_(1)
-        seq = {H: ws(1, 10240, H, 128, 128, 64, 0, bf) for H in (2, 4, 8, 16)}
+        seq = {(io, H): ws(1, 10240, H, 128, 128, 64, 0, io) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
         set_(0)
         # few heads split (the chain would leave most of 256 CUs idle); H = 16 does not
-        for H in (2, 4, 8):
-            assert auto[H] > seq[H], H
-        assert auto[16] == seq[16]
-        # short prompts never split automatically (segments of at least 16 chunks)
+        # (two runs of every segment would not fit beside each other)
+        for key in [(bf, 1), (bf, 2), (bf, 4), (f32, 1), (f32, 2), (f32, 4), (f32, 8)]:
+            assert auto[key] > seq[key], key
+        for key in [(bf, 16), (f32, 16)]:
+            assert auto[key] == seq[key], key
+        # short bf16 prompts stay sequential (the split's fixed costs outweigh its gain)
         set_(1)
-        short_seq = ws(1, 1000, 2, 128, 128, 64, 0, bf)
+        short_seq = ws(1, 2048, 2, 128, 128, 64, 0, bf)
         set_(0)
-        assert ws(1, 1000, 2, 128, 128, 64, 0, bf) == short_seq
+        assert ws(1, 2048, 2, 128, 128, 64, 0, bf) == short_seq
         # forced: more segments, more workspace; ragged input never splits
         set_(2)
         two = ws(1, 4096, 2, 128, 128, 64, 0, bf)
