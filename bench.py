@@ -105,6 +105,8 @@ def main():
     ap.add_argument("--sets", type=int, default=4, help="rotating resident input sets")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--segments", type=int, default=0,
+                    help="segments per sequence of the prefill (0 automatic, 1 sequential)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of MIB MiB before timing (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -123,6 +125,7 @@ def main():
     w = I.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    gdn.gdn_set_prefill_segments(args.segments)
     stream = torch.cuda.current_stream(dev)
 
     x_host = I.make_workload(args.workload)
@@ -151,6 +154,8 @@ def main():
         need = gdn.gdn_chunk_prefill_workspace_bytes(x_host["q"].shape[0], x_host["q"].shape[1], w.H, w.dk,
                                                      w.dv, 64, n_seqs, io_code)
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        segments = gdn.gdn_chunk_prefill_segments(x_host["q"].shape[0], x_host["q"].shape[1], w.H, w.dk, w.dv,
+                                                  n_seqs, io_code)
         for d in sets:
             d["o"] = torch.empty_like(d["v"])
             d["S_T"] = torch.empty_like(d["S0"]) if d["S0"] is not None else None
@@ -197,8 +202,13 @@ def main():
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = None if w.decode else measured_traffic(w.name)
-    roof["kernel"] = "one gdn_decode_step call" if w.decode else \
-        "one gdn_chunk_prefill call (k_prefill_fused_bf16 for bf16 io)"
+    if w.decode:
+        roof["kernel"] = "one gdn_decode_step call"
+    elif segments > 1:
+        roof["kernel"] = ("one gdn_chunk_prefill call, segment-parallel form with %d segments (segment "
+                          "setup, chunk terms, paired chain, scan, output pass)" % segments)
+    else:
+        roof["kernel"] = "one gdn_chunk_prefill call (k_prefill_fused_bf16 for bf16 io)"
     roof["alg_bytes"] = byts
     roof["alg_flops"] = flops
     roof["avg_call_us"] = avg_call_s * 1e6

@@ -134,6 +134,15 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
 int gdn_set_prefill_segments(int segments);
 
 /*
+ * Segments per sequence that gdn_chunk_prefill would use for these sizes on the
+ * current device under the current setting, given a workspace of
+ * gdn_chunk_prefill_workspace_bytes(...) bytes: 1 for the sequential form, 0 for
+ * arguments gdn_chunk_prefill would reject.  Queries the device's compute-unit
+ * count (a HIP call); enqueues nothing.
+ */
+int gdn_chunk_prefill_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype);
+
+/*
  * One decode step (the recurrence at T = 1; section 2.2, section 3.2): one
  * token for each of B sequences.
  *

@@ -16,7 +16,7 @@ import torch
 __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
-    "gdn_set_prefill_segments",
+    "gdn_set_prefill_segments", "gdn_chunk_prefill_segments",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -49,6 +49,8 @@ def lib():
         L.gdn_chunk_prefill_workspace_bytes.restype = S
         L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill.restype = I
+        L.gdn_chunk_prefill_segments.argtypes = [I] * 7
+        L.gdn_chunk_prefill_segments.restype = I
         L.gdn_set_prefill_segments.argtypes = [I]
         L.gdn_set_prefill_segments.restype = I
         L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
@@ -80,6 +82,11 @@ def gdn_set_prefill_segments(segments: int) -> int:
     if prev < 0:
         raise ValueError("segments=%d out of range [0, 64]" % segments)
     return prev
+
+
+def gdn_chunk_prefill_segments(B, T, H, dk, dv, n_seqs=0, io_dtype=GDN_BF16) -> int:
+    """Segments per sequence a prefill of these sizes would use on the current device (1: sequential)."""
+    return int(lib().gdn_chunk_prefill_segments(B, T, H, dk, dv, n_seqs, io_dtype))
 
 
 def _dev(t, name, dtype=None):

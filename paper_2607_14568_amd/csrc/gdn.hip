@@ -21,6 +21,12 @@
 // contractions on MFMA (bf16 operands with fp32 accumulation for bf16 io, fp32
 // MFMA for fp32 io) and the state kept in fp32.
 //
+// When the chain alone would leave most compute units idle (few sequences and
+// heads, many chunks), dense input takes the segment-parallel form: the
+// sequence is cut into segments whose chains run at once, and the affine chunk
+// map composes them (k_segment_prep, k_state_chain_pair*, k_segment_scan,
+// k_segment_correct).
+//
 // Decode (k_decode_step) is the recurrence at T = 1: one pass over the state,
 // row by row (rows of S never mix).
 #include <hip/hip_runtime.h>
@@ -1620,24 +1626,30 @@ __global__ __launch_bounds__(NT) void k_decode_step(const IO* __restrict__ q, co
 }
 
 // ------------------------------------------------------------------ segment-parallel form
-// The chunk map of section 3.2 is affine in the state: S_{c+1}^T = M_c S_c^T + N_c.
-// With each sequence cut at chunk boundaries into P segments of L chunks, all
-// segments' chains run at once, twice, over the same chunk terms:
+// The chunk map of section 3.2 is affine in the state: S_{c+1}^T = M_c S_c^T + N_c,
+// so a run of chunks composes to S_end = S_start M_p + N_p (S orientation; M_p is
+// the product of the chunks' M_c, transposed, and N_p what the run leaves from a
+// zero state).  With each sequence cut at chunk boundaries into P segments of L
+// chunks, all segments' chains run at once, twice, over the same chunk terms:
 //   run 1: the true values, from S0 for segment 0 and from zero for the others.
 //     It gives o for segment 0, for segment p the part o0 of o that leaves out
-//     the state entering it, and the segment's offset N_p (its final state);
+//     the state entering it, and the segment's N_p (its final state);
 //   run 2: zero values from the identity (dk state rows).  Row i of its final
-//     state is row i of the segment's transition (S_end = S_start M_p + N_p in
-//     the S orientation), and its output Y_t[i] = (e_i M_{p,t}) (scale q_t) is
-//     what a unit state row i adds to o_t.
+//     state is row i of M_p, and its output Y_t[i] = (e_i M_{p,t}) (scale q_t),
+//     with M_{p,t} the map from the segment's start to token t, is what a unit
+//     state row i adds to o_t.
 // Rows of the state evolve independently of one another, so with X_p the state
 // entering segment p:
 //     X_1 = N_0,   X_{p+1} = X_p M_p + N_p,   o_t = o0_t + X_p Y_t  (t in segment p).
 // Segments are packed as the sequences of a ragged call, so the chains and the
-// chunk terms are the ragged kernels unchanged.
+// chunk terms are the ragged kernels unchanged; the sequence table of that
+// call has a closed form and is written directly.
 struct SegParams {
     int nseq, P, L, T, NC, H, DV, DK;   // sequences; segments per sequence; chunks per segment; tokens and chunks per sequence
-    int32_t* cu;         // [nseq P + 1] segment offsets into the nseq T packed tokens
+    int32_t* seq_start;  // the ragged call's sequence table over the nseq P segments (see Params):
+    int32_t* seq_len;    //   token start and length, first chunk slot ([nseq P + 1]) and the
+    int32_t* chunk_off;  //   chains' order
+    int32_t* seq_perm;
     const float* S0;     // [nseq, H, DV, DK] or null (zeros)
     float* S0seg;        // [nseq P, H, DV, DK]: S0 for segment 0 of a sequence, zero for the others
     float* Iseg;         // [nseq P, H, DK, DK]: identity
@@ -1655,9 +1667,15 @@ template <int DK>
 __global__ __launch_bounds__(NT) void k_segment_prep(SegParams sp) {
     const int seg = blockIdx.y, nseg = sp.nseq * sp.P;
     const int i = blockIdx.x * NT + threadIdx.x;   // float4 within one segment's matrices
-    if (i == 0) {
-        const long off = (long)(seg % sp.P) * sp.L * CH;
-        sp.cu[seg] = (int32_t)((long)(seg / sp.P) * sp.T + (off < sp.T ? off : sp.T));
+    if (i == 0) {   // segment p of sequence b: chunks [p L, min((p + 1) L, NC)) of the sequence
+        const int b = seg / sp.P, p = seg % sp.P;
+        sp.chunk_off[seg] = b * sp.NC + min(p * sp.L, sp.NC);
+        if (seg < nseg) {
+            const long t0 = std::min((long)p * sp.L * CH, (long)sp.T), t1 = std::min((long)(p + 1) * sp.L * CH, (long)sp.T);
+            sp.seq_start[seg] = (int32_t)((long)b * sp.T + t0);
+            sp.seq_len[seg] = (int32_t)(t1 - t0);
+            sp.seq_perm[seg] = seg;
+        }
     }
     if (seg >= nseg) return;
     const int mat4 = sp.H * sp.DV * (DK / 4), id4 = sp.H * DK * (DK / 4);
@@ -2037,8 +2055,8 @@ struct SegPlan {
 struct SegCost {
     double seq_fixed, chunk, seg_fixed, per_token_head, per_segment;
 };
-constexpr SegCost COST_BF16 = {17.0, 0.73, 33.3, 3.6e-4, 1.4};
-constexpr SegCost COST_F32 = {12.0, 4.2, 40.0, 1.7e-3, 2.6};
+constexpr SegCost COST_BF16 = {17.0, 0.73, 28.5, 3.6e-4, 1.4};
+constexpr SegCost COST_F32 = {12.0, 4.2, 35.5, 1.7e-3, 2.6};
 
 // Segments per sequence.  Ragged input keeps the sequential form.
 SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io, long cus, int setting) {
@@ -2072,7 +2090,7 @@ SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io, l
 
 struct SegLayout {
     Layout base;   // ragged layout over the nseq P segments
-    size_t cu, S0seg, Iseg, N, M, X, Y, total;
+    size_t S0seg, Iseg, N, M, X, Y, total;
 };
 
 bool seg_layout(int B, int T, int H, int dk, int dv, int io, const SegPlan& sp, SegLayout* S) {
@@ -2084,7 +2102,6 @@ bool seg_layout(int B, int T, int H, int dk, int dv, int io, const SegPlan& sp, 
     const size_t tk = (size_t)B * T * H * dk * esz;
     size_t off = round_up(S->base.total, 256);
     auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, 256); return at; };
-    S->cu = take((size_t)(nseg + 1) * sizeof(int32_t));
     S->S0seg = take(sv);
     S->Iseg = take(sk);
     S->N = take(sv);
@@ -2106,14 +2123,23 @@ size_t plan_bytes(int B, int T, int H, int dk, int dv, int n_seqs, int io, const
     return ws_layout(B, T, H, dk, dv, n_seqs, io, &L) ? L.total : 0;
 }
 
+// The plan a call takes: the setting's (automatic: for this device), with fewer
+// segments while the workspace cannot hold it or a grid would overflow.
+SegPlan plan_for_call(int B, int T, int H, int dk, int dv, int n_seqs, int io, size_t workspace_bytes, SegLayout* S) {
+    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io, device_cus(), __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    const long nc = (T + CH - 1) / CH;
+    while (sp.P > 1 && !(seg_layout(B, T, H, dk, dv, io, sp, S) && S->total <= workspace_bytes &&
+                         (long)B * sp.P * H * ((dv + dk) / SL) < (1L << 31) && (long)B * (nc + SEG_MAX + 8) * H < (1L << 31)))
+        sp = plan_segments(B, T, H, dk, dv, n_seqs, io, 0, sp.P - 1);
+    return sp;
+}
+
 template <typename IO, int DK>
 void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st) {
     const long nseg = (long)sq.nseq * sq.P;
     const long per_seg = (long)sq.H * std::max(sq.DV, DK) * DK / 4;   // float4s of one segment's initial states
     hipLaunchKernelGGL((k_segment_prep<DK>), dim3((unsigned)((per_seg + NT - 1) / NT), (unsigned)(nseg + 1)), dim3(NT), 0,
                        st, sq);
-    hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start, p.seq_len,
-                       p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
     if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     else
@@ -2177,6 +2203,17 @@ extern "C" size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk,
     const SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, PLAN_CUS,
                                      __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
     return std::max(L.total, plan_bytes(B, T, H, dk, dv, n_seqs, io_dtype, sp));
+}
+
+extern "C" int gdn_chunk_prefill_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype) {
+    if (B < 1 || T < 0 || H < 1 || n_seqs < 0 || (n_seqs > 0 && B != 1)) return 0;
+    if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return 0;
+    if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return 0;
+    Layout L;
+    if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L)) return 0;
+    SegLayout S;
+    return plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype,
+                         gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, CH, n_seqs, io_dtype), &S).P;
 }
 
 extern "C" int gdn_set_prefill_segments(int segments) {
@@ -2249,17 +2286,12 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     // segment-parallel form when the plan splits and the workspace holds it
-    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, device_cus(),
-                               __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
     SegLayout S;
-    while (sp.P > 1 && !(seg_layout(B, T, H, dk, dv, io_dtype, sp, &S) && S.total <= workspace_bytes &&
-                         (long)B * sp.P * H * ((dv + dk) / SL) < (1L << 31) && (long)B * p.NC * H < (1L << 31)))
-        sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, 0, sp.P - 1);
+    const SegPlan sp = plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, workspace_bytes, &S);
     if (sp.P > 1) {
         const int nseg = B * sp.P;
         SegParams sq;
         sq.nseq = B; sq.P = sp.P; sq.L = sp.L; sq.T = T; sq.NC = p.NC; sq.H = H; sq.DV = dv; sq.DK = dk;
-        sq.cu = reinterpret_cast<int32_t*>(ws + S.cu);
         sq.S0 = S0;
         sq.S0seg = reinterpret_cast<float*>(ws + S.S0seg);
         sq.Iseg = reinterpret_cast<float*>(ws + S.Iseg);
@@ -2273,13 +2305,14 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
         Params r = p;
         r.B = 1; r.T = B * T; r.n_seq = nseg; r.ragged = 1;
         r.cpt = (r.T + CH - 1) / CH; r.NC = r.cpt;
-        r.cu = sq.cu;
+        r.cu = nullptr;
         r.S0 = sq.S0seg; r.ST = const_cast<float*>(sq.N);
         r.seq_start = reinterpret_cast<int32_t*>(ws);
         r.seq_len = r.seq_start + (nseg + 1);
         r.chunk_off = r.seq_len + (nseg + 1);
         r.seq_perm = r.chunk_off + (nseg + 1);
-        r.cprefix = r.seq_perm + (nseg + 1);
+        r.cprefix = r.seq_perm + (nseg + 1);   // read only by the one-launch form
+        sq.seq_start = r.seq_start; sq.seq_len = r.seq_len; sq.chunk_off = r.chunk_off; sq.seq_perm = r.seq_perm;
         r.wsG = reinterpret_cast<float*>(ws + S.base.G);
         r.wsT = ws + S.base.T;
         r.wsP = ws + S.base.P;

@@ -57,6 +57,12 @@ WORKLOADS = {
     # same shape with slow decay (mean alpha ~ 0.84): long-memory numerics
     "prefill_10k_bf16_slow": Workload("prefill_10k_bf16_slow", B=1, T=10240, H=16, dk=128,
                                       dv=128, io="bf16", seed=1012, s0_std=0.02, g_shift=-2.0),
+    # one device's share of the 16 heads under an 8-way head split: the sequential chain
+    # leaves most CUs idle, so the prefill takes the segment-parallel form
+    "prefill_10k_h2_bf16": Workload("prefill_10k_h2_bf16", B=1, T=10240, H=2, dk=128, dv=128,
+                                    io="bf16", seed=1005, s0_std=0.02, g_shift=2.0),
+    "prefill_10k_h2_f32": Workload("prefill_10k_h2_f32", B=1, T=10240, H=2, dk=128, dv=128,
+                                   io="f32", seed=1006, s0_std=0.02, g_shift=2.0),
     # 8 packed sequences of uniform length in [512, 4096], per-sequence state
     "ragged_8seq_bf16": Workload("ragged_8seq_bf16", B=1, T=0, H=16, dk=128, dv=128, io="bf16",
                                  seed=1003, s0_std=0.02, ragged=8),
