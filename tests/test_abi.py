@@ -97,6 +97,16 @@ def test_segment_setting_and_workspace():
         assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
         set_(1)
         assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
+        # the count a call would use: forced counts need no device; invalid sizes give 0
+        q = gdn.gdn_chunk_prefill_segments
+        set_(3)
+        assert q(1, 4096, 2, 128, 128, 0, bf) == 3
+        assert q(1, 4096, 2, 128, 128, 3, bf) == 1           # ragged: sequential
+        assert q(1, 100, 2, 128, 128, 0, bf) == 2            # two chunks: at most two segments
+        set_(1)
+        assert q(1, 4096, 2, 128, 128, 0, bf) == 1
+        for bad in [(0, 10, 1, 64, 64, 0, 0), (1, 10, 1, 96, 64, 0, 0), (2, 10, 1, 64, 64, 3, 0), (1, 10, 1, 64, 64, 0, 7)]:
+            assert q(*bad) == 0, bad
     finally:
         set_(prev)
 

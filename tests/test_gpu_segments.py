@@ -107,6 +107,12 @@ def test_segmented_in_place_state(segments):
     assert oracle.max_rel_err(f64(o), o_ref) < TOL["f32"]
 
 
+def test_headline_shape_stays_sequential(segments):
+    """16 heads at T=10240: the two runs of two segments would not fit beside each other."""
+    for io in (gdn.GDN_BF16, gdn.GDN_F32):
+        assert gdn.gdn_chunk_prefill_segments(1, 10240, 16, 128, 128, 0, io) == 1
+
+
 def test_segmented_agrees_with_sequential(segments):
     """The same inputs through both forms: equal to bf16 rounding of o, and close in S_T."""
     x = inputs.make_prefill(B=1, T=2000, H=2, dk=128, dv=128, io="bf16", seed=23, s0_std=0.05)
@@ -155,6 +161,7 @@ def test_automatic_split_long_prompt(segments, io, H):
                             s0_std=0.02, g_shift=2.0)
     assert gdn.gdn_chunk_prefill_workspace_bytes(1, 10240, H, 128, 128, 64, 0, IO[io]) > \
         _seq_bytes(segments, 1, 10240, H, IO[io])
+    assert gdn.gdn_chunk_prefill_segments(1, 10240, H, 128, 128, 0, IO[io]) > 1
     _check(x, io, "automatic split T=10240 H=%d %s" % (H, io))
 
 
