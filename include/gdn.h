@@ -108,6 +108,35 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
                              void* stream);
 
 /*
+ * Chunked prefill that also stores the state at chunk boundaries inside each
+ * sequence: the hook for a cache of recurrent-state snapshots indexed by prompt
+ * position (section 3, the engine's prefix-snapshot cache; section 6).  Arguments
+ * as gdn_chunk_prefill, plus:
+ *   snap_every  positive: a snapshot every snap_every chunks -- snapshot j
+ *               (j = 1, 2, ...) of a sequence is its state after its first
+ *               j * snap_every * chunk tokens, taken while that count is less than
+ *               the sequence's length (the state at the end is S_T)
+ *   snaps       [n, n_snap, H, dv, dk] fp32 DEVICE, n_snap = (T - 1) / (snap_every
+ *               * chunk) (integer division; T bounds every sequence's length);
+ *               snapshot j of sequence s at [s, j - 1]; entries past a sequence's
+ *               last snapshot are left as they were.  16-byte aligned; may be NULL
+ *               when n_snap is 0.  Must not overlap any other argument.
+ * The sequential form always (gdn_set_prefill_segments does not apply); the
+ * workspace is the one gdn_chunk_prefill_workspace_bytes gives.  Errors as
+ * gdn_chunk_prefill, and GDN_ERR_INVALID_ARG for snap_every < 1 or a missing or
+ * misaligned snaps.
+ */
+gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v,
+                                       const float* g, const float* beta, const float* S0,
+                                       void* o, float* S_T,
+                                       int B, int T, int H, int dk, int dv, int chunk,
+                                       const int32_t* cu_seqlens, int n_seqs,
+                                       int io_dtype, float scale,
+                                       int snap_every, float* snaps,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/*
  * Segment-parallel prefill (section 3.2: the chunk map is affine in the state,
  * S_{c+1}^T = M_c S_c^T + N_c, so a sequence's chunks can be grouped into
  * segments whose maps compose).  Dense input can be cut at chunk boundaries

@@ -16,7 +16,7 @@ import torch
 __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
-    "gdn_set_prefill_segments", "gdn_chunk_prefill_segments",
+    "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -49,6 +49,9 @@ def lib():
         L.gdn_chunk_prefill_workspace_bytes.restype = S
         L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill.restype = I
+        L.gdn_chunk_prefill_snapshots.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, I, P, P, S,
+                                                  P]
+        L.gdn_chunk_prefill_snapshots.restype = I
         L.gdn_chunk_prefill_segments.argtypes = [I] * 7
         L.gdn_chunk_prefill_segments.restype = I
         L.gdn_set_prefill_segments.argtypes = [I]
@@ -107,15 +110,7 @@ def _stream(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, scale=1.0,
-                      o=None, S_T=None, store_state=True, workspace=None):
-    """Chunked prefill; see ``gdn_chunk_prefill`` in include/gdn.h.
-
-    q,k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype); g, beta [B,T,H]
-    fp32; S0 [n,H,dv,dk] fp32 or None.  Ragged: B == 1 and ``cu_seqlens`` an
-    int32 CUDA tensor [n+1].  Returns ``(o, S_T)`` (S_T is None when
-    ``store_state`` is False).  ``S_T`` may be passed (also ``S_T is S0``).
-    """
+def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -149,11 +144,48 @@ def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, s
     need = gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
+    return dict(io=io, B=B, T=T, H=H, dk=dk, dv=dv, n=n, n_seqs=n_seqs, o=o, S_T=S_T, workspace=workspace)
+
+
+def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, scale=1.0,
+                      o=None, S_T=None, store_state=True, workspace=None):
+    """Chunked prefill; see ``gdn_chunk_prefill`` in include/gdn.h.
+
+    q,k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype); g, beta [B,T,H]
+    fp32; S0 [n,H,dv,dk] fp32 or None.  Ragged: B == 1 and ``cu_seqlens`` an
+    int32 CUDA tensor [n+1].  Returns ``(o, S_T)`` (S_T is None when
+    ``store_state`` is False).  ``S_T`` may be passed (also ``S_T is S0``).
+    """
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace)
     _check(lib().gdn_chunk_prefill(
-        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(o), _ptr(S_T),
-        B, T, H, dk, dv, chunk, _ptr(cu_seqlens), n_seqs, io, float(scale),
-        _ptr(workspace), workspace.numel(), _stream(q.device)))
-    return o, S_T
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"], float(scale),
+        _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
+    return a["o"], a["S_T"]
+
+
+def gdn_chunk_prefill_snapshots(q, k, v, g, beta, S0=None, *, snap_every, chunk=64, cu_seqlens=None, scale=1.0,
+                                o=None, S_T=None, snaps=None, store_state=True, workspace=None):
+    """Prefill that also returns state snapshots; see ``gdn_chunk_prefill_snapshots`` in include/gdn.h.
+
+    Returns ``(o, S_T, snaps)``; ``snaps`` is [n, (T-1) // (snap_every*chunk), H, dv, dk] fp32
+    (allocated zero-filled when not given; entries past a sequence's last snapshot keep their values).
+    """
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace)
+    n_snap = max(0, (a["T"] - 1) // (int(snap_every) * chunk)) if snap_every >= 1 else 0
+    shape = (a["n"], n_snap, a["H"], a["dv"], a["dk"])
+    if snaps is None:
+        snaps = torch.zeros(shape, device=q.device, dtype=torch.float32)
+    else:
+        _dev(snaps, "snaps", torch.float32)
+        if tuple(snaps.shape) != shape:
+            raise ValueError("snaps must be %s" % (shape,))
+    _check(lib().gdn_chunk_prefill_snapshots(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"], float(scale),
+        int(snap_every), _ptr(snaps) if n_snap > 0 else None, _ptr(a["workspace"]), a["workspace"].numel(),
+        _stream(q.device)))
+    return a["o"], a["S_T"], snaps
 
 
 def gdn_decode_step(q, k, v, g, beta, S, *, scale=1.0, o=None):

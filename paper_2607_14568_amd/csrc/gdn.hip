@@ -120,6 +120,9 @@ struct Params {
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
     int xcd_items;       // fused bf16 launch: chunk-terms items assigned by XCD (dense, 8 | H, 8 | npw)
     float scale;
+    float* snaps;        // state snapshots [n_seq, n_snap, H, DV, dk] (the SNAP kernels only)
+    int snap_every;      // ... after every snap_every chunks of a sequence, strictly inside it
+    int n_snap;
 };
 
 // Sequence at rank r when sequences are taken longest first (ragged), else r.
@@ -422,7 +425,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 
 // ------------------------------------------------------------------ fp32 state chain
 // One workgroup per (sequence, head, 16-row slice of S); chunks in order.
-template <int DK>
+template <int DK, bool SNAP = false>
 __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) {
     using IO = float;
     constexpr int PAD = 16 / sizeof(IO);
@@ -552,6 +555,12 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
         const int n = min(CH, len - c * CH);
         const float(*sSc)[DK + 4] = sS[c & 1];
         __syncthreads();   // previous chunk done with every tile
+        if constexpr (SNAP) {   // S_c, the state after c chunks
+            if (c > 0 && c % p.snap_every == 0) {
+                float* sn = p.snaps + (((long)s * p.n_snap + c / p.snap_every - 1) * H + h) * (long)DV * DK + (long)js * SL * DK;
+                for (int i = tid; i < SL * DK; i += NT) sn[i] = sSc[i / DK][i % DK];
+            }
+        }
         store(pre);
         __syncthreads();
 
@@ -651,9 +660,9 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
         }
 }
 
-template <int DK>
+template <int DK, bool SNAP = false>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
-    state_chain_f32<DK>(p, blockIdx.x);
+    state_chain_f32<DK, SNAP>(p, blockIdx.x);
 }
 
 // ------------------------------------------------------------------ bf16 state chain
@@ -774,8 +783,9 @@ template <int DK> struct ChainLds {
 // same launch; a chunk's terms are read only once its flag carries this call's
 // epoch, with loads that bypass the caches (their writers store the same way).
 // IDENT: the identity run of the segment-parallel form -- values read as zeros
-// and S_T stored transposed in bf16 (layout 2 of Params::st_t).
-template <int DK, bool FUSED, bool IDENT = false>
+// and S_T stored transposed in bf16 (layout 2 of Params::st_t).  SNAP: the
+// state is also stored after every snap_every chunks.
+template <int DK, bool FUSED, bool IDENT = false, bool SNAP = false>
 __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid, ChainLds<DK>& lds) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
     constexpr int HKD = NKD / 2;        // ... whose S^T rows one chain wave keeps
@@ -1024,7 +1034,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
                 for (int k2 = 0; k2 < HKD; ++k2) offY[mt][k2] = kq(16 * mt + l16, 32 * (w * HKD + k2) + 8 * lg);
-            auto cstep = [&](auto SLOT) {   // chunk c = SLOT (mod RING)
+            auto cstep = [&](int c, auto SLOT) {   // chunk c = SLOT (mod RING)
                 constexpr int b = decltype(SLOT)::value, bn = (b + 1) % RING, x2 = b & 1;
                 lds_barrier();   // barrier A_c: S_c halves and R'_c visible
                 const bf16x8 rfx = sRf[x2][1 - w][lane];
@@ -1060,6 +1070,14 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][0], df0, acc[m], 0, 0, 0);
                     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[m][1], df1, acc[m], 0, 0, 0);
                 }
+                if constexpr (SNAP) {   // S_{c+1}, the state after c + 1 chunks
+                    if ((c + 1) % p.snap_every == 0 && c + 1 < nc) {
+                        float* sn = p.snaps + (((long)s * p.n_snap + (c + 1) / p.snap_every - 1) * H + h) * (long)DV * DK +
+                                    (long)(js * SL + l16) * DK;
+#pragma unroll
+                        for (int m = 0; m < HMD; ++m) *reinterpret_cast<floatx4*>(sn + chan(w * HMD + m)) = acc[m];
+                    }
+                }
                 // S_{c+1}: this wave's half for the output waves, and its share of X_{c+1}
                 publish_s(1 - x2);
                 floatx4 yp[4];
@@ -1087,10 +1105,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 sRf[1 - x2][w][lane] = rfo;
             };
             for (int c = 0; c < nc; c += RING) {
-                cstep(Ic<0>{});
-                if (c + 1 < nc) cstep(Ic<1>{});
-                if (c + 2 < nc) cstep(Ic<2>{});
-                if (c + 3 < nc) cstep(Ic<3>{});
+                cstep(c, Ic<0>{});
+                if (c + 1 < nc) cstep(c + 1, Ic<1>{});
+                if (c + 2 < nc) cstep(c + 2, Ic<2>{});
+                if (c + 3 < nc) cstep(c + 3, Ic<3>{});
             }
             if constexpr (IDENT) {
                 bf16_t* st = reinterpret_cast<bf16_t*>(p.ST) + srow0 - (long)js * SL * DK + js * SL + l16;
@@ -1222,10 +1240,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 }
 
 // One workgroup per CU (its LDS), so two waves per SIMD: the register budget is that of two waves.
-template <int DK>
+template <int DK, bool SNAP = false>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_bf16(Params p) {
     __shared__ ChainLds<DK> lds;
-    state_chain_bf16<DK, false>(p, blockIdx.x, lds);
+    state_chain_bf16<DK, false, false, SNAP>(p, blockIdx.x, lds);
 }
 
 // ------------------------------------------------------------------ bf16 chunk terms
@@ -1543,7 +1561,7 @@ __global__ __launch_bounds__(NT, 3) void k_chunk_terms_bf16(Params p) {
 // in chunk order), the rest are chain workgroups.  The chunk-terms workgroups
 // are dispatched first and never wait, so the chain workgroups' waits end
 // whatever number of workgroups the device holds at once.
-template <int DK>
+template <int DK, bool SNAP = false>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_prefill_fused_bf16(Params p) {
     static_assert(NT_CHAIN == 2 * NT, "two work items per chunk-terms workgroup");
     __shared__ union Lds {
@@ -1579,7 +1597,7 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
             }
         }
     } else {
-        state_chain_bf16<DK, true>(p, blockIdx.x - p.npw, lds.c);
+        state_chain_bf16<DK, true, false, SNAP>(p, blockIdx.x - p.npw, lds.c);
     }
 }
 
@@ -2000,7 +2018,7 @@ uint64_t next_epoch() {
     return (salt << 32) | (uint32_t)(++counter);
 }
 
-template <typename IO, int DK>
+template <typename IO, int DK, bool SNAP = false>
 void launch_prefill(Params p, long slots, hipStream_t st) {
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
@@ -2018,7 +2036,7 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
             p.xcd_items = !p.ragged && p.H % 8 == 0 && p.npw >= 8;
             if (p.xcd_items) p.npw &= ~7;
             p.epoch = next_epoch();
-            hipLaunchKernelGGL((k_prefill_fused_bf16<DK>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
+            hipLaunchKernelGGL((k_prefill_fused_bf16<DK, SNAP>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
             return;
         }
     }
@@ -2030,9 +2048,9 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
     }
     const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
     if constexpr (sizeof(IO) == 2)
-        hipLaunchKernelGGL((k_state_chain_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain_bf16<DK, SNAP>), grid, dim3(NT_CHAIN), 0, st, p);
     else
-        hipLaunchKernelGGL((k_state_chain<DK>), grid, dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain<DK, SNAP>), grid, dim3(NT), 0, st, p);
 }
 
 // ---- segment-parallel form: plan, workspace, launches
@@ -2221,12 +2239,11 @@ extern "C" int gdn_set_prefill_segments(int segments) {
     return __atomic_exchange_n(&g_segments, segments, __ATOMIC_RELAXED);
 }
 
-extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v, const float* g,
-                                        const float* beta, const float* S0, void* o, float* S_T, int B,
-                                        int T, int H, int dk, int dv, int chunk, const int32_t* cu_seqlens,
-                                        int n_seqs, int io_dtype, float scale, void* workspace,
-                                        size_t workspace_bytes, void* stream) {
-    g_err[0] = '\0';
+// The prefill behind both entry points: snap_every = 0 takes no snapshots.
+static gdn_status prefill(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                          const float* S0, void* o, float* S_T, int B, int T, int H, int dk, int dv, int chunk,
+                          const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int snap_every,
+                          float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1 || T < 0) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d T=%d out of range", B, H, T);
@@ -2281,13 +2298,17 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     p.npw = 0;
     p.xcd_items = 0;
     p.scale = scale;
+    p.snaps = snaps;
+    p.snap_every = snap_every;
+    p.n_snap = snap_every > 0 ? (T - 1) / (snap_every * CH) : 0;
     if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.flags = nullptr; }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
-    // segment-parallel form when the plan splits and the workspace holds it
+    // segment-parallel form when the plan splits and the workspace holds it (never
+    // with snapshots: the states inside segments are not formed)
     SegLayout S;
-    const SegPlan sp = plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, workspace_bytes, &S);
+    const SegPlan sp = p.n_snap > 0 ? SegPlan{} : plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, workspace_bytes, &S);
     if (sp.P > 1) {
         const int nseg = B * sp.P;
         SegParams sq;
@@ -2328,7 +2349,15 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
         if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
         return GDN_OK;
     }
-    if (io_dtype == GDN_BF16) {
+    if (p.n_snap > 0) {
+        if (io_dtype == GDN_BF16) {
+            if (dk == 128) launch_prefill<bf16_t, 128, true>(p, L.slots, hs);
+            else launch_prefill<bf16_t, 64, true>(p, L.slots, hs);
+        } else {
+            if (dk == 128) launch_prefill<float, 128, true>(p, L.slots, hs);
+            else launch_prefill<float, 64, true>(p, L.slots, hs);
+        }
+    } else if (io_dtype == GDN_BF16) {
         if (dk == 128) launch_prefill<bf16_t, 128>(p, L.slots, hs);
         else launch_prefill<bf16_t, 64>(p, L.slots, hs);
     } else {
@@ -2338,6 +2367,33 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
+}
+
+extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v, const float* g,
+                                        const float* beta, const float* S0, void* o, float* S_T, int B,
+                                        int T, int H, int dk, int dv, int chunk, const int32_t* cu_seqlens,
+                                        int n_seqs, int io_dtype, float scale, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+    g_err[0] = '\0';
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+                   nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v, const float* g,
+                                                  const float* beta, const float* S0, void* o, float* S_T, int B,
+                                                  int T, int H, int dk, int dv, int chunk,
+                                                  const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale,
+                                                  int snap_every, float* snaps, void* workspace,
+                                                  size_t workspace_bytes, void* stream) {
+    g_err[0] = '\0';
+    if (snap_every < 1) return fail(GDN_ERR_INVALID_ARG, "snap_every=%d must be positive", snap_every);
+    if (chunk == CH && T > 0 && (T - 1) / ((long)snap_every * CH) > 0) {
+        if (!snaps) return fail(GDN_ERR_INVALID_ARG, "snaps must be non-null when a snapshot falls inside the prompt");
+        if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
+    }
+    if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale,
+                   snap_every, snaps, workspace, workspace_bytes, stream);
 }
 
 extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* v, const float* g,

@@ -162,6 +162,30 @@ def test_prefill_argument_checks(L, kw, code):
     assert L.gdn_last_error_message().decode()
 
 
+def _snapshots(L, snap_every=1, snaps=A, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=2, dk=64, dv=64, chunk=64,
+             cu=None, n_seqs=0, io=0, scale=1.0, ws=A, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return L.gdn_chunk_prefill_snapshots(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S0"], a["o"], a["ST"],
+                                         a["B"], a["T"], a["H"], a["dk"], a["dv"], a["chunk"], a["cu"], a["n_seqs"],
+                                         a["io"], a["scale"], snap_every, snaps, a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(snap_every=0), INVALID),
+    (dict(snap_every=-3), INVALID),
+    (dict(snaps=None), INVALID),              # T=128: one snapshot falls inside the prompt
+    (dict(snaps=A + 8), INVALID),             # not 16-byte aligned
+    (dict(snaps=A, chunk=32), UNSUPPORTED),   # the prefill's own checks still apply
+    (dict(snaps=A, io=5), INVALID),
+    (dict(snaps=A, ws_bytes=100), WORKSPACE),
+])
+def test_snapshot_argument_checks(L, kw, code):
+    rc = _snapshots(L, **kw)
+    assert rc == code, (kw, rc, L.gdn_last_error_message())
+    assert L.gdn_last_error_message().decode()
+
+
 def test_prefill_workspace_exact_boundary(L):
     need = gdn.gdn_chunk_prefill_workspace_bytes(1, 128, 2, 64, 64, 64, 0, 0)
     assert _prefill(L, ws_bytes=need - 1) == WORKSPACE
