@@ -108,6 +108,32 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
                              void* stream);
 
 /*
+ * Chunked prefill with grouped key heads: q and k carry H_k heads and each of
+ * the H value heads reads one of them, value head h the key head h / (H / H_k)
+ * (section 2.2 keeps one state per value head; the model family's recurrent
+ * layers share query and key heads across groups of value heads).  Every
+ * value head still has its own state, gate g, write strength beta and output.
+ *
+ *   q, k     [B, T, H_k, dk] io_dtype
+ *   v, o     [B, T, H, dv]   io_dtype
+ *   g, beta  [B, T, H]       fp32
+ *   S0, S_T  [n, H, dv, dk]  fp32 (as gdn_chunk_prefill)
+ *   H_k      1 <= H_k <= H and H_k divides H (GDN_ERR_INVALID_ARG otherwise);
+ *            H_k = H is gdn_chunk_prefill exactly
+ * All other arguments, the workspace (gdn_chunk_prefill_workspace_bytes with the
+ * value-head count H), the segment-parallel setting and the errors are those of
+ * gdn_chunk_prefill.
+ */
+gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v,
+                                     const float* g, const float* beta, const float* S0,
+                                     void* o, float* S_T,
+                                     int B, int T, int H, int H_k, int dk, int dv, int chunk,
+                                     const int32_t* cu_seqlens, int n_seqs,
+                                     int io_dtype, float scale,
+                                     void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+/*
  * Chunked prefill that also stores the state at chunk boundaries inside each
  * sequence: the hook for a cache of recurrent-state snapshots indexed by prompt
  * position (section 3, the engine's prefix-snapshot cache; section 6).  Arguments
@@ -187,6 +213,17 @@ gdn_status gdn_decode_step(const void* q, const void* k, const void* v,
                            const float* g, const float* beta, float* S, void* o,
                            int B, int H, int dk, int dv, int io_dtype, float scale,
                            void* stream);
+
+/*
+ * One decode step with grouped key heads (as gdn_chunk_prefill_grouped): q, k
+ * [B, H_k, dk]; value head h reads key head h / (H / H_k).  v, o, g, beta and S
+ * as gdn_decode_step; 1 <= H_k <= H and H_k divides H (GDN_ERR_INVALID_ARG
+ * otherwise).  Needs no workspace.
+ */
+gdn_status gdn_decode_step_grouped(const void* q, const void* k, const void* v,
+                                   const float* g, const float* beta, float* S, void* o,
+                                   int B, int H, int H_k, int dk, int dv, int io_dtype, float scale,
+                                   void* stream);
 
 #ifdef __cplusplus
 }

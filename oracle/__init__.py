@@ -106,6 +106,31 @@ def recurrence(q, k, v, g, beta, S0=None, *, cu_seqlens=None, scale=1.0, n_threa
     return (o, ST) if return_state else o
 
 
+def expand_key_heads(x, H):
+    """Query or key heads [..., H_k, d] -> one per value head [..., H, d].
+
+    Grouped key heads (section 2.2 keeps one state per value head): value head h
+    reads key head h // (H // H_k), so consecutive groups of H // H_k value heads
+    share a query and key head.
+    """
+    x = _f64(x)
+    Hk = x.shape[-2]
+    assert H % Hk == 0, (H, Hk)
+    return np.ascontiguousarray(x[..., np.arange(H) // (H // Hk), :])
+
+
+def recurrence_grouped(q, k, v, g, beta, S0=None, **kw):
+    """:func:`recurrence` with q,k [B,T,H_k,dk] shared by groups of value heads (v [B,T,H,dv])."""
+    H = np.shape(v)[2]
+    return recurrence(expand_key_heads(q, H), expand_key_heads(k, H), v, g, beta, S0, **kw)
+
+
+def decode_step_grouped(q, k, v, g, beta, S, **kw):
+    """:func:`decode_step` with q,k [B,H_k,dk] shared by groups of value heads (v [B,H,dv])."""
+    H = np.shape(v)[1]
+    return decode_step(expand_key_heads(q, H), expand_key_heads(k, H), v, g, beta, S, **kw)
+
+
 def decode_step(q, k, v, g, beta, S, *, scale=1.0, n_threads=0):
     """One token per sequence: q,k [B,H,dk]; v [B,H,dv]; g,beta [B,H]; S [B,H,dv,dk].
 

@@ -17,6 +17,7 @@ __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
     "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
+    "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -49,6 +50,8 @@ def lib():
         L.gdn_chunk_prefill_workspace_bytes.restype = S
         L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill.restype = I
+        L.gdn_chunk_prefill_grouped.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, P, S, P]
+        L.gdn_chunk_prefill_grouped.restype = I
         L.gdn_chunk_prefill_snapshots.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, I, P, P, S,
                                                   P]
         L.gdn_chunk_prefill_snapshots.restype = I
@@ -58,6 +61,8 @@ def lib():
         L.gdn_set_prefill_segments.restype = I
         L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
         L.gdn_decode_step.restype = I
+        L.gdn_decode_step_grouped.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P]
+        L.gdn_decode_step_grouped.restype = I
         _lib = L
     return _lib
 
@@ -110,7 +115,7 @@ def _stream(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace):
+def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=False):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -118,7 +123,8 @@ def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, 
         _dev(t, name, q.dtype)
     _dev(g, "g", torch.float32)
     _dev(beta, "beta", torch.float32)
-    B, T, H, dk = q.shape
+    B, T, HK, dk = q.shape
+    H = v.shape[2] if grouped else HK
     dv = v.shape[-1]
     if k.shape != q.shape or tuple(v.shape[:3]) != (B, T, H) or tuple(g.shape) != (B, T, H) \
             or beta.shape != g.shape:
@@ -144,7 +150,7 @@ def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, 
     need = gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
-    return dict(io=io, B=B, T=T, H=H, dk=dk, dv=dv, n=n, n_seqs=n_seqs, o=o, S_T=S_T, workspace=workspace)
+    return dict(io=io, B=B, T=T, H=H, HK=HK, dk=dk, dv=dv, n=n, n_seqs=n_seqs, o=o, S_T=S_T, workspace=workspace)
 
 
 def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, scale=1.0,
@@ -161,6 +167,21 @@ def gdn_chunk_prefill(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, s
         _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
         a["B"], a["T"], a["H"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"], float(scale),
         _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
+    return a["o"], a["S_T"]
+
+
+def gdn_chunk_prefill_grouped(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens=None, scale=1.0,
+                              o=None, S_T=None, store_state=True, workspace=None):
+    """Prefill with grouped key heads; see ``gdn_chunk_prefill_grouped`` in include/gdn.h.
+
+    q,k [B,T,H_k,dk]; v [B,T,H,dv]; g, beta [B,T,H]; value head h reads key head
+    h // (H // H_k).  Otherwise as ``gdn_chunk_prefill``.
+    """
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=True)
+    _check(lib().gdn_chunk_prefill_grouped(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
+        float(scale), _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
     return a["o"], a["S_T"]
 
 
@@ -190,6 +211,15 @@ def gdn_chunk_prefill_snapshots(q, k, v, g, beta, S0=None, *, snap_every, chunk=
 
 def gdn_decode_step(q, k, v, g, beta, S, *, scale=1.0, o=None):
     """One decode step; ``S`` [B,H,dv,dk] fp32 is updated in place.  Returns o [B,H,dv]."""
+    return _decode(q, k, v, g, beta, S, scale, o, grouped=False)
+
+
+def gdn_decode_step_grouped(q, k, v, g, beta, S, *, scale=1.0, o=None):
+    """One decode step with grouped key heads: q, k [B,H_k,dk], v [B,H,dv]; ``S`` updated in place.  Returns o."""
+    return _decode(q, k, v, g, beta, S, scale, o, grouped=True)
+
+
+def _decode(q, k, v, g, beta, S, scale, o, grouped):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -198,7 +228,8 @@ def gdn_decode_step(q, k, v, g, beta, S, *, scale=1.0, o=None):
     _dev(g, "g", torch.float32)
     _dev(beta, "beta", torch.float32)
     _dev(S, "S", torch.float32)
-    B, H, dk = q.shape
+    B, HK, dk = q.shape
+    H = v.shape[1] if grouped else HK
     dv = v.shape[-1]
     if k.shape != q.shape or tuple(v.shape[:2]) != (B, H) or tuple(g.shape) != (B, H) \
             or beta.shape != g.shape or tuple(S.shape) != (B, H, dv, dk):
@@ -207,6 +238,10 @@ def gdn_decode_step(q, k, v, g, beta, S, *, scale=1.0, o=None):
         o = torch.empty_like(v)
     else:
         _dev(o, "o", q.dtype)
-    _check(lib().gdn_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
-                                 B, H, dk, dv, io, float(scale), _stream(q.device)))
+    if grouped:
+        _check(lib().gdn_decode_step_grouped(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
+                                             B, H, HK, dk, dv, io, float(scale), _stream(q.device)))
+    else:
+        _check(lib().gdn_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
+                                     B, H, dk, dv, io, float(scale), _stream(q.device)))
     return o

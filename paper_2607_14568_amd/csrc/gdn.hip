@@ -102,6 +102,7 @@ struct Params {
     int st_t;          // S_T layout: 0 as declared; 1 transposed, [n, H, dk, DV] (key channel, then
                        // state row); 2 transposed in bf16 (the bf16 chain's identity run)
     int B, T, H, DV;
+    int HK, G;         // key heads (q and k carry HK heads) and value heads per key head: head h reads key head h / G
     int n_seq;         // dense: B; ragged: number of packed sequences
     int ragged;
     int NC;            // dense: chunks per sequence
@@ -342,7 +343,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         p.wsG[slot * 2 * CH + lane] = expf((float)x);
         p.wsG[slot * 2 * CH + CH + lane] = expf((float)(xn - x));
     }
-    stage_rows2<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), sQ, reinterpret_cast<const IO*>(p.q), t0, n, H, h);
+    stage_rows2<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), sQ, reinterpret_cast<const IO*>(p.q), t0, n, p.HK,
+                                  h / p.G);
     __syncthreads();
 
     // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P)
@@ -479,16 +481,17 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
     auto ld = [](__amdgpu_buffer_rsrc_t r, int voff) {   // the whole offset in voff: it is what the range check sees
         return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
     };
-    const int kvo = ((tid / (DK / VE)) * H * DK + (tid % (DK / VE)) * VE) * (int)sizeof(IO);
+    const int HK = p.HK, hk = h / p.G;   // q and k rows of this head
+    const int kvo = ((tid / (DK / VE)) * HK * DK + (tid % (DK / VE)) * VE) * (int)sizeof(IO);
     const int vvo = ((tid / VPV) * H * DV + js * SL + (tid % VPV) * VE) * (int)sizeof(IO);
     auto load_kq = [&](int c, Pre& x) {
         const long t0 = start + (long)c * CH;
-        const long rb = (long)(min(CH, len - c * CH) - 1) * H + 1;   // rows of the head's chunk, in [T][H] rows
-        const auto rk = rs(reinterpret_cast<const IO*>(p.k) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
-        const auto rq = rs(reinterpret_cast<const IO*>(p.q) + (t0 * H + h) * DK, rb * DK * sizeof(IO));
+        const long rb = (long)(min(CH, len - c * CH) - 1) * HK + 1;   // rows of the key head's chunk, in [T][HK] rows
+        const auto rk = rs(reinterpret_cast<const IO*>(p.k) + (t0 * HK + hk) * DK, rb * DK * sizeof(IO));
+        const auto rq = rs(reinterpret_cast<const IO*>(p.q) + (t0 * HK + hk) * DK, rb * DK * sizeof(IO));
 #pragma unroll
         for (int j = 0; j < NKV; ++j) {
-            const int so = (NT / (DK / VE)) * j * H * DK * (int)sizeof(IO);
+            const int so = (NT / (DK / VE)) * j * HK * DK * (int)sizeof(IO);
             x.k[j] = ld(rk, kvo + so);
             x.q[j] = ld(rq, kvo + so);
         }
@@ -829,6 +832,12 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         return rsrc(reinterpret_cast<const bf16_t*>(base) + (tok0(c) * H + h) * width,
                     (uint32_t)(((long)(rows(c) - 1) * H + 1) * width * 2));
     };
+    // ... and over the rows of q or k, which carry HK heads (this head reads key head h / G)
+    const int HK = p.HK, hk = h / p.G;
+    auto krsrc = [&](const void* base, int c) {
+        return rsrc(reinterpret_cast<const bf16_t*>(base) + (tok0(c) * HK + hk) * DK,
+                    (uint32_t)(((long)(rows(c) - 1) * HK + 1) * DK * 2));
+    };
     // values; the identity run's read as zeros (a descriptor of no bytes)
     auto vrsrc = [&](int c) { return IDENT ? rsrc(p.k, 0u) : crsrc(p.v, DV, c); };
 
@@ -876,13 +885,13 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
         for (int j = 0; j < (NCH + NL - 1) / NL; ++j) {
             const int r = RPI * (li + NL * j) + lane / NCH;
-            koff[j] = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+            koff[j] = (r * HK * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
         }
         const int voff = ((32 * (li == NL - 1) + (lane >> 1)) * H * DV + js * SL + (lane & 1) * 8) * 2;
         // a chunk's copies of the inputs (K, V) and of its chunk terms (W, gamma)
         auto issue_in = [&](int c, auto SLOT, auto LI) {
             constexpr int sl = decltype(SLOT)::value, L = decltype(LI)::value;
-            const auto rk = crsrc(p.k, DK, c);
+            const auto rk = krsrc(p.k, c);
 #pragma unroll
             for (int i = L; i < NCH; i += NL) bdma16(rk, &sK[sl][RPI * i * DK], koff[i / NL]);
             if constexpr (L >= NL - 2) bdma16(vrsrc(c), &sV[sl][32 * (L == NL - 1) * SL], voff);
@@ -1138,10 +1147,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
             for (int j = 0; j < 32 / RPI; ++j) {
                 const int r = RPI * j + lane / NCH;
-                qoff[j] = ((32 * ow + r) * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+                qoff[j] = ((32 * ow + r) * HK * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             }
             auto load_q = [&](int c, bf16_t* sq) {
-                const auto rq = crsrc(p.q, DK, c);
+                const auto rq = krsrc(p.q, c);
 #pragma unroll
                 for (int j = 0; j < 32 / RPI; ++j) bdma16(rq, sq + RPI * j * DK, qoff[j]);
             };
@@ -1397,13 +1406,14 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     {   // K and Q tiles straight into LDS; loads i = wave, wave + 4, ...
         const bf16_t* gk = reinterpret_cast<const bf16_t*>(p.k);
         const bf16_t* gq = reinterpret_cast<const bf16_t*>(p.q);
-        const long row0 = t0 * H + h;
-        const uint32_t bytes = (uint32_t)(((long)(n - 1) * H + 1) * DK * 2);
+        const int HK = p.HK;   // q and k carry HK heads; this head reads key head h / G
+        const long row0 = t0 * HK + h / p.G;
+        const uint32_t bytes = (uint32_t)(((long)(n - 1) * HK + 1) * DK * 2);
         const auto rk = rsrc(gk + row0 * DK, bytes);
         const auto rq = rsrc(gq + row0 * DK, bytes);
         for (int i = wave; i < NCH; i += 4) {
             const int r = RPI * i + lane / NCH;
-            const int off = (r * H * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
+            const int off = (r * HK * DK + (((lane % NCH) ^ swz(r)) << 3)) * 2;
             bdma16(rk, sK + RPI * i * DK, off);
             bdma16(rq, sQ + RPI * i * DK, off);
         }
@@ -1608,16 +1618,18 @@ template <typename IO, int DK>
 __global__ __launch_bounds__(NT) void k_decode_step(const IO* __restrict__ q, const IO* __restrict__ k,
                                                     const IO* __restrict__ v, const float* __restrict__ g,
                                                     const float* __restrict__ beta, float* __restrict__ S,
-                                                    IO* __restrict__ o, int DV, int rows_per_wg, float scale) {
+                                                    IO* __restrict__ o, int H, int HK, int DV, int rows_per_wg,
+                                                    float scale) {
     constexpr int LPR = DK / 4;        // lanes per row
     constexpr int RPP = NT / LPR;      // rows per pass of the workgroup
-    const int bh = blockIdx.y;
+    const int bh = blockIdx.y;                                 // sequence * H + head
+    const long bk = (long)(bh / H) * HK + (bh % H) / (H / HK);   // its key row: key head h / (H / HK)
     const int tid = threadIdx.x, sub = tid % LPR;
     float kv[4], qv[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        kv[e] = to_f(k[(long)bh * DK + 4 * sub + e]);
-        qv[e] = scale * to_f(q[(long)bh * DK + 4 * sub + e]);
+        kv[e] = to_f(k[bk * DK + 4 * sub + e]);
+        qv[e] = scale * to_f(q[bk * DK + 4 * sub + e]);
     }
     const float a = expf(g[bh]);
     const float b = beta[bh];
@@ -2180,11 +2192,11 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
 
 template <typename IO, int DK>
 void launch_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
-                   float* S, void* o, int B, int H, int dv, float scale, hipStream_t st) {
+                   float* S, void* o, int B, int H, int HK, int dv, float scale, hipStream_t st) {
     const int rows_per_wg = 32;
     dim3 grid((dv + rows_per_wg - 1) / rows_per_wg, B * H);
     hipLaunchKernelGGL((k_decode_step<IO, DK>), grid, dim3(NT), 0, st, (const IO*)q, (const IO*)k,
-                       (const IO*)v, g, beta, S, (IO*)o, dv, rows_per_wg, scale);
+                       (const IO*)v, g, beta, S, (IO*)o, H, HK, dv, rows_per_wg, scale);
 }
 
 }  // namespace
@@ -2241,12 +2253,14 @@ extern "C" int gdn_set_prefill_segments(int segments) {
 
 // The prefill behind both entry points: snap_every = 0 takes no snapshots.
 static gdn_status prefill(const void* q, const void* k, const void* v, const float* g, const float* beta,
-                          const float* S0, void* o, float* S_T, int B, int T, int H, int dk, int dv, int chunk,
+                          const float* S0, void* o, float* S_T, int B, int T, int H, int HK, int dk, int dv, int chunk,
                           const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int snap_every,
                           float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1 || T < 0) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d T=%d out of range", B, H, T);
+    if (HK < 1 || HK > H || H % HK != 0)
+        return fail(GDN_ERR_INVALID_ARG, "H_k=%d key heads must divide the H=%d value heads", HK, H);
     gdn_status st = check_dims(dk, dv);
     if (st != GDN_OK) return st;
     if (chunk < 1) return fail(GDN_ERR_INVALID_ARG, "chunk=%d must be positive", chunk);
@@ -2279,6 +2293,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     Params p;
     p.q = q; p.k = k; p.v = v; p.g = g; p.beta = beta; p.S0 = S0; p.o = o; p.ST = S_T; p.st_t = 0;
     p.B = B; p.T = T; p.H = H; p.DV = dv;
+    p.HK = HK; p.G = H / HK;
     p.n_seq = n_seq;
     p.ragged = n_seqs > 0;
     p.NC = (T + CH - 1) / CH;
@@ -2375,7 +2390,17 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
                                         int n_seqs, int io_dtype, float scale, void* workspace,
                                         size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+                   nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v, const float* g,
+                                                const float* beta, const float* S0, void* o, float* S_T, int B,
+                                                int T, int H, int H_k, int dk, int dv, int chunk,
+                                                const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale,
+                                                void* workspace, size_t workspace_bytes, void* stream) {
+    g_err[0] = '\0';
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
                    nullptr, workspace, workspace_bytes, stream);
 }
 
@@ -2392,17 +2417,17 @@ extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, 
         if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
     }
     if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale,
                    snap_every, snaps, workspace, workspace_bytes, stream);
 }
 
-extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* v, const float* g,
-                                      const float* beta, float* S, void* o, int B, int H, int dk, int dv,
-                                      int io_dtype, float scale, void* stream) {
-    g_err[0] = '\0';
+static gdn_status decode(const void* q, const void* k, const void* v, const float* g, const float* beta, float* S,
+                         void* o, int B, int H, int HK, int dk, int dv, int io_dtype, float scale, void* stream) {
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d out of range", B, H);
+    if (HK < 1 || HK > H || H % HK != 0)
+        return fail(GDN_ERR_INVALID_ARG, "H_k=%d key heads must divide the H=%d value heads", HK, H);
     gdn_status st = check_dims(dk, dv);
     if (st != GDN_OK) return st;
     if (!q || !k || !v || !g || !beta || !S || !o)
@@ -2417,13 +2442,27 @@ extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     if (io_dtype == GDN_BF16) {
-        if (dk == 128) launch_decode<bf16_t, 128>(q, k, v, g, beta, S, o, B, H, dv, scale, hs);
-        else launch_decode<bf16_t, 64>(q, k, v, g, beta, S, o, B, H, dv, scale, hs);
+        if (dk == 128) launch_decode<bf16_t, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
+        else launch_decode<bf16_t, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
     } else {
-        if (dk == 128) launch_decode<float, 128>(q, k, v, g, beta, S, o, B, H, dv, scale, hs);
-        else launch_decode<float, 64>(q, k, v, g, beta, S, o, B, H, dv, scale, hs);
+        if (dk == 128) launch_decode<float, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
+        else launch_decode<float, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
+}
+
+extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* v, const float* g,
+                                      const float* beta, float* S, void* o, int B, int H, int dk, int dv,
+                                      int io_dtype, float scale, void* stream) {
+    g_err[0] = '\0';
+    return decode(q, k, v, g, beta, S, o, B, H, H, dk, dv, io_dtype, scale, stream);
+}
+
+extern "C" gdn_status gdn_decode_step_grouped(const void* q, const void* k, const void* v, const float* g,
+                                              const float* beta, float* S, void* o, int B, int H, int H_k, int dk,
+                                              int dv, int io_dtype, float scale, void* stream) {
+    g_err[0] = '\0';
+    return decode(q, k, v, g, beta, S, o, B, H, H_k, dk, dv, io_dtype, scale, stream);
 }

@@ -81,13 +81,14 @@ def _l2n(x: np.ndarray) -> np.ndarray:
 
 
 def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
-                 lengths=None, ragged=0, len_range=(512, 4096)):
+                 lengths=None, ragged=0, len_range=(512, 4096), H_k=None):
     """Dense (B,T) or ragged (``ragged`` sequences, or explicit ``lengths``) inputs.
 
-    Returns a dict of CPU torch tensors: q,k [B,T,H,dk] and v [B,T,H,dv] in the io
-    dtype; g, beta [B,T,H] fp32; S0 [n_seq,H,dv,dk] fp32 or None; cu_seqlens
-    int32 [n_seq+1] or None.
+    Returns a dict of CPU torch tensors: q,k [B,T,H_k,dk] (H_k = H unless given)
+    and v [B,T,H,dv] in the io dtype; g, beta [B,T,H] fp32; S0 [n_seq,H,dv,dk]
+    fp32 or None; cu_seqlens int32 [n_seq+1] or None.
     """
+    H_k = H if H_k is None else H_k
     rng = np.random.default_rng(seed)
     cu = None
     if ragged or lengths is not None:
@@ -99,8 +100,8 @@ def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
         n_seq = len(lengths)
     else:
         n_seq = B
-    q = _l2n(rng.standard_normal((B, T, H, dk)))
-    k = _l2n(rng.standard_normal((B, T, H, dk)))
+    q = _l2n(rng.standard_normal((B, T, H_k, dk)))
+    k = _l2n(rng.standard_normal((B, T, H_k, dk)))
     v = rng.standard_normal((B, T, H, dv))
     beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((B, T, H))))
     g = -np.logaddexp(0.0, rng.standard_normal((B, T, H)) + g_shift)
@@ -114,15 +115,16 @@ def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
     )
 
 
-def make_decode(B, H, dk, dv, io="f32", seed=0, s0_std=0.02, pool=16):
+def make_decode(B, H, dk, dv, io="f32", seed=0, s0_std=0.02, pool=16, H_k=None):
     """Decode inputs: a pool of ``pool`` tokens per sequence, cycled by step index.
 
-    Returns q,k [pool,B,H,dk], v [pool,B,H,dv] (io dtype); g, beta [pool,B,H] fp32;
-    S [B,H,dv,dk] fp32.
+    Returns q,k [pool,B,H_k,dk] (H_k = H unless given), v [pool,B,H,dv] (io
+    dtype); g, beta [pool,B,H] fp32; S [B,H,dv,dk] fp32.
     """
+    H_k = H if H_k is None else H_k
     rng = np.random.default_rng(seed)
-    q = _l2n(rng.standard_normal((pool, B, H, dk)))
-    k = _l2n(rng.standard_normal((pool, B, H, dk)))
+    q = _l2n(rng.standard_normal((pool, B, H_k, dk)))
+    k = _l2n(rng.standard_normal((pool, B, H_k, dk)))
     v = rng.standard_normal((pool, B, H, dv))
     beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((pool, B, H))))
     g = -np.logaddexp(0.0, rng.standard_normal((pool, B, H)))

@@ -191,6 +191,61 @@ def test_prefill_workspace_exact_boundary(L):
     assert _prefill(L, ws_bytes=need - 1) == WORKSPACE
 
 
+def _prefill_grouped(L, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=4, Hk=2, dk=64, dv=64, chunk=64,
+             cu=None, n_seqs=0, io=0, scale=1.0, ws=A, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return L.gdn_chunk_prefill_grouped(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S0"], a["o"], a["ST"],
+                                       a["B"], a["T"], a["H"], a["Hk"], a["dk"], a["dv"], a["chunk"], a["cu"],
+                                       a["n_seqs"], a["io"], a["scale"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hk=0), INVALID),
+    (dict(Hk=-2), INVALID),
+    (dict(Hk=8), INVALID),                    # more key heads than value heads
+    (dict(Hk=3), INVALID),                    # does not divide H = 4
+    (dict(H=6, Hk=4), INVALID),
+    (dict(H=0, Hk=1), INVALID),
+    (dict(dk=96), UNSUPPORTED),               # the prefill's own checks still apply
+    (dict(chunk=32), UNSUPPORTED),
+    (dict(q=A + 8), INVALID),
+    (dict(ws_bytes=1000), WORKSPACE),
+])
+def test_grouped_prefill_argument_checks(L, kw, code):
+    rc = _prefill_grouped(L, **kw)
+    assert rc == code, (kw, rc, L.gdn_last_error_message())
+    assert L.gdn_last_error_message().decode()
+
+
+def _decode_grouped(L, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=4, Hk=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
+    a.update(kw)
+    return L.gdn_decode_step_grouped(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S"], a["o"], a["B"], a["H"],
+                                     a["Hk"], a["dk"], a["dv"], a["io"], a["scale"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hk=0), INVALID), (dict(Hk=3), INVALID), (dict(Hk=5), INVALID), (dict(B=0), INVALID),
+    (dict(dk=100), UNSUPPORTED), (dict(S=None), INVALID), (dict(S=A + 8), INVALID),
+])
+def test_grouped_decode_argument_checks(L, kw, code):
+    assert _decode_grouped(L, **kw) == code
+
+
+def test_binding_grouped_shapes():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("checks CPU-tensor rejection only")
+    x = torch.zeros(1, 4, 2, 64)
+    v = torch.zeros(1, 4, 4, 64)
+    g = torch.zeros(1, 4, 4)
+    with pytest.raises(TypeError):
+        gdn.gdn_chunk_prefill_grouped(x, x, v, g, g)
+    with pytest.raises(TypeError):
+        gdn.gdn_decode_step_grouped(x[0], x[0], v[0], g[0], g[0], torch.zeros(1, 4, 64, 64))
+
+
 def _decode(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
     a.update(kw)

@@ -290,3 +290,74 @@ def test_chunk_terms_solve_their_triangular_systems():
     gam = np.exp(np.cumsum(g[0, :, 0]))
     np.testing.assert_allclose((I + tm["A"]) @ tm["W"], (beta[0, :, 0] * gam)[:, None] * k[0, :, 0],
                                atol=1e-12)
+
+
+# --------------------------------------------------------------------------- grouped key heads
+def _grouped_brute(q, k, v, g, beta, S0, G):
+    """Per value head h, token by token, with the rank-1 form and the key head h // G chosen by hand."""
+    B, T, H, dv = v.shape
+    dk = q.shape[-1]
+    o = np.zeros((B, T, H, dv))
+    ST = np.zeros((B, H, dv, dk))
+    for b in range(B):
+        for h in range(H):
+            kh = h // G
+            S = np.zeros((dv, dk)) if S0 is None else S0[b, h].copy()
+            for t in range(T):
+                kt, qt = k[b, t, kh], q[b, t, kh]
+                a, bt = math.exp(g[b, t, h]), beta[b, t, h]
+                S = a * (S - bt * np.outer(S @ kt, kt)) + bt * np.outer(v[b, t, h], kt)
+                o[b, t, h] = S @ qt
+            ST[b, h] = S
+    return o, ST
+
+
+@pytest.mark.parametrize("H,Hk", [(4, 2), (6, 3), (4, 1), (3, 3)])
+def test_grouped_key_heads_brute_force(H, Hk):
+    """Value head h reads key head h // (H / H_k): checked against a hand loop over heads."""
+    rng = np.random.default_rng(40 + H * 7 + Hk)
+    B, T, dk, dv = 2, 9, 4, 3
+    q = rng.standard_normal((B, T, Hk, dk))
+    k = rng.standard_normal((B, T, Hk, dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((B, T, H, dv))
+    beta = 1 / (1 + np.exp(-rng.standard_normal((B, T, H))))
+    g = -np.logaddexp(0, rng.standard_normal((B, T, H)))
+    S0 = 0.3 * rng.standard_normal((B, H, dv, dk))
+    o, ST = oracle.recurrence_grouped(q, k, v, g, beta, S0)
+    ro, rS = _grouped_brute(q, k, v, g, beta, S0, H // Hk)
+    np.testing.assert_allclose(o, ro, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(ST, rS, rtol=1e-12, atol=1e-12)
+
+
+def test_grouped_heads_sharing_a_key_head_differ_only_through_their_own_inputs():
+    """Two value heads of one group with equal v, g, beta give equal results; a head of another group does not."""
+    rng = np.random.default_rng(77)
+    B, T, H, Hk, dk, dv = 1, 11, 4, 2, 5, 3
+    q = rng.standard_normal((B, T, Hk, dk))
+    k = rng.standard_normal((B, T, Hk, dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = np.repeat(rng.standard_normal((B, T, 1, dv)), H, axis=2)
+    beta = np.full((B, T, H), 0.6)
+    g = np.full((B, T, H), -0.2)
+    o, ST = oracle.recurrence_grouped(q, k, v, g, beta)
+    np.testing.assert_array_equal(o[:, :, 0], o[:, :, 1])
+    np.testing.assert_array_equal(o[:, :, 2], o[:, :, 3])
+    assert np.abs(o[:, :, 0] - o[:, :, 2]).max() > 1e-3
+
+
+def test_grouped_decode_equals_grouped_prefill():
+    rng = np.random.default_rng(78)
+    B, T, H, Hk, dk, dv = 2, 6, 4, 2, 5, 3
+    q = rng.standard_normal((B, T, Hk, dk))
+    k = rng.standard_normal((B, T, Hk, dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((B, T, H, dv))
+    beta = 1 / (1 + np.exp(-rng.standard_normal((B, T, H))))
+    g = -np.logaddexp(0, rng.standard_normal((B, T, H)))
+    S = 0.1 * rng.standard_normal((B, H, dv, dk))
+    o, ST = oracle.recurrence_grouped(q, k, v, g, beta, S)
+    for t in range(T):
+        ot, S = oracle.decode_step_grouped(q[:, t], k[:, t], v[:, t], g[:, t], beta[:, t], S)
+        np.testing.assert_allclose(ot, o[:, t], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(S, ST, rtol=1e-12, atol=1e-12)
