@@ -54,6 +54,12 @@ typedef enum gdn_status {
 
 typedef enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
 
+/* Input transforms the _ex entry points apply inside their kernels (bit flags). */
+typedef enum gdn_flags {
+    GDN_QK_L2NORM = 1,     /* q and k scaled per (token, head) to k / sqrt(|k|^2 + 1e-6)          */
+    GDN_GATE_LOGITS = 2    /* g and beta arrive as logits a, b: g = -softplus(a), beta = sigmoid(b) */
+} gdn_flags;
+
 /* Library version, (major << 16) | minor. */
 int gdn_version(void);
 
@@ -132,6 +138,30 @@ gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v
                                      int io_dtype, float scale,
                                      void* workspace, size_t workspace_bytes,
                                      void* stream);
+
+/*
+ * Chunked prefill with the per-position input transforms done in its kernels
+ * (section 3 batches the per-position operations around the projections over
+ * the whole chunk; these are the ones that feed the scan).  Arguments as
+ * gdn_chunk_prefill_grouped, plus:
+ *   flags  0 or a combination of
+ *          GDN_QK_L2NORM    q and k are taken as given and each row (token, key
+ *                           head) is used scaled to x / sqrt(|x|^2 + 1e-6); `scale`
+ *                           still multiplies q afterwards.  A zero row stays zero.
+ *          GDN_GATE_LOGITS  the `g` and `beta` arguments hold logits a and b:
+ *                           log-decay g = -softplus(a) = -log(1 + exp(a)), write
+ *                           strength beta = 1 / (1 + exp(-b)).
+ *          Other bits: GDN_ERR_INVALID_ARG.  flags = 0 is gdn_chunk_prefill_grouped.
+ * The workspace is the one gdn_chunk_prefill_workspace_bytes gives.
+ */
+gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v,
+                                const float* g, const float* beta, const float* S0,
+                                void* o, float* S_T,
+                                int B, int T, int H, int H_k, int dk, int dv, int chunk,
+                                const int32_t* cu_seqlens, int n_seqs,
+                                int io_dtype, float scale, int flags,
+                                void* workspace, size_t workspace_bytes,
+                                void* stream);
 
 /*
  * Chunked prefill that also stores the state at chunk boundaries inside each
@@ -224,6 +254,15 @@ gdn_status gdn_decode_step_grouped(const void* q, const void* k, const void* v,
                                    const float* g, const float* beta, float* S, void* o,
                                    int B, int H, int H_k, int dk, int dv, int io_dtype, float scale,
                                    void* stream);
+
+/*
+ * One decode step with the input transforms of gdn_chunk_prefill_ex (`flags`)
+ * done in its kernel; otherwise as gdn_decode_step_grouped.  Needs no workspace.
+ */
+gdn_status gdn_decode_step_ex(const void* q, const void* k, const void* v,
+                              const float* g, const float* beta, float* S, void* o,
+                              int B, int H, int H_k, int dk, int dv, int io_dtype, float scale,
+                              int flags, void* stream);
 
 #ifdef __cplusplus
 }

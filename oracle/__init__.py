@@ -131,6 +131,39 @@ def decode_step_grouped(q, k, v, g, beta, S, **kw):
     return decode_step(expand_key_heads(q, H), expand_key_heads(k, H), v, g, beta, S, **kw)
 
 
+L2_EPS = 1e-6   # of the unit-length transform of q and k
+
+
+def l2_rows(x):
+    """Each row (last axis) scaled to x / sqrt(|x|^2 + 1e-6): the kernels' GDN_QK_L2NORM transform."""
+    x = _f64(x)
+    return x / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + L2_EPS)
+
+
+def gates_from_logits(a, b):
+    """GDN_GATE_LOGITS: log-decay g = -softplus(a) = -log(1 + exp(a)), write strength beta = sigmoid(b)."""
+    a, b = _f64(a), _f64(b)
+    return -np.logaddexp(0.0, a), 1.0 / (1.0 + np.exp(-b))
+
+
+def recurrence_ex(q, k, v, g, beta, S0=None, *, qk_l2norm=False, gate_logits=False, **kw):
+    """:func:`recurrence_grouped` after the input transforms the _ex entry points apply in their kernels."""
+    if qk_l2norm:
+        q, k = l2_rows(q), l2_rows(k)
+    if gate_logits:
+        g, beta = gates_from_logits(g, beta)
+    return recurrence_grouped(q, k, v, g, beta, S0, **kw)
+
+
+def decode_step_ex(q, k, v, g, beta, S, *, qk_l2norm=False, gate_logits=False, **kw):
+    """:func:`decode_step_grouped` after the same input transforms."""
+    if qk_l2norm:
+        q, k = l2_rows(q), l2_rows(k)
+    if gate_logits:
+        g, beta = gates_from_logits(g, beta)
+    return decode_step_grouped(q, k, v, g, beta, S, **kw)
+
+
 def decode_step(q, k, v, g, beta, S, *, scale=1.0, n_threads=0):
     """One token per sequence: q,k [B,H,dk]; v [B,H,dv]; g,beta [B,H]; S [B,H,dv,dk].
 

@@ -17,13 +17,15 @@ __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
     "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
-    "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped",
+    "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped", "gdn_chunk_prefill_ex", "gdn_decode_step_ex",
+    "GDN_QK_L2NORM", "GDN_GATE_LOGITS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgdn.so")
 
 GDN_F32, GDN_BF16 = 0, 1
+GDN_QK_L2NORM, GDN_GATE_LOGITS = 1, 2
 _IO = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
 _lib = None
 
@@ -52,6 +54,8 @@ def lib():
         L.gdn_chunk_prefill.restype = I
         L.gdn_chunk_prefill_grouped.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill_grouped.restype = I
+        L.gdn_chunk_prefill_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, P, S, P]
+        L.gdn_chunk_prefill_ex.restype = I
         L.gdn_chunk_prefill_snapshots.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, I, P, P, S,
                                                   P]
         L.gdn_chunk_prefill_snapshots.restype = I
@@ -63,6 +67,8 @@ def lib():
         L.gdn_decode_step.restype = I
         L.gdn_decode_step_grouped.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P]
         L.gdn_decode_step_grouped.restype = I
+        L.gdn_decode_step_ex.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P]
+        L.gdn_decode_step_ex.restype = I
         _lib = L
     return _lib
 
@@ -185,6 +191,21 @@ def gdn_chunk_prefill_grouped(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens
     return a["o"], a["S_T"]
 
 
+def gdn_chunk_prefill_ex(q, k, v, g, beta, S0=None, *, flags=0, chunk=64, cu_seqlens=None, scale=1.0,
+                         o=None, S_T=None, store_state=True, workspace=None):
+    """Prefill with in-kernel input transforms; see ``gdn_chunk_prefill_ex`` in include/gdn.h.
+
+    Shapes as ``gdn_chunk_prefill_grouped``.  ``flags``: GDN_QK_L2NORM (q, k taken
+    unnormalised) and/or GDN_GATE_LOGITS (``g``, ``beta`` hold the logits a, b).
+    """
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=True)
+    _check(lib().gdn_chunk_prefill_ex(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
+        float(scale), int(flags), _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
+    return a["o"], a["S_T"]
+
+
 def gdn_chunk_prefill_snapshots(q, k, v, g, beta, S0=None, *, snap_every, chunk=64, cu_seqlens=None, scale=1.0,
                                 o=None, S_T=None, snaps=None, store_state=True, workspace=None):
     """Prefill that also returns state snapshots; see ``gdn_chunk_prefill_snapshots`` in include/gdn.h.
@@ -219,7 +240,12 @@ def gdn_decode_step_grouped(q, k, v, g, beta, S, *, scale=1.0, o=None):
     return _decode(q, k, v, g, beta, S, scale, o, grouped=True)
 
 
-def _decode(q, k, v, g, beta, S, scale, o, grouped):
+def gdn_decode_step_ex(q, k, v, g, beta, S, *, flags=0, scale=1.0, o=None):
+    """One decode step with in-kernel input transforms (``flags`` as ``gdn_chunk_prefill_ex``).  Returns o."""
+    return _decode(q, k, v, g, beta, S, scale, o, grouped=True, flags=flags)
+
+
+def _decode(q, k, v, g, beta, S, scale, o, grouped, flags=None):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -238,7 +264,10 @@ def _decode(q, k, v, g, beta, S, scale, o, grouped):
         o = torch.empty_like(v)
     else:
         _dev(o, "o", q.dtype)
-    if grouped:
+    if flags is not None:
+        _check(lib().gdn_decode_step_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
+                                        B, H, HK, dk, dv, io, float(scale), int(flags), _stream(q.device)))
+    elif grouped:
         _check(lib().gdn_decode_step_grouped(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
                                              B, H, HK, dk, dv, io, float(scale), _stream(q.device)))
     else:

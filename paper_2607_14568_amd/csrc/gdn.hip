@@ -52,6 +52,16 @@ typedef uint16_t bf16_t;
 constexpr int CH = 64;    // chunk length (tokens)
 constexpr int NT = 256;   // threads per workgroup: 4 waves of 64
 constexpr int SL = 16;    // state rows (value channels) per chain workgroup
+constexpr int GS = 4 * CH;   // floats per (chunk slot, head) of the decay vectors: gamma, D, gamma s_k, gamma s_q
+
+// Input transforms the kernels can apply themselves (bits of Params::pre, the
+// flags of the _ex entry points): q and k scaled to unit length per (token,
+// head), k / sqrt(|k|^2 + eps); and g, beta given as logits, g = -softplus(a),
+// beta = sigmoid(b).
+constexpr int PRE_L2 = 1, PRE_GATES = 2;
+constexpr float L2_EPS = 1e-6f;
+__device__ __forceinline__ float gate_g(float a) { return -(fmaxf(a, 0.f) + log1pf(expf(-fabsf(a)))); }
+__device__ __forceinline__ float gate_beta(float b) { return 1.f / (1.f + expf(-b)); }
 
 // ------------------------------------------------------------------ conversions
 __device__ __forceinline__ float to_f(float x) { return x; }
@@ -113,7 +123,8 @@ struct Params {
     int32_t* seq_perm;   // ragged: sequences by chunk count, longest first
     int32_t* cprefix;    // ragged: [cpt + 1] (sequence, chunk index < c) pair counts
     int cpt;             // chunks of the longest possible sequence
-    float* wsG;          // [slot][H][128]: gamma_r = exp(G_r), then exp(G_n - G_r)
+    float* wsG;          // [slot][H][GS]: gamma_r = exp(G_r), D_r = exp(G_n - G_r) (times s_k,r with PRE_L2
+                         // in fp32 io), and with PRE_L2 gamma_r s_k,r and gamma_r s_q,r (s = 1 / |row|)
     void* wsT;           // [slot][H][64][64] io type
     void* wsP;           // [slot][H][64][64] io type
     uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
@@ -121,6 +132,7 @@ struct Params {
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
     int xcd_items;       // fused bf16 launch: chunk-terms items assigned by XCD (dense, 8 | H, 8 | npw)
     float scale;
+    int pre;             // PRE_L2 | PRE_GATES
     float* snaps;        // state snapshots [n_seq, n_snap, H, DV, dk] (the SNAP kernels only)
     int snap_every;      // ... after every snap_every chunks of a sequence, strictly inside it
     int n_snap;
@@ -316,7 +328,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __shared__ __attribute__((aligned(16))) float sP[CH][CH + 4];
     __shared__ float sZ[4][16][17];
     __shared__ double sG[CH];
-    __shared__ float sB[CH], sD[CH];
+    __shared__ float sB[CH], sD[CH], sSk[CH], sSq[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -329,6 +341,10 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         if (lane < n) {
             gv = p.g[(t0 + lane) * H + h];
             bv = p.beta[(t0 + lane) * H + h];
+            if (p.pre & PRE_GATES) {
+                gv = gate_g(gv);
+                bv = gate_beta(bv);
+            }
         }
         double x = gv;   // inclusive prefix sum over the chunk, fp64
 #pragma unroll
@@ -340,12 +356,30 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         sG[lane] = x;
         sB[lane] = bv;
         sD[lane] = expf((float)(xn - x));
-        p.wsG[slot * 2 * CH + lane] = expf((float)x);
-        p.wsG[slot * 2 * CH + CH + lane] = expf((float)(xn - x));
+        p.wsG[slot * GS + lane] = expf((float)x);
     }
     stage_rows2<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), sQ, reinterpret_cast<const IO*>(p.q), t0, n, p.HK,
                                   h / p.G);
     __syncthreads();
+    const bool l2 = p.pre & PRE_L2;
+    if (l2) {   // reciprocal row lengths of K (threads 0..63) and Q (64..127); rows past the chunk: 0
+        if (tid < 2 * CH) {
+            const int r = tid % CH;
+            const IO(*X)[DK + PAD] = tid < CH ? sK : sQ;
+            float ss = 0.f;
+            for (int j = 0; j < DK; ++j) ss += X[r][j] * X[r][j];
+            (tid < CH ? sSk : sSq)[r] = r < n ? 1.f / sqrtf(ss + L2_EPS) : 0.f;
+        }
+        __syncthreads();
+    }
+    if (tid < CH) {   // D (times s_k with PRE_L2), and the scaled decays the chain applies to K S^T and Q S^T
+        const float gam = expf((float)sG[tid]);
+        p.wsG[slot * GS + CH + tid] = l2 ? sD[tid] * sSk[tid] : sD[tid];
+        if (l2) {
+            p.wsG[slot * GS + 2 * CH + tid] = gam * sSk[tid];
+            p.wsG[slot * GS + 3 * CH + tid] = gam * sSq[tid];
+        }
+    }
 
     // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P)
     for (int job = wave; job < 20; job += 4) {
@@ -365,10 +399,11 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int r = bi * 16 + 4 * lg + e, i = bj * 16 + l16;
+            const float nrm = l2 ? (which ? sSq[r] : sSk[r]) * sSk[i] : 1.f;
             if (which == 0) {
-                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * acc[e] : 0.f;
+                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * (nrm * acc[e]) : 0.f;
             } else {
-                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * acc[e] : 0.f;
+                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * (nrm * acc[e]) : 0.f;
             }
         }
     }
@@ -449,7 +484,7 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
     __shared__ __attribute__((aligned(16))) IO sP[CH][CH + PAD];
     __shared__ float sV[CH][SL + 1];
     __shared__ __attribute__((aligned(16))) float sRt[SL][CH + 4], sUt[SL][CH + 4];   // R, U transposed
-    __shared__ __attribute__((aligned(16))) float sGam[CH], sDec[CH], sBeta[CH];
+    __shared__ __attribute__((aligned(16))) float sGam[CH], sDec[CH], sBeta[CH], sGk[CH], sGq[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
@@ -472,7 +507,7 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
     static_assert(CH * (DK / VE) % NT == 0 && CH * (CH / VE) % NT == 0, "loads per thread");
     struct Pre {
         uint4 k[NKV], q[NKV], t[NTV], pp[NTV], v[NVV];
-        float gam, dec, beta;
+        float gam, dec, beta, gk, gq;   // gk, gq: the decay applied to K S^T and to Q S^T
     };
     // buffer loads: one lane offset per tensor, rows past the chunk end read as zeros
     auto rs = [](const void* base, long bytes) {
@@ -514,9 +549,15 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
         for (int j = 0; j < NVV; ++j)
             x.v[j] = tid + NT * j < CH * VPV ? ld(rv, vvo + (NT / VPV) * j * H * DV * (int)sizeof(IO)) : make_uint4(0, 0, 0, 0);
         if (tid < CH) {
-            x.gam = p.wsG[slot * 2 * CH + tid];
-            x.dec = p.wsG[slot * 2 * CH + CH + tid];
+            x.gam = p.wsG[slot * GS + tid];
+            x.dec = p.wsG[slot * GS + CH + tid];
+            x.gk = x.gq = x.gam;
+            if (p.pre & PRE_L2) {
+                x.gk = p.wsG[slot * GS + 2 * CH + tid];
+                x.gq = p.wsG[slot * GS + 3 * CH + tid];
+            }
             x.beta = tid < n ? p.beta[(t0 + tid) * H + h] : 0.f;
+            if ((p.pre & PRE_GATES) && tid < n) x.beta = gate_beta(x.beta);
         }
     };
     auto store = [&](const Pre& x) {
@@ -545,6 +586,8 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
             sGam[tid] = x.gam;
             sDec[tid] = x.dec;
             sBeta[tid] = x.beta;
+            sGk[tid] = x.gk;
+            sGq[tid] = x.gq;
         }
     };
 
@@ -584,7 +627,7 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int r = wave * 16 + 4 * lg + e;
-                rv[e] = sBeta[r] * (sV[r][l16] - sGam[r] * x[e]);
+                rv[e] = sBeta[r] * (sV[r][l16] - sGk[r] * x[e]);
             }
             *reinterpret_cast<floatx4*>(&sRt[l16][wave * 16 + 4 * lg]) = rv;
         }
@@ -622,7 +665,7 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
             const int r = wave * 16 + 4 * lg + e;
             if (r < n)
                 go[((t0 + r) * H + h) * (long)DV + js * SL + l16] =
-                    from_f<IO>(p.scale * (sGam[r] * oq[e] + op[e]));
+                    from_f<IO>(p.scale * (sGq[r] * oq[e] + op[e]));
         }
 
         // S^T <- gamma_n S^T + K^T D U   (tiles of 16 key channels)
@@ -776,6 +819,8 @@ template <int DK> struct ChainLds {
     bf16x8 sW[RING][NFRAG][64];   // diag(D) T diag(beta)
     bf16_t sV[RING][CH * SL];
     float sG[RING][CH];           // gamma_r
+    float sGk[RING][CH];          // gamma_r s_k,r and gamma_r s_q,r (PRE_L2: K and Q taken unscaled)
+    float sGq[RING][CH];
     bf16x8 sSf[2][DK / 32][64];   // S_c and R'_c as MFMA operands, by chunk parity
     bf16x8 sRf[2][2][64];
     floatx4 sY[2][2][64];         // each chain wave's share of X_{c+1} for the other wave's token tiles
@@ -787,8 +832,10 @@ template <int DK> struct ChainLds {
 // epoch, with loads that bypass the caches (their writers store the same way).
 // IDENT: the identity run of the segment-parallel form -- values read as zeros
 // and S_T stored transposed in bf16 (layout 2 of Params::st_t).  SNAP: the
-// state is also stored after every snap_every chunks.
-template <int DK, bool FUSED, bool IDENT = false, bool SNAP = false>
+// state is also stored after every snap_every chunks.  NORM (PRE_L2): K and Q
+// rows arrive unscaled, so K S^T and Q S^T take the decays gamma s_k and gamma
+// s_q (the chunk terms fold s_k into W).
+template <int DK, bool FUSED, bool IDENT = false, bool SNAP = false, bool NORM = false>
 __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid, ChainLds<DK>& lds) {
     constexpr int NKD = DK / 32;        // MFMA contraction blocks over the key channels
     constexpr int HKD = NKD / 2;        // ... whose S^T rows one chain wave keeps
@@ -813,6 +860,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     auto& sY = lds.sY;
     auto& sV = lds.sV;
     auto& sG = lds.sG;
+    auto& sGk = NORM ? lds.sGk : lds.sG;   // decay of K S^T
+    auto& sGq = NORM ? lds.sGq : lds.sG;   // decay of Q S^T
     auto& sSf = lds.sSf;
     auto& sRf = lds.sRf;
     auto& sQ = lds.sQ;
@@ -902,7 +951,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
             const auto rw = rsrc(wsT + sc * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
 #pragma unroll
             for (int f = L; f < NFRAG; f += NL) bdma16<AUX>(rw, &sW[sl][f][0], (f * 64 + lane) * 16);
-            if constexpr (L == 0) bdma4<AUX>(rsrc(p.wsG + sc * 2 * CH, CH * 4), &sG[sl][0], lane * 4);
+            const auto rg = rsrc(p.wsG + sc * GS, GS * 4);
+            if constexpr (L == 0) bdma4<AUX>(rg, &sG[sl][0], lane * 4);
+            if constexpr (NORM && L == 1) bdma4<AUX>(rg, &lds.sGk[sl][0], (2 * CH + lane) * 4);
+            if constexpr (NORM && L == 2) bdma4<AUX>(rg, &lds.sGq[sl][0], (3 * CH + lane) * 4);
         };
         auto issue = [&](int c, auto SLOT, auto LI) {
             issue_in(c, SLOT, LI);
@@ -913,7 +965,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         // those loads in flight, so chunk c+2 has landed before barrier A_{c+1}.
         auto run = [&](auto LI) {
             constexpr int L = decltype(LI)::value;
-            constexpr int NI = (NCH - L + NL - 1) / NL + (NFRAG - L + NL - 1) / NL + (L >= NL - 2) + (L == 0);
+            constexpr int NI = (NCH - L + NL - 1) / NL + (NFRAG - L + NL - 1) / NL + (L >= NL - 2) + (L == 0) +
+                               (NORM && (L == 1 || L == 2));
             auto lstep = [&](int c, auto SLOT) {
                 constexpr int bn = (decltype(SLOT)::value + 3) % RING;
                 lds_barrier();   // A_c
@@ -999,7 +1052,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     r.vv[i] = lds_tr8(&sV[bn][offV[i]]);
-                    r.gm[i] = *reinterpret_cast<const floatx4*>(&sG[bn][16 * (2 * w + i) + 4 * lg]);
+                    r.gm[i] = *reinterpret_cast<const floatx4*>(&sGk[bn][16 * (2 * w + i) + 4 * lg]);
                 }
                 return r;
             };
@@ -1199,7 +1252,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int mt = 2 * ow + i, tok = 16 * mt + l16;
-                    const float gm = sG[b][tok];
+                    const float gm = sGq[b][tok];
                     floatx4 oq = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int kk = 0; kk < NKD; ++kk)
@@ -1249,10 +1302,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 }
 
 // One workgroup per CU (its LDS), so two waves per SIMD: the register budget is that of two waves.
-template <int DK, bool SNAP = false>
+template <int DK, bool SNAP = false, bool NORM = false>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_bf16(Params p) {
     __shared__ ChainLds<DK> lds;
-    state_chain_bf16<DK, false, false, SNAP>(p, blockIdx.x, lds);
+    state_chain_bf16<DK, false, false, SNAP, NORM>(p, blockIdx.x, lds);
 }
 
 // ------------------------------------------------------------------ bf16 chunk terms
@@ -1269,9 +1322,10 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
 // substitution with the rows of A in registers; its off-diagonal blocks one
 // block diagonal at a time by fp32 MFMA block products; the fragments of W and
 // P' from a bf16 copy of T.
-template <int DK, int W>
+template <int DK, int W, bool NORM>
 __device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, const double* sGl, const float* sB,
-                                            int l16, int lg, floatx4 (&ablk)[3], floatx4 (&pblk)[3]) {
+                                            const float* sSk, const float* sSq, int l16, int lg, floatx4 (&ablk)[3],
+                                            floatx4 (&pblk)[3]) {
     constexpr int NCH = DK / 8, NKD = DK / 32;
     // lower 16x16 blocks (bi, bj): KK^T takes entries W, W+4, ..; QK^T entries (W+2)%4, ..
     constexpr int BI[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
@@ -1303,6 +1357,7 @@ __device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, 
         for (int e = 0; e < 4; ++e) {
             const int r = 16 * bi + 4 * lg + e;
             const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - gi));
+            if constexpr (NORM) acc[e] *= sSk[r] * sSk[i];
             ablk[j][e] = r > i ? sB[r] * gam * acc[e] : 0.f;
         }
     }
@@ -1318,6 +1373,7 @@ __device__ __forceinline__ void gram_blocks(const bf16_t* sK, const bf16_t* sQ, 
         for (int e = 0; e < 4; ++e) {
             const int r = 16 * bi + 4 * lg + e;
             const float gam = __builtin_amdgcn_exp2f((float)(sGl[r] - gi));
+            if constexpr (NORM) acc[e] *= sSq[r] * sSk[i];
             pblk[j][e] = r >= i ? gam * acc[e] : 0.f;
         }
     }
@@ -1350,6 +1406,7 @@ template <int DK> struct TermsLds {
     double sGl[CH];
     __attribute__((aligned(16))) float sB[CH];
     __attribute__((aligned(16))) float sD[CH];
+    float sSk[CH], sSq[CH];   // reciprocal row lengths of K and Q (PRE_L2)
 };
 
 // Chunk terms of work item gi = chunk slot * H + head, by the 4 waves whose
@@ -1358,7 +1415,7 @@ template <int DK> struct TermsLds {
 // result is stored with cache-bypassing stores, then the slot's flag is set to
 // the call's epoch; and the item's V rows, which only the chain reads, are
 // copied into vsink (LDS nobody reads) so that they wait in L2 for the chain.
-template <int DK, bool FUSED>
+template <int DK, bool FUSED, bool NORM>
 __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi, TermsLds<DK>& lds, const int tid,
                                                  const bool store, bf16_t* vsink = nullptr) {
     constexpr int NCH = DK / 8;     // 16-byte chunks per K/Q row
@@ -1392,6 +1449,8 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     double* sGl = lds.sGl;
     float* sB = lds.sB;
     float* sD = lds.sD;
+    float* sSk = lds.sSk;
+    float* sSq = lds.sSq;
     bf16_t* sK = reinterpret_cast<bf16_t*>(r0);
     bf16_t* sQ = sK + TILE;
     float(*sA)[PA] = reinterpret_cast<float(*)[PA]>(r0);
@@ -1420,8 +1479,12 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     }
     if (wave == 0) {
         // prefix sums of g in log2 units, fp64; padded rows: no decay, no write
-        const float gv = lane < n ? p.g[(t0 + lane) * H + h] : 0.f;
-        const float bv = lane < n ? p.beta[(t0 + lane) * H + h] : 0.f;
+        float gv = lane < n ? p.g[(t0 + lane) * H + h] : 0.f;
+        float bv = lane < n ? p.beta[(t0 + lane) * H + h] : 0.f;
+        if ((p.pre & PRE_GATES) && lane < n) {
+            gv = gate_g(gv);
+            bv = gate_beta(bv);
+        }
         double x = (double)gv * 1.4426950408889634;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
@@ -1434,13 +1497,43 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
         sB[lane] = bv;
         sD[lane] = dec;
         if (store) {
-            const auto rg = rsrc(p.wsG + slot * 2 * CH, 2 * CH * 4);
+            const auto rg = rsrc(p.wsG + slot * GS, GS * 4);
             bstore4<AUX>(__builtin_amdgcn_exp2f((float)x), rg, lane * 4);
             bstore4<AUX>(dec, rg, (CH + lane) * 4);
         }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if constexpr (NORM) {
+        // reciprocal row lengths: 4 lanes per row, each summing 4 of its 16-byte pieces (in any order)
+        const int r = tid >> 2, part = tid & 3;
+        float sk = 0.f, sq = 0.f;
+#pragma unroll
+        for (int j = 0; j < NCH / 4; ++j) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(sK + r * DK + 8 * (NCH / 4 * part + j));
+            const bf16x8 b = *reinterpret_cast<const bf16x8*>(sQ + r * DK + 8 * (NCH / 4 * part + j));
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                sk += (float)a[e] * (float)a[e];
+                sq += (float)b[e] * (float)b[e];
+            }
+        }
+        sk += __shfl_xor(sk, 1, 64);
+        sk += __shfl_xor(sk, 2, 64);
+        sq += __shfl_xor(sq, 1, 64);
+        sq += __shfl_xor(sq, 2, 64);
+        if (part == 0) {
+            sSk[r] = r < n ? 1.f / sqrtf(sk + L2_EPS) : 0.f;
+            sSq[r] = r < n ? 1.f / sqrtf(sq + L2_EPS) : 0.f;
+        }
+        __syncthreads();
+        if (store && tid < CH) {   // the chain's decays for K S^T and Q S^T: gamma s_k, gamma s_q
+            const auto rg = rsrc(p.wsG + slot * GS, GS * 4);
+            const float gam = __builtin_amdgcn_exp2f((float)sGl[tid]);
+            bstore4<AUX>(gam * sSk[tid], rg, (2 * CH + tid) * 4);
+            bstore4<AUX>(gam * sSq[tid], rg, (3 * CH + tid) * 4);
+        }
+    }
     if constexpr (FUSED) {   // V rows of the item into L2 (waited for before the flag is set)
         const int DV = p.DV, vch = DV / 8, vrpi = 64 / vch;
         const auto rv = rsrc(reinterpret_cast<const bf16_t*>(p.v) + (t0 * H + h) * DV,
@@ -1452,10 +1545,10 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     // token-token blocks, all operands in registers
     floatx4 ablk[3], pblk[3];
     switch (wave) {
-        case 0: gram_blocks<DK, 0>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
-        case 1: gram_blocks<DK, 1>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
-        case 2: gram_blocks<DK, 2>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
-        default: gram_blocks<DK, 3>(sK, sQ, sGl, sB, l16, lg, ablk, pblk); break;
+        case 0: gram_blocks<DK, 0, NORM>(sK, sQ, sGl, sB, sSk, sSq, l16, lg, ablk, pblk); break;
+        case 1: gram_blocks<DK, 1, NORM>(sK, sQ, sGl, sB, sSk, sSq, l16, lg, ablk, pblk); break;
+        case 2: gram_blocks<DK, 2, NORM>(sK, sQ, sGl, sB, sSk, sSq, l16, lg, ablk, pblk); break;
+        default: gram_blocks<DK, 3, NORM>(sK, sQ, sGl, sB, sSk, sSq, l16, lg, ablk, pblk); break;
     }
     __syncthreads();   // every tile read done: A, P and T take the space over
     switch (wave) {
@@ -1525,8 +1618,8 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     const auto rP = rsrc(reinterpret_cast<bf16_t*>(p.wsP) + slot * tp_elems<bf16_t>(), tp_elems<bf16_t>() * 2);
     for (int f = wave; f < NFRAG; f += 4) {
         const int mt = frag_mt(f), kk2 = frag_kk(f), r = 16 * mt + l16;
-        // W fragment: D_r T[r][tau] beta_tau
-        const float dr = sD[r];
+        // W fragment: D_r T[r][tau] beta_tau (times s_k,r with PRE_L2: the state update takes K unscaled)
+        const float dr = NORM ? sD[r] * sSk[r] : sD[r];
         const floatx4 b0 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 4 * lg]);
         const floatx4 b1 = *reinterpret_cast<const floatx4*>(&sB[32 * kk2 + 16 + 4 * lg]);
         const floatx4 zero = {0.f, 0.f, 0.f, 0.f};   // blocks of T above the diagonal
@@ -1560,10 +1653,10 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     }
 }
 
-template <int DK>
+template <int DK, bool NORM = false>
 __global__ __launch_bounds__(NT, 3) void k_chunk_terms_bf16(Params p) {
     __shared__ TermsLds<DK> lds;
-    chunk_terms_bf16<DK, false>(p, blockIdx.x, lds, threadIdx.x, true);
+    chunk_terms_bf16<DK, false, NORM>(p, blockIdx.x, lds, threadIdx.x, true);
 }
 
 // One launch for the whole bf16 prefill: workgroups [0, npw) form chunk terms
@@ -1571,7 +1664,7 @@ __global__ __launch_bounds__(NT, 3) void k_chunk_terms_bf16(Params p) {
 // in chunk order), the rest are chain workgroups.  The chunk-terms workgroups
 // are dispatched first and never wait, so the chain workgroups' waits end
 // whatever number of workgroups the device holds at once.
-template <int DK, bool SNAP = false>
+template <int DK, bool SNAP = false, bool NORM = false>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_prefill_fused_bf16(Params p) {
     static_assert(NT_CHAIN == 2 * NT, "two work items per chunk-terms workgroup");
     __shared__ union Lds {
@@ -1595,19 +1688,21 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
                 const long j = min(k + half, items - 1);
                 const int c = (int)(j / ((long)p.n_seq * hu)), r = (int)((j / hu) % p.n_seq), u = (int)(j % hu);
                 const long gi = ((long)r * p.NC + c) * H + h0 + 8 * u;
-                chunk_terms_bf16<DK, true>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items, lds.t[half].vsink);
+                chunk_terms_bf16<DK, true, NORM>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items,
+                                                 lds.t[half].vsink);
                 __syncthreads();   // the next item reuses the LDS
             }
         } else {
             const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
             for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
                 const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
-                chunk_terms_bf16<DK, true>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items, lds.t[half].vsink);
+                chunk_terms_bf16<DK, true, NORM>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items,
+                                                 lds.t[half].vsink);
                 __syncthreads();   // the next item reuses the LDS
             }
         }
     } else {
-        state_chain_bf16<DK, true, false, SNAP>(p, blockIdx.x - p.npw, lds.c);
+        state_chain_bf16<DK, true, false, SNAP, NORM>(p, blockIdx.x - p.npw, lds.c);
     }
 }
 
@@ -1619,7 +1714,7 @@ __global__ __launch_bounds__(NT) void k_decode_step(const IO* __restrict__ q, co
                                                     const IO* __restrict__ v, const float* __restrict__ g,
                                                     const float* __restrict__ beta, float* __restrict__ S,
                                                     IO* __restrict__ o, int H, int HK, int DV, int rows_per_wg,
-                                                    float scale) {
+                                                    float scale, int pre) {
     constexpr int LPR = DK / 4;        // lanes per row
     constexpr int RPP = NT / LPR;      // rows per pass of the workgroup
     const int bh = blockIdx.y;                                 // sequence * H + head
@@ -1629,10 +1724,26 @@ __global__ __launch_bounds__(NT) void k_decode_step(const IO* __restrict__ q, co
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         kv[e] = to_f(k[bk * DK + 4 * sub + e]);
-        qv[e] = scale * to_f(q[bk * DK + 4 * sub + e]);
+        qv[e] = to_f(q[bk * DK + 4 * sub + e]);
     }
-    const float a = expf(g[bh]);
-    const float b = beta[bh];
+    float sq = scale;
+    if (pre & PRE_L2) {   // unit rows: the LPR lanes of a row hold all of k and q
+        float kk = kv[0] * kv[0] + kv[1] * kv[1] + kv[2] * kv[2] + kv[3] * kv[3];
+        float qq = qv[0] * qv[0] + qv[1] * qv[1] + qv[2] * qv[2] + qv[3] * qv[3];
+#pragma unroll
+        for (int m = LPR / 2; m >= 1; m >>= 1) {
+            kk += __shfl_xor(kk, m, 64);
+            qq += __shfl_xor(qq, m, 64);
+        }
+        const float sk = 1.f / sqrtf(kk + L2_EPS);
+        sq *= 1.f / sqrtf(qq + L2_EPS);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kv[e] *= sk;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) qv[e] *= sq;
+    const float a = expf((pre & PRE_GATES) ? gate_g(g[bh]) : g[bh]);
+    const float b = (pre & PRE_GATES) ? gate_beta(beta[bh]) : beta[bh];
     const int r0 = blockIdx.x * rows_per_wg;
     const int r1 = min(r0 + rows_per_wg, DV);
     for (int r = r0 + tid / LPR; r < r1; r += RPP) {
@@ -1945,16 +2056,16 @@ struct ChainAlt {
     int first;
 };
 
-template <int DK>
+template <int DK, bool NORM = false>
 __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_pair_bf16(Params p,
                                                                                                          ChainAlt a) {
     __shared__ ChainLds<DK> lds;
     const int bid = blockIdx.x;
     if (bid >= a.first) {
         p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV;
-        state_chain_bf16<DK, false, true>(p, bid - a.first, lds);
+        state_chain_bf16<DK, false, true, false, NORM>(p, bid - a.first, lds);
     } else {
-        state_chain_bf16<DK, false>(p, bid, lds);
+        state_chain_bf16<DK, false, false, false, NORM>(p, bid, lds);
     }
 }
 
@@ -1994,7 +2105,7 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     const size_t per = (size_t)L->slots * H;
     L->meta = 0;
     L->G = n_seqs > 0 ? round_up(((size_t)4 * (n_seqs + 1) + 2 * (size_t)(cpt + 2)) * sizeof(int32_t), 256) : 0;
-    L->T = L->G + round_up(per * 2 * CH * sizeof(float), 256);
+    L->T = L->G + round_up(per * GS * sizeof(float), 256);
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
     L->F = L->P + round_up(per * tp * esz, 256);
@@ -2030,8 +2141,9 @@ uint64_t next_epoch() {
     return (salt << 32) | (uint32_t)(++counter);
 }
 
-template <typename IO, int DK, bool SNAP = false>
+template <typename IO, int DK, bool SNAP = false, bool NORM = false>
 void launch_prefill(Params p, long slots, hipStream_t st) {
+    static_assert(!(SNAP && NORM), "snapshot calls take no input transforms");
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
                            p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
@@ -2048,19 +2160,20 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
             p.xcd_items = !p.ragged && p.H % 8 == 0 && p.npw >= 8;
             if (p.xcd_items) p.npw &= ~7;
             p.epoch = next_epoch();
-            hipLaunchKernelGGL((k_prefill_fused_bf16<DK, SNAP>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0, st, p);
+            hipLaunchKernelGGL((k_prefill_fused_bf16<DK, SNAP, NORM>), dim3((unsigned)(p.npw + nchain)), dim3(NT_CHAIN), 0,
+                               st, p);
             return;
         }
     }
     if (slots > 0 && p.T > 0) {
         if constexpr (sizeof(IO) == 2)
-            hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+            hipLaunchKernelGGL((k_chunk_terms_bf16<DK, NORM>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
         else
             hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     }
     const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
     if constexpr (sizeof(IO) == 2)
-        hipLaunchKernelGGL((k_state_chain_bf16<DK, SNAP>), grid, dim3(NT_CHAIN), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain_bf16<DK, SNAP, NORM>), grid, dim3(NT_CHAIN), 0, st, p);
     else
         hipLaunchKernelGGL((k_state_chain<DK, SNAP>), grid, dim3(NT), 0, st, p);
 }
@@ -2164,14 +2277,14 @@ SegPlan plan_for_call(int B, int T, int H, int dk, int dv, int n_seqs, int io, s
     return sp;
 }
 
-template <typename IO, int DK>
+template <typename IO, int DK, bool NORM = false>
 void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st) {
     const long nseg = (long)sq.nseq * sq.P;
     const long per_seg = (long)sq.H * std::max(sq.DV, DK) * DK / 4;   // float4s of one segment's initial states
     hipLaunchKernelGGL((k_segment_prep<DK>), dim3((unsigned)((per_seg + NT - 1) / NT), (unsigned)(nseg + 1)), dim3(NT), 0,
                        st, sq);
     if constexpr (sizeof(IO) == 2)
-        hipLaunchKernelGGL((k_chunk_terms_bf16<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_chunk_terms_bf16<DK, NORM>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     else
         hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     ChainAlt a;
@@ -2179,7 +2292,7 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
     a.first = (int)(nseg * p.H * (p.DV / SL));
     const dim3 grid((unsigned)(a.first + nseg * p.H * (DK / SL)));
     if constexpr (sizeof(IO) == 2)
-        hipLaunchKernelGGL((k_state_chain_pair_bf16<DK>), grid, dim3(NT_CHAIN), 0, st, p, a);
+        hipLaunchKernelGGL((k_state_chain_pair_bf16<DK, NORM>), grid, dim3(NT_CHAIN), 0, st, p, a);
     else
         hipLaunchKernelGGL((k_state_chain_pair<DK>), grid, dim3(NT), 0, st, p, a);
     const long units = (long)sq.nseq * sq.H;   // (sequence, head) pairs, each on one XCD
@@ -2192,11 +2305,11 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
 
 template <typename IO, int DK>
 void launch_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
-                   float* S, void* o, int B, int H, int HK, int dv, float scale, hipStream_t st) {
+                   float* S, void* o, int B, int H, int HK, int dv, float scale, int pre, hipStream_t st) {
     const int rows_per_wg = 32;
     dim3 grid((dv + rows_per_wg - 1) / rows_per_wg, B * H);
     hipLaunchKernelGGL((k_decode_step<IO, DK>), grid, dim3(NT), 0, st, (const IO*)q, (const IO*)k,
-                       (const IO*)v, g, beta, S, (IO*)o, H, HK, dv, rows_per_wg, scale);
+                       (const IO*)v, g, beta, S, (IO*)o, H, HK, dv, rows_per_wg, scale, pre);
 }
 
 }  // namespace
@@ -2254,8 +2367,9 @@ extern "C" int gdn_set_prefill_segments(int segments) {
 // The prefill behind both entry points: snap_every = 0 takes no snapshots.
 static gdn_status prefill(const void* q, const void* k, const void* v, const float* g, const float* beta,
                           const float* S0, void* o, float* S_T, int B, int T, int H, int HK, int dk, int dv, int chunk,
-                          const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int snap_every,
+                          const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int pre, int snap_every,
                           float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
+    if (pre & ~(PRE_L2 | PRE_GATES)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", pre);
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1 || T < 0) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d T=%d out of range", B, H, T);
@@ -2313,6 +2427,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.npw = 0;
     p.xcd_items = 0;
     p.scale = scale;
+    p.pre = pre;
     p.snaps = snaps;
     p.snap_every = snap_every;
     p.n_snap = snap_every > 0 ? (T - 1) / (snap_every * CH) : 0;
@@ -2353,9 +2468,12 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
         r.wsT = ws + S.base.T;
         r.wsP = ws + S.base.P;
         r.flags = reinterpret_cast<uint64_t*>(ws + S.base.F);
+        const bool norm = pre & PRE_L2;
         if (io_dtype == GDN_BF16) {
-            if (dk == 128) launch_segmented<bf16_t, 128>(r, sq, S.base.slots, hs);
-            else launch_segmented<bf16_t, 64>(r, sq, S.base.slots, hs);
+            if (dk == 128) norm ? launch_segmented<bf16_t, 128, true>(r, sq, S.base.slots, hs)
+                                : launch_segmented<bf16_t, 128>(r, sq, S.base.slots, hs);
+            else norm ? launch_segmented<bf16_t, 64, true>(r, sq, S.base.slots, hs)
+                      : launch_segmented<bf16_t, 64>(r, sq, S.base.slots, hs);
         } else {
             if (dk == 128) launch_segmented<float, 128>(r, sq, S.base.slots, hs);
             else launch_segmented<float, 64>(r, sq, S.base.slots, hs);
@@ -2373,8 +2491,13 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
             else launch_prefill<float, 64, true>(p, L.slots, hs);
         }
     } else if (io_dtype == GDN_BF16) {
-        if (dk == 128) launch_prefill<bf16_t, 128>(p, L.slots, hs);
-        else launch_prefill<bf16_t, 64>(p, L.slots, hs);
+        if (pre & PRE_L2) {
+            if (dk == 128) launch_prefill<bf16_t, 128, false, true>(p, L.slots, hs);
+            else launch_prefill<bf16_t, 64, false, true>(p, L.slots, hs);
+        } else {
+            if (dk == 128) launch_prefill<bf16_t, 128>(p, L.slots, hs);
+            else launch_prefill<bf16_t, 64>(p, L.slots, hs);
+        }
     } else {
         if (dk == 128) launch_prefill<float, 128>(p, L.slots, hs);
         else launch_prefill<float, 64>(p, L.slots, hs);
@@ -2390,7 +2513,7 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
                                         int n_seqs, int io_dtype, float scale, void* workspace,
                                         size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0, 0,
                    nullptr, workspace, workspace_bytes, stream);
 }
 
@@ -2400,8 +2523,18 @@ extern "C" gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, co
                                                 const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale,
                                                 void* workspace, size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0, 0,
                    nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v, const float* g,
+                                           const float* beta, const float* S0, void* o, float* S_T, int B, int T,
+                                           int H, int H_k, int dk, int dv, int chunk, const int32_t* cu_seqlens,
+                                           int n_seqs, int io_dtype, float scale, int flags, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+    g_err[0] = '\0';
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
+                   0, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v, const float* g,
@@ -2417,12 +2550,14 @@ extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, 
         if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
     }
     if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
                    snap_every, snaps, workspace, workspace_bytes, stream);
 }
 
 static gdn_status decode(const void* q, const void* k, const void* v, const float* g, const float* beta, float* S,
-                         void* o, int B, int H, int HK, int dk, int dv, int io_dtype, float scale, void* stream) {
+                         void* o, int B, int H, int HK, int dk, int dv, int io_dtype, float scale, int pre,
+                         void* stream) {
+    if (pre & ~(PRE_L2 | PRE_GATES)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", pre);
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d out of range", B, H);
@@ -2442,11 +2577,11 @@ static gdn_status decode(const void* q, const void* k, const void* v, const floa
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     if (io_dtype == GDN_BF16) {
-        if (dk == 128) launch_decode<bf16_t, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
-        else launch_decode<bf16_t, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
+        if (dk == 128) launch_decode<bf16_t, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, pre, hs);
+        else launch_decode<bf16_t, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, pre, hs);
     } else {
-        if (dk == 128) launch_decode<float, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
-        else launch_decode<float, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, hs);
+        if (dk == 128) launch_decode<float, 128>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, pre, hs);
+        else launch_decode<float, 64>(q, k, v, g, beta, S, o, B, H, HK, dv, scale, pre, hs);
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -2457,12 +2592,19 @@ extern "C" gdn_status gdn_decode_step(const void* q, const void* k, const void* 
                                       const float* beta, float* S, void* o, int B, int H, int dk, int dv,
                                       int io_dtype, float scale, void* stream) {
     g_err[0] = '\0';
-    return decode(q, k, v, g, beta, S, o, B, H, H, dk, dv, io_dtype, scale, stream);
+    return decode(q, k, v, g, beta, S, o, B, H, H, dk, dv, io_dtype, scale, 0, stream);
 }
 
 extern "C" gdn_status gdn_decode_step_grouped(const void* q, const void* k, const void* v, const float* g,
                                               const float* beta, float* S, void* o, int B, int H, int H_k, int dk,
                                               int dv, int io_dtype, float scale, void* stream) {
     g_err[0] = '\0';
-    return decode(q, k, v, g, beta, S, o, B, H, H_k, dk, dv, io_dtype, scale, stream);
+    return decode(q, k, v, g, beta, S, o, B, H, H_k, dk, dv, io_dtype, scale, 0, stream);
+}
+
+extern "C" gdn_status gdn_decode_step_ex(const void* q, const void* k, const void* v, const float* g,
+                                         const float* beta, float* S, void* o, int B, int H, int H_k, int dk, int dv,
+                                         int io_dtype, float scale, int flags, void* stream) {
+    g_err[0] = '\0';
+    return decode(q, k, v, g, beta, S, o, B, H, H_k, dk, dv, io_dtype, scale, flags, stream);
 }

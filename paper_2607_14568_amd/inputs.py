@@ -81,12 +81,15 @@ def _l2n(x: np.ndarray) -> np.ndarray:
 
 
 def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
-                 lengths=None, ragged=0, len_range=(512, 4096), H_k=None):
+                 lengths=None, ragged=0, len_range=(512, 4096), H_k=None, raw=False):
     """Dense (B,T) or ragged (``ragged`` sequences, or explicit ``lengths``) inputs.
 
     Returns a dict of CPU torch tensors: q,k [B,T,H_k,dk] (H_k = H unless given)
     and v [B,T,H,dv] in the io dtype; g, beta [B,T,H] fp32; S0 [n_seq,H,dv,dk]
-    fp32 or None; cu_seqlens int32 [n_seq+1] or None.
+    fp32 or None; cu_seqlens int32 [n_seq+1] or None.  ``raw``: the same draws
+    before the recipe's last steps -- q, k not scaled to unit length, and g, beta
+    holding the logits a = N(0,1) + g_shift, b = N(0,1) (for the entry points that
+    take GDN_QK_L2NORM and GDN_GATE_LOGITS).
     """
     H_k = H if H_k is None else H_k
     rng = np.random.default_rng(seed)
@@ -100,11 +103,17 @@ def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
         n_seq = len(lengths)
     else:
         n_seq = B
-    q = _l2n(rng.standard_normal((B, T, H_k, dk)))
-    k = _l2n(rng.standard_normal((B, T, H_k, dk)))
+    q = rng.standard_normal((B, T, H_k, dk))
+    k = rng.standard_normal((B, T, H_k, dk))
     v = rng.standard_normal((B, T, H, dv))
-    beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((B, T, H))))
-    g = -np.logaddexp(0.0, rng.standard_normal((B, T, H)) + g_shift)
+    b_logit = rng.standard_normal((B, T, H))
+    a_logit = rng.standard_normal((B, T, H)) + g_shift
+    if raw:
+        beta, g = b_logit, a_logit
+    else:
+        q, k = _l2n(q), _l2n(k)
+        beta = 1.0 / (1.0 + np.exp(-b_logit))
+        g = -np.logaddexp(0.0, a_logit)
     S0 = s0_std * rng.standard_normal((n_seq, H, dv, dk)) if s0_std > 0 else None
     return dict(
         q=_round_io(q, io), k=_round_io(k, io), v=_round_io(v, io),
@@ -115,19 +124,25 @@ def make_prefill(B, T, H, dk, dv, io="f32", seed=0, s0_std=0.0, g_shift=0.0,
     )
 
 
-def make_decode(B, H, dk, dv, io="f32", seed=0, s0_std=0.02, pool=16, H_k=None):
+def make_decode(B, H, dk, dv, io="f32", seed=0, s0_std=0.02, pool=16, H_k=None, raw=False):
     """Decode inputs: a pool of ``pool`` tokens per sequence, cycled by step index.
 
     Returns q,k [pool,B,H_k,dk] (H_k = H unless given), v [pool,B,H,dv] (io
-    dtype); g, beta [pool,B,H] fp32; S [B,H,dv,dk] fp32.
+    dtype); g, beta [pool,B,H] fp32; S [B,H,dv,dk] fp32.  ``raw`` as make_prefill.
     """
     H_k = H if H_k is None else H_k
     rng = np.random.default_rng(seed)
-    q = _l2n(rng.standard_normal((pool, B, H_k, dk)))
-    k = _l2n(rng.standard_normal((pool, B, H_k, dk)))
+    q = rng.standard_normal((pool, B, H_k, dk))
+    k = rng.standard_normal((pool, B, H_k, dk))
     v = rng.standard_normal((pool, B, H, dv))
-    beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((pool, B, H))))
-    g = -np.logaddexp(0.0, rng.standard_normal((pool, B, H)))
+    b_logit = rng.standard_normal((pool, B, H))
+    a_logit = rng.standard_normal((pool, B, H))
+    if raw:
+        beta, g = b_logit, a_logit
+    else:
+        q, k = _l2n(q), _l2n(k)
+        beta = 1.0 / (1.0 + np.exp(-b_logit))
+        g = -np.logaddexp(0.0, a_logit)
     S = s0_std * rng.standard_normal((B, H, dv, dk))
     return dict(q=_round_io(q, io), k=_round_io(k, io), v=_round_io(v, io),
                 g=torch.from_numpy(g.astype(np.float32)),

@@ -246,6 +246,39 @@ def test_binding_grouped_shapes():
         gdn.gdn_decode_step_grouped(x[0], x[0], v[0], g[0], g[0], torch.zeros(1, 4, 64, 64))
 
 
+def _prefill_ex(L, **kw):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=4, Hk=2, dk=64, dv=64, chunk=64,
+             cu=None, n_seqs=0, io=0, scale=1.0, flags=3, ws=A, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return L.gdn_chunk_prefill_ex(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S0"], a["o"], a["ST"],
+                                  a["B"], a["T"], a["H"], a["Hk"], a["dk"], a["dv"], a["chunk"], a["cu"],
+                                  a["n_seqs"], a["io"], a["scale"], a["flags"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(flags=4), INVALID), (dict(flags=-1), INVALID), (dict(flags=8 | 1), INVALID),
+    (dict(Hk=3), INVALID), (dict(dk=96), UNSUPPORTED), (dict(chunk=128), UNSUPPORTED),
+    (dict(q=None), INVALID), (dict(ws_bytes=10), WORKSPACE), (dict(io=7), INVALID),
+])
+def test_ex_prefill_argument_checks(L, kw, code):
+    rc = _prefill_ex(L, **kw)
+    assert rc == code, (kw, rc, L.gdn_last_error_message())
+    assert L.gdn_last_error_message().decode()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(flags=4), INVALID), (dict(flags=-2), INVALID), (dict(Hk=3), INVALID), (dict(dk=100), UNSUPPORTED),
+    (dict(S=None), INVALID),
+])
+def test_ex_decode_argument_checks(L, kw, code):
+    a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=4, Hk=2, dk=128, dv=128, io=0, scale=1.0, flags=1,
+             stream=None)
+    a.update(kw)
+    rc = L.gdn_decode_step_ex(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S"], a["o"], a["B"], a["H"], a["Hk"],
+                              a["dk"], a["dv"], a["io"], a["scale"], a["flags"], a["stream"])
+    assert rc == code, (kw, rc)
+
+
 def _decode(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
     a.update(kw)

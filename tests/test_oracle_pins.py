@@ -361,3 +361,72 @@ def test_grouped_decode_equals_grouped_prefill():
         ot, S = oracle.decode_step_grouped(q[:, t], k[:, t], v[:, t], g[:, t], beta[:, t], S)
         np.testing.assert_allclose(ot, o[:, t], rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(S, ST, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- in-kernel input transforms
+def test_gate_logits_closed_forms():
+    """a = 0 gives alpha = 1/2 exactly; b = 0 gives beta = 1/2; softplus against math.log1p(math.exp(a))."""
+    a = np.array([0.0, -3.5, 2.25, 10.0, -30.0])
+    b = np.array([0.0, 1.0, -2.0, 4.0, -8.0])
+    g, beta = oracle.gates_from_logits(a, b)
+    for ai, gi in zip(a, g):
+        assert abs(gi + math.log1p(math.exp(ai))) < 1e-14 * max(1.0, abs(ai))
+    for bi, be in zip(b, beta):
+        assert abs(be - 1.0 / (1.0 + math.exp(-bi))) < 1e-15
+    assert abs(math.exp(g[0]) - 0.5) < 1e-15 and beta[0] == 0.5
+    # through the recurrence: logits (0, 0) everywhere = alpha = beta = 1/2 given directly
+    q, k, v, _, _, S0 = _rand(51, T=9)
+    z = np.zeros(q.shape[:3])
+    o1, s1 = oracle.recurrence_ex(q, k, v, z, z, S0, gate_logits=True)
+    o2, s2 = oracle.recurrence(q, k, v, z - math.log(2.0), z + 0.5, S0)
+    np.testing.assert_allclose(o1, o2, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(s1, s2, rtol=1e-13, atol=1e-14)
+
+
+def test_l2_transform_against_hand_normalised_rows_and_scale_invariance():
+    rng = np.random.default_rng(52)
+    B, T, H, dk, dv = 1, 10, 2, 6, 3
+    q = 3.0 * rng.standard_normal((B, T, H, dk))
+    k = 0.5 * rng.standard_normal((B, T, H, dk))
+    v = rng.standard_normal((B, T, H, dv))
+    g = -np.logaddexp(0, rng.standard_normal((B, T, H)))
+    beta = 1 / (1 + np.exp(-rng.standard_normal((B, T, H))))
+
+    def unit(x):   # row by row with math.sqrt
+        y = np.empty_like(x)
+        for idx in np.ndindex(x.shape[:-1]):
+            y[idx] = x[idx] / math.sqrt(sum(float(t) * float(t) for t in x[idx]) + 1e-6)
+        return y
+    o1, s1 = oracle.recurrence_ex(q, k, v, g, beta, qk_l2norm=True)
+    o2, s2 = oracle.recurrence(unit(q), unit(k), v, g, beta)
+    np.testing.assert_allclose(o1, o2, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(s1, s2, rtol=1e-12, atol=1e-13)
+    # a positive factor per (token, head) on q or k changes nothing beyond the epsilon's share
+    c = np.exp(rng.uniform(-1, 1, size=(B, T, H, 1)))
+    # (rows here have |x|^2 > 0.09, so the epsilon moves each by under 6e-6 relative)
+    o3, s3 = oracle.recurrence_ex(q * c, k / c, v, g, beta, qk_l2norm=True)
+    np.testing.assert_allclose(o3, o1, rtol=0, atol=1e-4 * np.abs(o1).max())
+    np.testing.assert_allclose(s3, s1, rtol=0, atol=1e-4 * np.abs(s1).max())
+    # a zero key row writes nothing: that token only decays the state
+    k0 = k.copy()
+    k0[0, 4, 1] = 0.0
+    _, sa = oracle.recurrence_ex(q[:, :5], k0[:, :5], v[:, :5], g[:, :5], beta[:, :5], qk_l2norm=True)
+    _, sb = oracle.recurrence_ex(q[:, :4], k0[:, :4], v[:, :4], g[:, :4], beta[:, :4], qk_l2norm=True)
+    np.testing.assert_allclose(sa[0, 1], math.exp(g[0, 4, 1]) * sb[0, 1], rtol=1e-13, atol=1e-15)
+
+
+def test_ex_decode_equals_ex_prefill():
+    rng = np.random.default_rng(53)
+    B, T, H, Hk, dk, dv = 2, 5, 4, 2, 5, 3
+    q = 2.0 * rng.standard_normal((B, T, Hk, dk))
+    k = rng.standard_normal((B, T, Hk, dk))
+    v = rng.standard_normal((B, T, H, dv))
+    a = rng.standard_normal((B, T, H))
+    b = rng.standard_normal((B, T, H))
+    S = 0.1 * rng.standard_normal((B, H, dv, dk))
+    kw = dict(qk_l2norm=True, gate_logits=True)
+    o, ST = oracle.recurrence_ex(q, k, v, a, b, S, **kw)
+    for t in range(T):
+        ot, S = oracle.decode_step_ex(q[:, t], k[:, t], v[:, t], a[:, t], b[:, t], S, **kw)
+        np.testing.assert_allclose(ot, o[:, t], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(S, ST, rtol=1e-12, atol=1e-12)
