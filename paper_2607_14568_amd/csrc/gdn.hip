@@ -321,11 +321,15 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     const long t0 = start + (long)c * CH;
     const int n = min(CH, len - c * CH);
 
-    __shared__ __attribute__((aligned(16))) IO sK[CH][DK + PAD];
-    __shared__ __attribute__((aligned(16))) IO sQ[CH][DK + PAD];
-    __shared__ __attribute__((aligned(16))) float sA[CH][CH + 4];
-    __shared__ __attribute__((aligned(16))) float sTi[CH][CH + 4];
-    __shared__ __attribute__((aligned(16))) float sP[CH][CH + 4];
+    // The K and Q tiles are dead once the token-token products are in registers:
+    // A, T and P take their space (two workgroups fit a CU's LDS).
+    constexpr int SZ_TILES = 2 * CH * (DK + PAD) * (int)sizeof(IO), SZ_MATS = 3 * CH * (CH + 4) * 4;
+    __shared__ __attribute__((aligned(16))) char smem[SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS];
+    IO(*sK)[DK + PAD] = reinterpret_cast<IO(*)[DK + PAD]>(smem);
+    IO(*sQ)[DK + PAD] = sK + CH;
+    float(*sA)[CH + 4] = reinterpret_cast<float(*)[CH + 4]>(smem);
+    float(*sTi)[CH + 4] = sA + CH;
+    float(*sP)[CH + 4] = sTi + CH;
     __shared__ float sZ[4][16][17];
     __shared__ double sG[CH];
     __shared__ float sB[CH], sD[CH], sSk[CH], sSq[CH];
@@ -381,12 +385,19 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
     }
 
-    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P)
-    for (int job = wave; job < 20; job += 4) {
-        const int which = job / 10;
-        int t = job % 10, bi = 0;
+    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P): job = wave + 4 u
+    auto job_block = [](int job, int& which, int& bi, int& bj) {
+        which = job / 10;
+        int t = job % 10;
+        bi = 0;
         while (t > bi) { t -= bi + 1; ++bi; }
-        const int bj = t;
+        bj = t;
+    };
+    floatx4 accs[5];
+#pragma unroll
+    for (int u = 0; u < 5; ++u) {
+        int which, bi, bj;
+        job_block(wave + 4 * u, which, bi, bj);
         const IO(*X)[DK + PAD] = which ? sQ : sK;
         // instruction 4 j + e: lane group lg carries contraction index 16 j + 4 lg + e
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -396,14 +407,21 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], acc, 0, 0, 0);
         }
+        accs[u] = acc;
+    }
+    __syncthreads();   // every tile read done: A and P overwrite them
+#pragma unroll
+    for (int u = 0; u < 5; ++u) {
+        int which, bi, bj;
+        job_block(wave + 4 * u, which, bi, bj);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int r = bi * 16 + 4 * lg + e, i = bj * 16 + l16;
             const float nrm = l2 ? (which ? sSq[r] : sSk[r]) * sSk[i] : 1.f;
             if (which == 0) {
-                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * (nrm * acc[e]) : 0.f;
+                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
             } else {
-                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * (nrm * acc[e]) : 0.f;
+                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
             }
         }
     }
@@ -548,16 +566,17 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
 #pragma unroll
         for (int j = 0; j < NVV; ++j)
             x.v[j] = tid + NT * j < CH * VPV ? ld(rv, vvo + (NT / VPV) * j * H * DV * (int)sizeof(IO)) : make_uint4(0, 0, 0, 0);
+        // (prefetch only: nothing here may read a loaded value, or the wait for it
+        // would also wait for every load issued before)
         if (tid < CH) {
             x.gam = p.wsG[slot * GS + tid];
             x.dec = p.wsG[slot * GS + CH + tid];
-            x.gk = x.gq = x.gam;
             if (p.pre & PRE_L2) {
                 x.gk = p.wsG[slot * GS + 2 * CH + tid];
                 x.gq = p.wsG[slot * GS + 3 * CH + tid];
             }
-            x.beta = tid < n ? p.beta[(t0 + tid) * H + h] : 0.f;
-            if ((p.pre & PRE_GATES) && tid < n) x.beta = gate_beta(x.beta);
+            // padded rows write nothing: beta = 0, or a logit whose sigmoid is 0
+            x.beta = tid < n ? p.beta[(t0 + tid) * H + h] : ((p.pre & PRE_GATES) ? -INFINITY : 0.f);
         }
     };
     auto store = [&](const Pre& x) {
@@ -583,11 +602,12 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) 
             }
         }
         if (tid < CH) {
+            const bool l2 = p.pre & PRE_L2;
             sGam[tid] = x.gam;
             sDec[tid] = x.dec;
-            sBeta[tid] = x.beta;
-            sGk[tid] = x.gk;
-            sGq[tid] = x.gq;
+            sBeta[tid] = (p.pre & PRE_GATES) ? gate_beta(x.beta) : x.beta;
+            sGk[tid] = l2 ? x.gk : x.gam;
+            sGq[tid] = l2 ? x.gq : x.gam;
         }
     };
 
