@@ -96,6 +96,95 @@ def cpu_baseline(w, x, budget_s):
             "sample": sample, "seconds": round(el, 3)}
 
 
+ATTN = {   # causal attention prefill workloads (the backbone's softmax-attention layers): B, T, H, H_kv, d
+    "attn_10k_bf16": (1, 10240, 16, 8, 128),
+    "attn_2k_bf16": (1, 2048, 16, 8, 128),
+}
+
+
+def attention_bench(args):
+    """Causal attention prefill: one gdn_attention_prefill call per step over the whole prompt."""
+    import numpy as np
+    import torch
+    import paper_2607_14568_amd as gdn
+    from paper_2607_14568_amd import inputs as I
+
+    B, T, H, Hkv, d = ATTN[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    x_host = I.make_attention(B, T, H, Hkv, d, seed=1005)
+    sets = []
+    for i in range(max(1, args.sets)):
+        dd = {kk: vv.to(dev) for kk, vv in x_host.items()}
+        if i > 0:
+            dd = {kk: vv.clone() for kk, vv in dd.items()}
+        dd["o"] = torch.empty_like(dd["q"])
+        sets.append(dd)
+    scale = 1.0 / d ** 0.5
+
+    def step(i):
+        dd = sets[i % len(sets)]
+        gdn.gdn_attention_prefill(dd["q"], dd["k"], dd["v"], scale=scale, o=dd["o"])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(args.warmup + i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t0
+    call_ms = [a.elapsed_time(b) for a, b in ev]
+    avg_call_s = sum(call_ms) / len(call_ms) * 1e-3
+    ms_per_step = t_wall * 1e3 / args.steps
+    flops = 2.0 * d * H * B * T * (T + 1)                 # Q K^T and P V over each query's causal prefix
+    byts = B * T * (2 * H + 2 * Hkv) * d * 2              # q, k, v read, o written (bf16)
+    roof = {"bound": "mfma", "achieved": flops / avg_call_s / 1e12, "peak": PEAK["bf16"] / 1e12, "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = "one gdn_attention_prefill call (k_attn_causal)"
+    roof["alg_flops"] = flops
+    roof["alg_bytes"] = byts
+    roof["avg_call_us"] = avg_call_s * 1e6
+    roof["min_call_us"] = min(call_ms) * 1e3
+    out = {
+        "metric": "causal softmax-attention prefill tokens/s (T=%d, H=%d, H_kv=%d, d=%d); %% of roofline" % (T, H, Hkv, d),
+        "value": B * T / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "T": T, "H": H, "H_kv": Hkv, "d": d, "io": "bf16",
+                   "parallelism": "none (1 GPU)", "input_sets": len(sets)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import attention as att
+        f = I.as_f64
+        q, k, v = f(x_host["q"]), f(x_host["k"]), f(x_host["v"])
+        rng = np.random.default_rng(0)
+        done, t0 = 0, time.perf_counter()
+        while True:   # query rows drawn uniformly: their mean cost is the mean cost of a token
+            rows = np.sort(rng.integers(0, T, 32))
+            att.causal_attention(q, k, v, scale, rows=rows)
+            done += len(rows)
+            el = time.perf_counter() - t0
+            if el > args.cpu_budget:
+                break
+        try:   # the threads numpy's BLAS ran the oracle's products on
+            from threadpoolctl import threadpool_info
+            cores = max([pi.get("num_threads", 1) for pi in threadpool_info() if pi.get("user_api") == "blas"] or [1])
+        except Exception:
+            cores = None
+        out["cpu_baseline"] = {"value": done * B / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+                               "sample": "%d query rows drawn uniformly from the %d-token prompt (all %d heads)"
+                                         % (done, T, H), "seconds": round(el, 3)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,6 +203,9 @@ def main():
         print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
               "(the multi-GPU sharding is a design note only)" % args.gpus, file=sys.stderr)
         sys.exit(2)
+
+    if args.workload in ATTN:
+        return attention_bench(args)
 
     import torch
     import paper_2607_14568_amd as gdn

@@ -264,6 +264,27 @@ gdn_status gdn_decode_step_ex(const void* q, const void* k, const void* v,
                               int B, int H, int H_k, int dk, int dv, int io_dtype, float scale,
                               int flags, void* stream);
 
+/*
+ * Causal softmax-attention prefill: the backbone's attention layers over a
+ * prompt (section 5: the scores Q K^T of each head, a softmax over each query's
+ * causal prefix, then the product with V; grouped query heads share a
+ * key/value head).  Per sequence b, head h, query position i:
+ *
+ *     o_i = sum_{j <= i} softmax_j(scale q_i . k_j) v_j     (k, v of head h / (H / H_kv))
+ *
+ *   q, o   [B, T, H, d]     bf16 (io_dtype must be GDN_BF16)
+ *   k, v   [B, T, H_kv, d]  bf16
+ *   d      64 or 128;  1 <= H_kv <= H, H_kv divides H;  T >= 0 (T = 0: nothing to do)
+ *   scale  multiplies q . k (1 / sqrt(d) gives the usual attention)
+ * The score matrix is never stored: the kernel keeps a running softmax per query
+ * (fp32) and needs no workspace.  Errors: GDN_ERR_INVALID_ARG for bad sizes,
+ * null or misaligned (16-byte) pointers or an unknown dtype; GDN_ERR_UNSUPPORTED
+ * for GDN_F32 io or another d.
+ */
+gdn_status gdn_attention_prefill(const void* q, const void* k, const void* v, void* o,
+                                 int B, int T, int H, int H_kv, int d, int io_dtype, float scale,
+                                 void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,7 +18,7 @@ __all__ = [
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
     "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
     "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped", "gdn_chunk_prefill_ex", "gdn_decode_step_ex",
-    "GDN_QK_L2NORM", "GDN_GATE_LOGITS",
+    "GDN_QK_L2NORM", "GDN_GATE_LOGITS", "gdn_attention_prefill",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -69,6 +69,8 @@ def lib():
         L.gdn_decode_step_grouped.restype = I
         L.gdn_decode_step_ex.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P]
         L.gdn_decode_step_ex.restype = I
+        L.gdn_attention_prefill.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P]
+        L.gdn_attention_prefill.restype = I
         _lib = L
     return _lib
 
@@ -273,4 +275,26 @@ def _decode(q, k, v, g, beta, S, scale, o, grouped, flags=None):
     else:
         _check(lib().gdn_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S), _ptr(o),
                                      B, H, dk, dv, io, float(scale), _stream(q.device)))
+    return o
+
+
+def gdn_attention_prefill(q, k, v, *, scale=None, o=None):
+    """Causal softmax attention; see ``gdn_attention_prefill`` in include/gdn.h.
+
+    q [B,T,H,d] and k, v [B,T,H_kv,d] bf16 CUDA tensors; ``scale`` defaults to
+    1/sqrt(d).  Returns o [B,T,H,d] bf16.
+    """
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, torch.bfloat16)
+    B, T, H, d = q.shape
+    Hkv = k.shape[2]
+    if tuple(k.shape) != (B, T, Hkv, d) or v.shape != k.shape:
+        raise ValueError("inconsistent shapes q%s k%s v%s" % (tuple(q.shape), tuple(k.shape), tuple(v.shape)))
+    if o is None:
+        o = torch.empty_like(q)
+    else:
+        _dev(o, "o", torch.bfloat16)
+    sc = float(scale) if scale is not None else 1.0 / float(d) ** 0.5
+    _check(lib().gdn_attention_prefill(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, T, H, Hkv, d, GDN_BF16, sc,
+                                       _stream(q.device)))
     return o

@@ -2096,6 +2096,164 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     state_chain_f32<DK>(p, bid);
 }
 
+// ------------------------------------------------------------------ causal attention prefill
+// The backbone's softmax-attention layers over a prompt (section 5: scores Q K^T
+// per head, a causal softmax, then P V; grouped query heads share a key/value
+// head): per (sequence, head h),
+//     o_i = sum_{j <= i} softmax_j(scale q_i . k_j) v_j,   key/value head h / (H / H_kv).
+// One workgroup per (sequence, head, block of AQ queries), 8 waves of 16 queries;
+// blocks of AKB keys and values stream through a double-buffered LDS ring (16-byte
+// chunks XOR-swizzled by row) up to the causal diagonal.  Per key block a wave
+// forms S^T = K Q^T (its Q^T operands held in registers), the running softmax of
+// each query column in fp32 (max and sum across the lane groups by shuffles),
+// and O^T += V^T P^T: the exponentiated S^T accumulators are the B operand as
+// they stand (contraction over keys in the order 32 kk + 16 (j / 4) + 4 lg + j % 4),
+// and the V^T operands come from transpose LDS reads in that order.  The full
+// score matrix never exists; the work skips key blocks past a wave's last query.
+constexpr int AQ = 128, AKB = 64, NT_ATT = 512;
+
+struct AttnParams {
+    const bf16_t* q;
+    const bf16_t* k;
+    const bf16_t* v;
+    bf16_t* o;
+    int B, T, H, HKV;
+    int nqb;            // query blocks per sequence
+    float scale_log2;   // scale * log2(e)
+};
+
+template <int DH> struct AttnLds {
+    bf16_t k[2][AKB * DH];
+    bf16_t v[2][AKB * DH];
+};
+
+template <int DH>
+__global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
+    constexpr int NCH = DH / 8;         // 16-byte chunks per row
+    constexpr int RPI = 64 / NCH;       // rows per 1 KB copy
+    constexpr int NKB = DH / 32;        // contraction blocks over the head dimension
+    constexpr int NDT = DH / 16;        // 16-row tiles of O^T
+    constexpr int NCP = 2 * AKB / RPI;  // 1 KB copies per key block (K and V)
+    __shared__ AttnLds<DH> lds;
+    const int BH = p.B * p.H;
+    const int qb = p.nqb - 1 - (int)(blockIdx.x / BH);   // blocks with the most keys first
+    const int bh = (int)(blockIdx.x % BH);
+    const int b = bh / p.H, h = bh % p.H, hk = h / (p.H / p.HKV);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int T = p.T;
+    const int q0 = qb * AQ, qw = q0 + 16 * wave;   // the workgroup's and this wave's first query
+    const long rsq = (long)p.H * DH, rsk = (long)p.HKV * DH;   // row strides (elements)
+    const bf16_t* qbase = p.q + ((long)b * T * p.H + h) * DH;
+    const bf16_t* kbase = p.k + ((long)b * T * p.HKV + hk) * DH;
+    const bf16_t* vbase = p.v + ((long)b * T * p.HKV + hk) * DH;
+    auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
+    auto kq = [](int r, int cc) { return r * DH + (((cc >> 3) ^ (((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1))) << 3) + (cc & 7); };
+    // descriptor over rows [r0, min(r0 + n, T)) of a [T][heads][DH] tensor; rows past T read as zeros
+    auto rows_rsrc = [&](const bf16_t* base, long rs, int r0, int n) {
+        const int m = min(n, T - r0);
+        return rsrc(base + (long)r0 * rs, m > 0 ? (uint32_t)(((long)(m - 1) * rs + DH) * 2) : 0u);
+    };
+
+    // Q^T operand: lane holds q[qw + l16][32 kb + 8 lg .. + 7]
+    bf16x8 qf[NKB];
+    {
+        const auto rq = rows_rsrc(qbase, rsq, qw, 16);
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) qf[kb] = bload16(rq, (int)((l16 * rsq + 32 * kb + 8 * lg) * 2));
+    }
+    // copies of key block j into ring slot j & 1: copy c < NCP / 2 is K rows RPI c .., the rest V
+    const int nkb = min((T + AKB - 1) / AKB, (q0 + AQ) / AKB);
+    auto issue = [&](int j) {
+        const int kb0 = j * AKB, sl = j & 1;
+        const auto rk = rows_rsrc(kbase, rsk, kb0, AKB);
+        const auto rv = rows_rsrc(vbase, rsk, kb0, AKB);
+#pragma unroll
+        for (int c = wave; c < NCP; c += NT_ATT / 64) {
+            const int cc = c % (NCP / 2), r = RPI * cc + lane / NCH;
+            const int off = (int)((r * rsk + (((lane % NCH) ^ swz(r)) << 3)) * 2);
+            if (c < NCP / 2) bdma16(rk, &lds.k[sl][RPI * cc * DH], off);
+            else bdma16(rv, &lds.v[sl][RPI * cc * DH], off);
+        }
+    };
+    float m = -INFINITY, l = 0.f;   // running max (log2 units) and sum of query qw + l16
+    floatx4 oacc[NDT];
+#pragma unroll
+    for (int t = 0; t < NDT; ++t) oacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (nkb > 0) issue(0);
+    for (int j = 0; j < nkb; ++j) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of block j
+        lds_barrier();                                       // everyone's; slot (j + 1) & 1 no longer read
+        if (j + 1 < nkb) issue(j + 1);
+        const int kb0 = j * AKB;
+        if (kb0 > qw + 15) continue;   // every key of the block follows this wave's queries
+        const bf16_t* sk = lds.k[j & 1];
+        const bf16_t* sv = lds.v[j & 1];
+        floatx4 st[4];   // S^T: keys 16 t + 4 lg + e, query l16
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            st[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+                st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(&sk[kq(16 * t + l16, 32 * kb + 8 * lg)]), qf[kb], st[t], 0, 0, 0);
+        }
+        const int qi = qw + l16;
+        const bool diag = kb0 + AKB - 1 > qw || kb0 + AKB > T;   // some key of the block is masked
+        float bm = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float x = st[t][e] * p.scale_log2;
+                if (diag) {
+                    const int kj = kb0 + 16 * t + 4 * lg + e;
+                    if (kj > qi || kj >= T) x = -INFINITY;
+                }
+                st[t][e] = x;
+                bm = fmaxf(bm, x);
+            }
+        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+        const float mn = fmaxf(m, bm);   // finite: block 0 holds key 0 <= every query
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);
+        float ls = 0.f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                st[t][e] = __builtin_amdgcn_exp2f(st[t][e] - mn);
+                ls += st[t][e];
+            }
+        ls += __shfl_xor(ls, 16, 64);
+        ls += __shfl_xor(ls, 32, 64);
+        l = l * alpha + ls;
+        m = mn;
+        const bf16x8 pf0 = pack_bf16(st[0], st[1]), pf1 = pack_bf16(st[2], st[3]);
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) {
+            oacc[t] *= alpha;
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int r = 32 * kk + 4 * lg + (l16 >> 2), c = 16 * t + 4 * (l16 & 3);
+                const bf16x8 va = join4(lds_tr8(&sv[kq(r, c)]), lds_tr8(&sv[kq(r + 16, c)]));
+                oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, kk ? pf1 : pf0, oacc[t], 0, 0, 0);
+            }
+        }
+    }
+    // o[qw + l16][16 t + 4 lg + e] = O^T / l
+    const int qi = qw + l16;
+    if (qi < T) {
+        const float inv = 1.f / l;
+        bf16_t* orow = p.o + (((long)b * T + qi) * p.H + h) * DH;
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) {
+            const floatx4 ov = oacc[t] * inv;
+            *reinterpret_cast<bf16x4*>(orow + 16 * t + 4 * lg) = __builtin_convertvector(ov, bf16x4);
+        }
+    }
+}
+
 // ------------------------------------------------------------------ host side
 thread_local char g_err[512] = "";
 
@@ -2330,6 +2488,11 @@ void launch_decode(const void* q, const void* k, const void* v, const float* g, 
     dim3 grid((dv + rows_per_wg - 1) / rows_per_wg, B * H);
     hipLaunchKernelGGL((k_decode_step<IO, DK>), grid, dim3(NT), 0, st, (const IO*)q, (const IO*)k,
                        (const IO*)v, g, beta, S, (IO*)o, H, HK, dv, rows_per_wg, scale, pre);
+}
+
+template <int DH>
+void launch_attention(AttnParams a, hipStream_t st) {
+    hipLaunchKernelGGL((k_attn_causal<DH>), dim3((unsigned)((long)a.nqb * a.B * a.H)), dim3(NT_ATT), 0, st, a);
 }
 
 }  // namespace
@@ -2627,4 +2790,40 @@ extern "C" gdn_status gdn_decode_step_ex(const void* q, const void* k, const voi
                                          int io_dtype, float scale, int flags, void* stream) {
     g_err[0] = '\0';
     return decode(q, k, v, g, beta, S, o, B, H, H_k, dk, dv, io_dtype, scale, flags, stream);
+}
+
+extern "C" gdn_status gdn_attention_prefill(const void* q, const void* k, const void* v, void* o, int B, int T, int H,
+                                            int H_kv, int d, int io_dtype, float scale, void* stream) {
+    g_err[0] = '\0';
+    if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
+        return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
+    if (B < 1 || T < 0 || H < 1) return fail(GDN_ERR_INVALID_ARG, "B=%d T=%d H=%d out of range", B, T, H);
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0)
+        return fail(GDN_ERR_INVALID_ARG, "H_kv=%d key/value heads must divide the H=%d query heads", H_kv, H);
+    if (d < 1) return fail(GDN_ERR_INVALID_ARG, "d=%d must be positive", d);
+    if (d != 64 && d != 128) return fail(GDN_ERR_UNSUPPORTED, "d=%d: only 64 and 128 are implemented", d);
+    if (io_dtype != GDN_BF16) return fail(GDN_ERR_UNSUPPORTED, "attention is implemented for bf16 io only");
+    if (T > 0 && (!q || !k || !v || !o)) return fail(GDN_ERR_INVALID_ARG, "q, k, v and o must be non-null");
+    const void* ptrs[] = {q, k, v, o};
+    for (const void* ptr : ptrs)
+        if (ptr && !aligned(ptr, 16)) return fail(GDN_ERR_INVALID_ARG, "tensor pointer %p is not 16-byte aligned", ptr);
+    if ((long)H * d > (1L << 20)) return fail(GDN_ERR_UNSUPPORTED, "H=%d too large", H);
+    const long nqb = ((long)T + AQ - 1) / AQ;
+    if (nqb * B * H >= (1L << 31)) return fail(GDN_ERR_UNSUPPORTED, "B*T*H too large");
+    if (T == 0) return GDN_OK;
+    AttnParams a;
+    a.q = static_cast<const bf16_t*>(q);
+    a.k = static_cast<const bf16_t*>(k);
+    a.v = static_cast<const bf16_t*>(v);
+    a.o = static_cast<bf16_t*>(o);
+    a.B = B; a.T = T; a.H = H; a.HKV = H_kv;
+    a.nqb = (int)nqb;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    if (d == 128) launch_attention<128>(a, hs);
+    else launch_attention<64>(a, hs);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
 }

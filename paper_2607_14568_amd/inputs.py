@@ -150,6 +150,16 @@ def make_decode(B, H, dk, dv, io="f32", seed=0, s0_std=0.02, pool=16, H_k=None, 
                 S=torch.from_numpy(S.astype(np.float32)))
 
 
+def make_attention(B, T, H, H_kv, d, seed=0):
+    """Attention inputs: q [B,T,H,d], k and v [B,T,H_kv,d], entries N(0,1), bf16."""
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((B, T, H, d), dtype=np.float32)
+    k = rng.standard_normal((B, T, H_kv, d), dtype=np.float32)
+    v = rng.standard_normal((B, T, H_kv, d), dtype=np.float32)
+    return dict(q=torch.from_numpy(q).to(torch.bfloat16), k=torch.from_numpy(k).to(torch.bfloat16),
+                v=torch.from_numpy(v).to(torch.bfloat16))
+
+
 def make_workload(name: str):
     w = WORKLOADS[name]
     if w.decode:

@@ -279,6 +279,25 @@ def test_ex_decode_argument_checks(L, kw, code):
     assert rc == code, (kw, rc)
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(io=2), INVALID), (dict(io=0), UNSUPPORTED), (dict(B=0), INVALID), (dict(T=-1), INVALID),
+    (dict(H=0), INVALID), (dict(Hkv=0), INVALID), (dict(Hkv=3), INVALID), (dict(Hkv=8), INVALID),
+    (dict(d=0), INVALID), (dict(d=96), UNSUPPORTED), (dict(d=256), UNSUPPORTED),
+    (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(k=A + 8), INVALID), (dict(v=A + 2), INVALID),
+    (dict(H=1 << 14), UNSUPPORTED),
+])
+def test_attention_argument_checks(L, kw, code):
+    a = dict(q=A, k=A, v=A, o=A, B=1, T=256, H=4, Hkv=2, d=128, io=1, scale=0.088, stream=None)
+    a.update(kw)
+    rc = L.gdn_attention_prefill(a["q"], a["k"], a["v"], a["o"], a["B"], a["T"], a["H"], a["Hkv"], a["d"], a["io"],
+                                 a["scale"], a["stream"])
+    assert rc == code, (kw, rc, L.gdn_last_error_message())
+
+
+def test_attention_empty_prompt_is_a_no_op(L):
+    assert L.gdn_attention_prefill(None, None, None, None, 2, 0, 4, 2, 128, 1, 0.1, None) == OK
+
+
 def _decode(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
     a.update(kw)

@@ -1,0 +1,73 @@
+"""GPU parity of the causal attention prefill (gdn_attention_prefill, through the C ABI)
+against the fp64 oracle (``oracle.attention.causal_attention``).
+
+bf16 q, k, v and o with fp32 softmax and accumulation; the bar is the bf16 one of
+the other parity tests: max|x - ref| / max|ref| < 2e-2 per output tensor.  At the
+full timed size the oracle is evaluated on sampled query rows (every head).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_14568_amd as gdn
+from oracle import attention as att
+from paper_2607_14568_amd import inputs
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+f64 = inputs.as_f64
+
+
+def _rel(x, ref):
+    return float(np.abs(x - ref).max() / np.abs(ref).max())
+
+
+def _check(B, T, H, Hkv, d, seed, scale=None, rows=None):
+    label = "attention B=%d T=%d H=%d H_kv=%d d=%d" % (B, T, H, Hkv, d)
+    print("case:", label, flush=True)
+    x = inputs.make_attention(B, T, H, Hkv, d, seed)
+    sc = 1.0 / d ** 0.5 if scale is None else scale
+    o = gdn.gdn_attention_prefill(x["q"].cuda(), x["k"].cuda(), x["v"].cuda(), scale=sc)
+    torch.cuda.synchronize()
+    ref = att.causal_attention(f64(x["q"]), f64(x["k"]), f64(x["v"]), sc, rows=rows)
+    got = f64(o) if rows is None else f64(o)[:, rows]
+    e = _rel(got, ref)
+    print("  max rel err o=%.3e" % e, flush=True)
+    assert np.isfinite(f64(o)).all()
+    assert e < TOL, (label, e)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 127, 128, 129, 300])
+def test_attention_shapes_and_tails(d, T):
+    _check(2, T, 4, 2, d, seed=700 + T + d)
+
+
+@pytest.mark.parametrize("H,Hkv", [(4, 4), (4, 1), (6, 2)])
+def test_attention_grouped_heads(H, Hkv):
+    _check(1, 700, H, Hkv, 128, seed=710 + H + Hkv)
+
+
+def test_attention_sharp_scores():
+    """A large scale: softmax close to one-hot, the running max changing often."""
+    _check(1, 500, 2, 1, 128, seed=720, scale=1.5)
+
+
+def test_attention_2k():
+    _check(1, 2048, 16, 8, 128, seed=721)
+
+
+def test_attention_full_size_sampled_rows():
+    """The timed shape: T=10240, 16 query heads over 8 key/value heads, d=128; 96 sampled query rows."""
+    rows = sorted(set([0, 1, 63, 64, 127, 128, 5000, 10239] + list(np.random.default_rng(5).integers(0, 10240, 88))))
+    _check(1, 10240, 16, 8, 128, seed=722, rows=rows)
+
+
+def test_attention_deterministic_and_grouped_equals_repeated_heads():
+    x = inputs.make_attention(1, 333, 4, 2, 128, seed=730)
+    q, k, v = x["q"].cuda(), x["k"].cuda(), x["v"].cuda()
+    a = gdn.gdn_attention_prefill(q, k, v)
+    b = gdn.gdn_attention_prefill(q, k, v)
+    c = gdn.gdn_attention_prefill(q, k.repeat_interleave(2, dim=2).contiguous(), v.repeat_interleave(2, dim=2).contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(a, c)

@@ -430,3 +430,68 @@ def test_ex_decode_equals_ex_prefill():
         ot, S = oracle.decode_step_ex(q[:, t], k[:, t], v[:, t], a[:, t], b[:, t], S, **kw)
         np.testing.assert_allclose(ot, o[:, t], rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(S, ST, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- causal attention oracle
+from oracle import attention as att  # noqa: E402
+
+
+def _att_brute(q, k, v, scale):
+    """Pure-Python loops with math.exp: o_i = sum_{j<=i} e^{s_ij} v_j / sum_{j<=i} e^{s_ij}."""
+    B, T, H, d = q.shape
+    Hkv = k.shape[2]
+    o = np.zeros(q.shape)
+    for b in range(B):
+        for h in range(H):
+            kh = h // (H // Hkv)
+            for i in range(T):
+                s = [scale * sum(float(q[b, i, h, c]) * float(k[b, j, kh, c]) for c in range(d)) for j in range(i + 1)]
+                mx = max(s)
+                w = [math.exp(x - mx) for x in s]
+                z = sum(w)
+                for c in range(d):
+                    o[b, i, h, c] = sum(w[j] * float(v[b, j, kh, c]) for j in range(i + 1)) / z
+    return o
+
+
+@pytest.mark.parametrize("H,Hkv", [(2, 1), (4, 2), (3, 3)])
+def test_attention_brute_force(H, Hkv):
+    rng = np.random.default_rng(60 + H + Hkv)
+    q = rng.standard_normal((2, 7, H, 3))
+    k = rng.standard_normal((2, 7, Hkv, 3))
+    v = rng.standard_normal((2, 7, Hkv, 3))
+    np.testing.assert_allclose(att.causal_attention(q, k, v, 0.7), _att_brute(q, k, v, 0.7), rtol=1e-12, atol=1e-13)
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(61)
+    B, T, H, d = 1, 9, 2, 4
+    q = rng.standard_normal((B, T, H, d))
+    k = np.repeat(rng.standard_normal((B, 1, 1, d)), T, axis=1)   # one key everywhere
+    v = rng.standard_normal((B, T, 1, d))
+    o = att.causal_attention(q, k, v, 0.5)
+    prefix_mean = np.cumsum(v[:, :, 0], axis=1) / np.arange(1, T + 1)[None, :, None]
+    for h in range(H):
+        np.testing.assert_allclose(o[:, :, h], prefix_mean, rtol=1e-13, atol=1e-14)   # equal scores: prefix means
+    k2 = rng.standard_normal((B, T, 1, d))
+    o2 = att.causal_attention(q, k2, v, 0.0)                                          # scale 0: the same
+    np.testing.assert_allclose(o2[:, :, 0], prefix_mean, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(o2[:, 0, 1], v[:, 0, 0], rtol=0, atol=0)               # first query sees only key 0
+
+
+def test_attention_invariances_and_sampled_rows():
+    rng = np.random.default_rng(62)
+    B, T, H, Hkv, d = 2, 40, 4, 2, 8
+    q = rng.standard_normal((B, T, H, d))
+    k = rng.standard_normal((B, T, Hkv, d))
+    v = rng.standard_normal((B, T, Hkv, d))
+    o = att.causal_attention(q, k, v, 0.35)
+    u = rng.standard_normal(d)            # k_j + u adds q_i.u to every score of row i: softmax unchanged
+    np.testing.assert_allclose(att.causal_attention(q, k + u, v, 0.35), o, rtol=1e-10, atol=1e-12)
+    rows = [0, 5, 17, 39]
+    np.testing.assert_allclose(att.causal_attention(q, k, v, 0.35, rows=rows), o[:, rows], rtol=1e-13, atol=1e-14)
+    # a value change at position j reaches only queries i >= j
+    v2 = v.copy()
+    v2[:, 20] += 1.0
+    o2 = att.causal_attention(q, k, v2, 0.35)
+    assert np.array_equal(o2[:, :20], o[:, :20]) and np.abs(o2[:, 20:] - o[:, 20:]).min() > 0
