@@ -317,7 +317,7 @@ def main():
         "roofline": roof,
     }
     if w.decode:
-        out["metric"] = "gated-delta-rule decode-step tokens/s (B=64,H=16,d=128)"
+        out["metric"] = "gated-delta-rule decode-step tokens/s (B=%d,H=%d,d=%d)" % (w.B, w.H, w.dk)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x_host, args.cpu_budget)
     print(json.dumps(out), flush=True)

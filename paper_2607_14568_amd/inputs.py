@@ -69,6 +69,9 @@ WORKLOADS = {
     # decode: 64 sequences, one token each per step, resident fp32 state
     "decode_b64_f32": Workload("decode_b64_f32", B=64, T=1, H=16, dk=128, dv=128, io="f32",
                                seed=1004, s0_std=0.02, decode=True),
+    # the same step over 512 sequences: 537 MB of state, larger than the 256 MB Infinity Cache
+    "decode_b512_f32": Workload("decode_b512_f32", B=512, T=1, H=16, dk=128, dv=128, io="f32",
+                                seed=1014, s0_std=0.02, decode=True, pool=4),
 }
 
 

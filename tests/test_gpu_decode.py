@@ -53,3 +53,9 @@ def test_decode_extreme_gates():
     y["g"][1].zero_()
     y["beta"][2].zero_()
     _replay(y, 6, 2e-4)
+
+
+def test_decode_b512_workload():
+    """512 sequences x 16 heads (537 MB of state, past the Infinity Cache): 3 steps, every output compared."""
+    print("case: decode_b512_f32", flush=True)
+    _replay(inputs.make_workload("decode_b512_f32"), 3, 2e-4)
