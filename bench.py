@@ -130,17 +130,16 @@ def attention_bench(args):
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record(stream)
     for i in range(args.steps):
-        ev[i][0].record(stream)
         step(args.warmup + i)
-        ev[i][1].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t0
-    call_ms = [a.elapsed_time(b) for a, b in ev]
-    avg_call_s = sum(call_ms) / len(call_ms) * 1e-3
+    avg_call_s = ev0.elapsed_time(ev1) / args.steps * 1e-3
     ms_per_step = t_wall * 1e3 / args.steps
     flops = 2.0 * d * H * B * T * (T + 1)                 # Q K^T and P V over each query's causal prefix
     byts = B * T * (2 * H + 2 * Hkv) * d * 2              # q, k, v read, o written (bf16)
@@ -151,7 +150,6 @@ def attention_bench(args):
     roof["alg_flops"] = flops
     roof["alg_bytes"] = byts
     roof["avg_call_us"] = avg_call_s * 1e6
-    roof["min_call_us"] = min(call_ms) * 1e3
     out = {
         "metric": "causal softmax-attention prefill tokens/s (T=%d, H=%d, H_kv=%d, d=%d); %% of roofline" % (T, H, Hkv, d),
         "value": B * T / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -267,19 +265,19 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # per-call durations with HIP events on the stream the library launches on
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    # average call duration: HIP events on the stream the library launches on, around the whole timed region
+    # (events between calls would add their own gaps to calls of a few microseconds)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
+    ev0.record(stream)
     for i in range(args.steps):
-        ev[i][0].record(stream)
         step(args.warmup + i)
-        ev[i][1].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
-    call_ms = [a.elapsed_time(b) for a, b in ev]
     ms_per_step = t_wall * 1e3 / args.steps
-    avg_call_s = sum(call_ms) / len(call_ms) * 1e-3
+    avg_call_s = ev0.elapsed_time(ev1) / args.steps * 1e-3
 
     ntok = sum(lens)
     value = ntok / (ms_per_step * 1e-3)
@@ -304,7 +302,6 @@ def main():
     roof["alg_bytes"] = byts
     roof["alg_flops"] = flops
     roof["avg_call_us"] = avg_call_s * 1e6
-    roof["min_call_us"] = min(call_ms) * 1e3
 
     out = {
         "metric": "gated-delta-rule prefill tokens/s at T=10240,H=16,d=128; % of roofline",
