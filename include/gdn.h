@@ -275,6 +275,9 @@ gdn_status gdn_decode_step_ex(const void* q, const void* k, const void* v,
  *   q, o   [B, T, H, d]     bf16 (io_dtype must be GDN_BF16)
  *   k, v   [B, T, H_kv, d]  bf16
  *   d      64 or 128;  1 <= H_kv <= H, H_kv divides H;  T >= 0 (T = 0: nothing to do)
+ *   cu_seqlens, n_seqs   packed sequences as in gdn_chunk_prefill (B must be 1; DEVICE int32
+ *          [n_seqs + 1]; each sequence attends only within itself; offsets outside the contract
+ *          are clamped on the device into a nondecreasing partition of [0, T]), or NULL and 0
  *   scale  multiplies q . k (1 / sqrt(d) gives the usual attention)
  * The score matrix is never stored: the kernel keeps a running softmax per query
  * (fp32) and needs no workspace.  Errors: GDN_ERR_INVALID_ARG for bad sizes,
@@ -282,8 +285,9 @@ gdn_status gdn_decode_step_ex(const void* q, const void* k, const void* v,
  * for GDN_F32 io or another d.
  */
 gdn_status gdn_attention_prefill(const void* q, const void* k, const void* v, void* o,
-                                 int B, int T, int H, int H_kv, int d, int io_dtype, float scale,
-                                 void* stream);
+                                 int B, int T, int H, int H_kv, int d,
+                                 const int32_t* cu_seqlens, int n_seqs,
+                                 int io_dtype, float scale, void* stream);
 
 #ifdef __cplusplus
 }

@@ -69,7 +69,7 @@ def lib():
         L.gdn_decode_step_grouped.restype = I
         L.gdn_decode_step_ex.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, I, P]
         L.gdn_decode_step_ex.restype = I
-        L.gdn_attention_prefill.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P]
+        L.gdn_attention_prefill.argtypes = [P, P, P, P, I, I, I, I, I, P, I, I, F, P]
         L.gdn_attention_prefill.restype = I
         _lib = L
     return _lib
@@ -278,12 +278,17 @@ def _decode(q, k, v, g, beta, S, scale, o, grouped, flags=None):
     return o
 
 
-def gdn_attention_prefill(q, k, v, *, scale=None, o=None):
+def gdn_attention_prefill(q, k, v, *, scale=None, cu_seqlens=None, o=None):
     """Causal softmax attention; see ``gdn_attention_prefill`` in include/gdn.h.
 
     q [B,T,H,d] and k, v [B,T,H_kv,d] bf16 CUDA tensors; ``scale`` defaults to
-    1/sqrt(d).  Returns o [B,T,H,d] bf16.
+    1/sqrt(d).  Packed sequences: B == 1 and ``cu_seqlens`` an int32 CUDA tensor
+    [n+1].  Returns o [B,T,H,d] bf16.
     """
+    n_seqs = 0
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        n_seqs = cu_seqlens.numel() - 1
     for name, t in (("q", q), ("k", k), ("v", v)):
         _dev(t, name, torch.bfloat16)
     B, T, H, d = q.shape
@@ -295,6 +300,6 @@ def gdn_attention_prefill(q, k, v, *, scale=None, o=None):
     else:
         _dev(o, "o", torch.bfloat16)
     sc = float(scale) if scale is not None else 1.0 / float(d) ** 0.5
-    _check(lib().gdn_attention_prefill(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, T, H, Hkv, d, GDN_BF16, sc,
-                                       _stream(q.device)))
+    _check(lib().gdn_attention_prefill(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, T, H, Hkv, d, _ptr(cu_seqlens), n_seqs,
+                                       GDN_BF16, sc, _stream(q.device)))
     return o

@@ -2118,7 +2118,9 @@ struct AttnParams {
     const bf16_t* v;
     bf16_t* o;
     int B, T, H, HKV;
-    int nqb;            // query blocks per sequence
+    int nqb;            // dense: query blocks per sequence; packed: blocks of the grid per head (an upper bound)
+    const int32_t* cu;  // packed sequences: offsets [n_seq + 1] (device), or null
+    int n_seq;
     float scale_log2;   // scale * log2(e)
 };
 
@@ -2136,17 +2138,40 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
     constexpr int NCP = 2 * AKB / RPI;  // 1 KB copies per key block (K and V)
     __shared__ AttnLds<DH> lds;
     const int BH = p.B * p.H;
-    const int qb = p.nqb - 1 - (int)(blockIdx.x / BH);   // blocks with the most keys first
+    int qb = p.nqb - 1 - (int)(blockIdx.x / BH);   // blocks with the most keys first
     const int bh = (int)(blockIdx.x % BH);
     const int b = bh / p.H, h = bh % p.H, hk = h / (p.H / p.HKV);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
-    const int T = p.T;
+    long seq0 = (long)b * p.T;   // first row of this workgroup's sequence
+    int T = p.T;                 // its length
+    if (p.cu) {
+        // packed sequences (B = 1): grid block qb (counted from the top) is block j of sequence s, where the
+        // sequences' blocks are numbered consecutively, each sequence's last block first.  Offsets outside the
+        // contract are clamped into a nondecreasing partition of [0, p.T], so every access stays in bounds.
+        int prev = 0, before = 0, s = 0;
+        int found = -1;
+        for (; s < p.n_seq; ++s) {
+            const int next = min(max(p.cu[s + 1], prev), p.T);
+            const int nb = (next - prev + AQ - 1) / AQ;
+            const int r = p.nqb - 1 - qb;   // rank of this block in that numbering
+            if (r < before + nb) {
+                found = nb - 1 - (r - before);
+                seq0 = prev;
+                T = next - prev;
+                break;
+            }
+            before += nb;
+            prev = next;
+        }
+        if (found < 0) return;   // past the last block (the grid is an upper bound)
+        qb = found;
+    }
     const int q0 = qb * AQ, qw = q0 + 16 * wave;   // the workgroup's and this wave's first query
     const long rsq = (long)p.H * DH, rsk = (long)p.HKV * DH;   // row strides (elements)
-    const bf16_t* qbase = p.q + ((long)b * T * p.H + h) * DH;
-    const bf16_t* kbase = p.k + ((long)b * T * p.HKV + hk) * DH;
-    const bf16_t* vbase = p.v + ((long)b * T * p.HKV + hk) * DH;
+    const bf16_t* qbase = p.q + (seq0 * p.H + h) * DH;
+    const bf16_t* kbase = p.k + (seq0 * p.HKV + hk) * DH;
+    const bf16_t* vbase = p.v + (seq0 * p.HKV + hk) * DH;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
     auto kq = [](int r, int cc) { return r * DH + (((cc >> 3) ^ (((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1))) << 3) + (cc & 7); };
     // descriptor over rows [r0, min(r0 + n, T)) of a [T][heads][DH] tensor; rows past T read as zeros
@@ -2245,7 +2270,7 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
     const int qi = qw + l16;
     if (qi < T) {
         const float inv = 1.f / l;
-        bf16_t* orow = p.o + (((long)b * T + qi) * p.H + h) * DH;
+        bf16_t* orow = p.o + ((seq0 + qi) * p.H + h) * DH;
 #pragma unroll
         for (int t = 0; t < NDT; ++t) {
             const floatx4 ov = oacc[t] * inv;
@@ -2793,7 +2818,8 @@ extern "C" gdn_status gdn_decode_step_ex(const void* q, const void* k, const voi
 }
 
 extern "C" gdn_status gdn_attention_prefill(const void* q, const void* k, const void* v, void* o, int B, int T, int H,
-                                            int H_kv, int d, int io_dtype, float scale, void* stream) {
+                                            int H_kv, int d, const int32_t* cu_seqlens, int n_seqs, int io_dtype,
+                                            float scale, void* stream) {
     g_err[0] = '\0';
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
@@ -2801,6 +2827,11 @@ extern "C" gdn_status gdn_attention_prefill(const void* q, const void* k, const 
     if (H_kv < 1 || H_kv > H || H % H_kv != 0)
         return fail(GDN_ERR_INVALID_ARG, "H_kv=%d key/value heads must divide the H=%d query heads", H_kv, H);
     if (d < 1) return fail(GDN_ERR_INVALID_ARG, "d=%d must be positive", d);
+    if ((cu_seqlens == nullptr) != (n_seqs == 0))
+        return fail(GDN_ERR_INVALID_ARG, "cu_seqlens and n_seqs=%d must be given together", n_seqs);
+    if (n_seqs < 0) return fail(GDN_ERR_INVALID_ARG, "n_seqs=%d is negative", n_seqs);
+    if (n_seqs > 0 && B != 1) return fail(GDN_ERR_INVALID_ARG, "packed sequences need B == 1 (got %d)", B);
+    if (cu_seqlens && !aligned(cu_seqlens, 4)) return fail(GDN_ERR_INVALID_ARG, "cu_seqlens is not 4-byte aligned");
     if (d != 64 && d != 128) return fail(GDN_ERR_UNSUPPORTED, "d=%d: only 64 and 128 are implemented", d);
     if (io_dtype != GDN_BF16) return fail(GDN_ERR_UNSUPPORTED, "attention is implemented for bf16 io only");
     if (T > 0 && (!q || !k || !v || !o)) return fail(GDN_ERR_INVALID_ARG, "q, k, v and o must be non-null");
@@ -2808,7 +2839,8 @@ extern "C" gdn_status gdn_attention_prefill(const void* q, const void* k, const 
     for (const void* ptr : ptrs)
         if (ptr && !aligned(ptr, 16)) return fail(GDN_ERR_INVALID_ARG, "tensor pointer %p is not 16-byte aligned", ptr);
     if ((long)H * d > (1L << 20)) return fail(GDN_ERR_UNSUPPORTED, "H=%d too large", H);
-    const long nqb = ((long)T + AQ - 1) / AQ;
+    // packed: each sequence adds at most one partial block to the dense count
+    const long nqb = ((long)T + AQ - 1) / AQ + (n_seqs > 0 ? n_seqs : 0);
     if (nqb * B * H >= (1L << 31)) return fail(GDN_ERR_UNSUPPORTED, "B*T*H too large");
     if (T == 0) return GDN_OK;
     AttnParams a;
@@ -2818,6 +2850,8 @@ extern "C" gdn_status gdn_attention_prefill(const void* q, const void* k, const 
     a.o = static_cast<bf16_t*>(o);
     a.B = B; a.T = T; a.H = H; a.HKV = H_kv;
     a.nqb = (int)nqb;
+    a.cu = cu_seqlens;
+    a.n_seq = n_seqs;
     a.scale_log2 = scale * 1.4426950408889634f;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();

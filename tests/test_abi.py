@@ -285,17 +285,22 @@ def test_ex_decode_argument_checks(L, kw, code):
     (dict(d=0), INVALID), (dict(d=96), UNSUPPORTED), (dict(d=256), UNSUPPORTED),
     (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(k=A + 8), INVALID), (dict(v=A + 2), INVALID),
     (dict(H=1 << 14), UNSUPPORTED),
+    (dict(cu=A), INVALID),                       # cu_seqlens without n_seqs
+    (dict(n=3), INVALID),                        # n_seqs without cu_seqlens
+    (dict(cu=A, n=2, B=2), INVALID),             # packed sequences need B == 1
+    (dict(cu=A + 2, n=2), INVALID),              # misaligned offsets
+    (dict(cu=A, n=-1), INVALID),
 ])
 def test_attention_argument_checks(L, kw, code):
-    a = dict(q=A, k=A, v=A, o=A, B=1, T=256, H=4, Hkv=2, d=128, io=1, scale=0.088, stream=None)
+    a = dict(q=A, k=A, v=A, o=A, B=1, T=256, H=4, Hkv=2, d=128, cu=None, n=0, io=1, scale=0.088, stream=None)
     a.update(kw)
-    rc = L.gdn_attention_prefill(a["q"], a["k"], a["v"], a["o"], a["B"], a["T"], a["H"], a["Hkv"], a["d"], a["io"],
-                                 a["scale"], a["stream"])
+    rc = L.gdn_attention_prefill(a["q"], a["k"], a["v"], a["o"], a["B"], a["T"], a["H"], a["Hkv"], a["d"], a["cu"],
+                                 a["n"], a["io"], a["scale"], a["stream"])
     assert rc == code, (kw, rc, L.gdn_last_error_message())
 
 
 def test_attention_empty_prompt_is_a_no_op(L):
-    assert L.gdn_attention_prefill(None, None, None, None, 2, 0, 4, 2, 128, 1, 0.1, None) == OK
+    assert L.gdn_attention_prefill(None, None, None, None, 2, 0, 4, 2, 128, None, 0, 1, 0.1, None) == OK
 
 
 def _decode(L, **kw):

@@ -71,3 +71,27 @@ def test_attention_deterministic_and_grouped_equals_repeated_heads():
     c = gdn.gdn_attention_prefill(q, k.repeat_interleave(2, dim=2).contiguous(), v.repeat_interleave(2, dim=2).contiguous())
     torch.cuda.synchronize()
     assert torch.equal(a, b) and torch.equal(a, c)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_attention_packed_sequences(d):
+    """Sequences packed with cu_seqlens (empty, one-token, block-edge and ragged lengths) attend only within
+    themselves: each compared with the oracle over that sequence alone."""
+    lens = [0, 1, 128, 129, 300, 64, 0, 777, 5]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    print("case: attention packed lengths %s d=%d" % (lens, d), flush=True)
+    x = inputs.make_attention(1, T, 4, 2, d, seed=740 + d)
+    sc = 1.0 / d ** 0.5
+    o = gdn.gdn_attention_prefill(x["q"].cuda(), x["k"].cuda(), x["v"].cuda(), scale=sc,
+                                  cu_seqlens=torch.from_numpy(cu).cuda())
+    torch.cuda.synchronize()
+    got = f64(o)
+    q, k, v = f64(x["q"]), f64(x["k"]), f64(x["v"])
+    worst = 0.0
+    for s0, s1 in zip(cu[:-1], cu[1:]):
+        if s1 > s0:
+            ref = att.causal_attention(q[:, s0:s1], k[:, s0:s1], v[:, s0:s1], sc)
+            worst = max(worst, _rel(got[:, s0:s1], ref))
+    print("  max rel err o=%.3e" % worst, flush=True)
+    assert worst < TOL
