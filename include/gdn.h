@@ -193,6 +193,22 @@ gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void*
                                        void* stream);
 
 /*
+ * Snapshots with grouped key heads and the in-kernel input transforms: arguments
+ * as gdn_chunk_prefill_snapshots plus H_k (as gdn_chunk_prefill_grouped; q and k
+ * [B, T, H_k, dk]) and flags (as gdn_chunk_prefill_ex).  H_k = H and flags = 0
+ * is gdn_chunk_prefill_snapshots.
+ */
+gdn_status gdn_chunk_prefill_snapshots_ex(const void* q, const void* k, const void* v,
+                                          const float* g, const float* beta, const float* S0,
+                                          void* o, float* S_T,
+                                          int B, int T, int H, int H_k, int dk, int dv, int chunk,
+                                          const int32_t* cu_seqlens, int n_seqs,
+                                          int io_dtype, float scale, int flags,
+                                          int snap_every, float* snaps,
+                                          void* workspace, size_t workspace_bytes,
+                                          void* stream);
+
+/*
  * Segment-parallel prefill (section 3.2: the chunk map is affine in the state,
  * S_{c+1}^T = M_c S_c^T + N_c, so a sequence's chunks can be grouped into
  * segments whose maps compose).  Dense input can be cut at chunk boundaries

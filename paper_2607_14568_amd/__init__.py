@@ -18,7 +18,7 @@ __all__ = [
     "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
     "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
     "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped", "gdn_chunk_prefill_ex", "gdn_decode_step_ex",
-    "GDN_QK_L2NORM", "GDN_GATE_LOGITS", "gdn_attention_prefill",
+    "GDN_QK_L2NORM", "GDN_GATE_LOGITS", "gdn_attention_prefill", "gdn_chunk_prefill_snapshots_ex",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -59,6 +59,9 @@ def lib():
         L.gdn_chunk_prefill_snapshots.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, I, P, P, S,
                                                   P]
         L.gdn_chunk_prefill_snapshots.restype = I
+        L.gdn_chunk_prefill_snapshots_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, I, P, P,
+                                                     S, P]
+        L.gdn_chunk_prefill_snapshots_ex.restype = I
         L.gdn_chunk_prefill_segments.argtypes = [I] * 7
         L.gdn_chunk_prefill_segments.restype = I
         L.gdn_set_prefill_segments.argtypes = [I]
@@ -229,6 +232,29 @@ def gdn_chunk_prefill_snapshots(q, k, v, g, beta, S0=None, *, snap_every, chunk=
         a["B"], a["T"], a["H"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"], float(scale),
         int(snap_every), _ptr(snaps) if n_snap > 0 else None, _ptr(a["workspace"]), a["workspace"].numel(),
         _stream(q.device)))
+    return a["o"], a["S_T"], snaps
+
+
+def gdn_chunk_prefill_snapshots_ex(q, k, v, g, beta, S0=None, *, snap_every, flags=0, chunk=64, cu_seqlens=None,
+                                   scale=1.0, o=None, S_T=None, snaps=None, store_state=True, workspace=None):
+    """Snapshots with grouped key heads and input transforms; see ``gdn_chunk_prefill_snapshots_ex``.
+
+    Shapes as ``gdn_chunk_prefill_grouped``; returns ``(o, S_T, snaps)`` as ``gdn_chunk_prefill_snapshots``.
+    """
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=True)
+    n_snap = max(0, (a["T"] - 1) // (int(snap_every) * chunk)) if snap_every >= 1 else 0
+    shape = (a["n"], n_snap, a["H"], a["dv"], a["dk"])
+    if snaps is None:
+        snaps = torch.zeros(shape, device=q.device, dtype=torch.float32)
+    else:
+        _dev(snaps, "snaps", torch.float32)
+        if tuple(snaps.shape) != shape:
+            raise ValueError("snaps must be %s" % (shape,))
+    _check(lib().gdn_chunk_prefill_snapshots_ex(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
+        float(scale), int(flags), int(snap_every), _ptr(snaps) if n_snap > 0 else None, _ptr(a["workspace"]),
+        a["workspace"].numel(), _stream(q.device)))
     return a["o"], a["S_T"], snaps
 
 

@@ -2346,7 +2346,6 @@ uint64_t next_epoch() {
 
 template <typename IO, int DK, bool SNAP = false, bool NORM = false>
 void launch_prefill(Params p, long slots, hipStream_t st) {
-    static_assert(!(SNAP && NORM), "snapshot calls take no input transforms");
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
                            p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
@@ -2692,8 +2691,13 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     }
     if (p.n_snap > 0) {
         if (io_dtype == GDN_BF16) {
-            if (dk == 128) launch_prefill<bf16_t, 128, true>(p, L.slots, hs);
-            else launch_prefill<bf16_t, 64, true>(p, L.slots, hs);
+            if (pre & PRE_L2) {
+                if (dk == 128) launch_prefill<bf16_t, 128, true, true>(p, L.slots, hs);
+                else launch_prefill<bf16_t, 64, true, true>(p, L.slots, hs);
+            } else {
+                if (dk == 128) launch_prefill<bf16_t, 128, true>(p, L.slots, hs);
+                else launch_prefill<bf16_t, 64, true>(p, L.slots, hs);
+            }
         } else {
             if (dk == 128) launch_prefill<float, 128, true>(p, L.slots, hs);
             else launch_prefill<float, 64, true>(p, L.slots, hs);
@@ -2745,6 +2749,20 @@ extern "C" gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const v
                    0, nullptr, workspace, workspace_bytes, stream);
 }
 
+static gdn_status snapshots(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                            const float* S0, void* o, float* S_T, int B, int T, int H, int HK, int dk, int dv, int chunk,
+                            const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int flags, int snap_every,
+                            float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
+    if (snap_every < 1) return fail(GDN_ERR_INVALID_ARG, "snap_every=%d must be positive", snap_every);
+    if (chunk == CH && T > 0 && (T - 1) / ((long)snap_every * CH) > 0) {
+        if (!snaps) return fail(GDN_ERR_INVALID_ARG, "snaps must be non-null when a snapshot falls inside the prompt");
+        if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
+    }
+    if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, HK, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
+                   snap_every, snaps, workspace, workspace_bytes, stream);
+}
+
 extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v, const float* g,
                                                   const float* beta, const float* S0, void* o, float* S_T, int B,
                                                   int T, int H, int dk, int dv, int chunk,
@@ -2752,14 +2770,19 @@ extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, 
                                                   int snap_every, float* snaps, void* workspace,
                                                   size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
-    if (snap_every < 1) return fail(GDN_ERR_INVALID_ARG, "snap_every=%d must be positive", snap_every);
-    if (chunk == CH && T > 0 && (T - 1) / ((long)snap_every * CH) > 0) {
-        if (!snaps) return fail(GDN_ERR_INVALID_ARG, "snaps must be non-null when a snapshot falls inside the prompt");
-        if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
-    }
-    if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
-                   snap_every, snaps, workspace, workspace_bytes, stream);
+    return snapshots(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0,
+                     snap_every, snaps, workspace, workspace_bytes, stream);
+}
+
+extern "C" gdn_status gdn_chunk_prefill_snapshots_ex(const void* q, const void* k, const void* v, const float* g,
+                                                     const float* beta, const float* S0, void* o, float* S_T, int B,
+                                                     int T, int H, int H_k, int dk, int dv, int chunk,
+                                                     const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale,
+                                                     int flags, int snap_every, float* snaps, void* workspace,
+                                                     size_t workspace_bytes, void* stream) {
+    g_err[0] = '\0';
+    return snapshots(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale,
+                     flags, snap_every, snaps, workspace, workspace_bytes, stream);
 }
 
 static gdn_status decode(const void* q, const void* k, const void* v, const float* g, const float* beta, float* S,

@@ -303,6 +303,21 @@ def test_attention_empty_prompt_is_a_no_op(L):
     assert L.gdn_attention_prefill(None, None, None, None, 2, 0, 4, 2, 128, None, 0, 1, 0.1, None) == OK
 
 
+def test_snapshots_ex_argument_checks(L):
+    def call(**kw):
+        a = dict(Hk=2, flags=3, snap_every=1, snaps=A, chunk=64, ws_bytes=1 << 40)
+        a.update(kw)
+        return L.gdn_chunk_prefill_snapshots_ex(A, A, A, A, A, None, A, A, 1, 128, 4, a["Hk"], 64, 64, a["chunk"], None,
+                                                0, 0, 1.0, a["flags"], a["snap_every"], a["snaps"], A, a["ws_bytes"],
+                                                None)
+    assert call(snap_every=0) == INVALID
+    assert call(snaps=None) == INVALID
+    assert call(flags=4) == INVALID
+    assert call(Hk=3) == INVALID
+    assert call(chunk=32) == UNSUPPORTED
+    assert call(ws_bytes=100) == WORKSPACE
+
+
 def _decode(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S=A, o=A, B=4, H=2, dk=128, dv=128, io=0, scale=1.0, stream=None)
     a.update(kw)

@@ -120,3 +120,44 @@ def test_no_snapshot_inside_a_short_prompt():
     assert sn.shape[1] == 0
     o_ref, ST_ref = oracle.recurrence(*(f64(x[k]) for k in TOKEN), f64(x["S0"]))
     assert oracle.max_rel_err(f64(ST), ST_ref) < TOL["f32"]
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("flags", [0, gdn.GDN_QK_L2NORM | gdn.GDN_GATE_LOGITS])
+def test_snapshots_ex_grouped_with_input_transforms(io, flags):
+    """Grouped key heads (4 value heads over 2) and, in one case, unnormalised q, k and gate logits: every snapshot
+    against the oracle's state of that prefix under the same transforms."""
+    print("case: snapshots_ex", io, flags, flush=True)
+    raw = bool(flags)
+    x = inputs.make_prefill(B=2, T=300, H=4, H_k=2, dk=128, dv=128, io=io, seed=820 + flags, s0_std=0.05, raw=raw)
+    d = _dev(x)
+    o, ST, sn = gdn.gdn_chunk_prefill_snapshots_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], snap_every=2,
+                                                   flags=flags)
+    torch.cuda.synchronize()
+    kw = dict(qk_l2norm=raw, gate_logits=raw)
+    o_ref, ST_ref = oracle.recurrence_ex(*(f64(x[k]) for k in TOKEN), f64(x["S0"]), **kw)
+    assert oracle.max_rel_err(f64(o), o_ref) < TOL[io]
+    assert oracle.max_rel_err(f64(ST), ST_ref) < TOL[io]
+    assert sn.shape[1] == (300 - 1) // 128
+    for s in range(2):
+        for j in range(sn.shape[1]):
+            t = (j + 1) * 128
+            _, S = oracle.recurrence_ex(*(f64(x[k][s:s + 1, :t]) for k in TOKEN), f64(x["S0"][s:s + 1]), **kw)
+            e = oracle.max_rel_err(f64(sn[s, j]), S[0])
+            assert e < TOL[io], (s, j, e)
+
+
+def test_snapshots_ex_full_size_one_launch():
+    """T=10240, 16 heads over 8 key heads, bf16, with the input transforms: the one-launch form's snapshot variant."""
+    flags = gdn.GDN_QK_L2NORM | gdn.GDN_GATE_LOGITS
+    x = inputs.make_prefill(B=1, T=10240, H=16, H_k=8, dk=128, dv=128, io="bf16", seed=821, s0_std=0.02, g_shift=-2.0,
+                            raw=True)
+    d = _dev(x)
+    o, ST, sn = gdn.gdn_chunk_prefill_snapshots_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], snap_every=40,
+                                                   flags=flags)
+    torch.cuda.synchronize()
+    kw = dict(qk_l2norm=True, gate_logits=True)
+    o_ref, ST_ref = oracle.recurrence_ex(*(f64(x[k]) for k in TOKEN), f64(x["S0"]), **kw)
+    assert oracle.max_rel_err(f64(o), o_ref) < 2e-2 and oracle.max_rel_err(f64(ST), ST_ref) < 2e-2
+    _, S = oracle.recurrence_ex(*(f64(x[k][:, :40 * 64 * 2]) for k in TOKEN), f64(x["S0"]), **kw)
+    assert oracle.max_rel_err(f64(sn[0, 1]), S[0]) < 2e-2
