@@ -2172,8 +2172,15 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
     const bf16_t* qbase = p.q + (seq0 * p.H + h) * DH;
     const bf16_t* kbase = p.k + (seq0 * p.HKV + hk) * DH;
     const bf16_t* vbase = p.v + (seq0 * p.HKV + hk) * DH;
-    auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
-    auto kq = [](int r, int cc) { return r * DH + (((cc >> 3) ^ (((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1))) << 3) + (cc & 7); };
+    // 16-byte chunk c of row r sits at chunk c ^ swz(r).  Both reads below are free of bank conflicts with it: the
+    // K read's 16 rows in a group of 16 lanes, and the V read's 8 rows x 2 chunks in a group of 32 lanes (row bit 2
+    // lands on chunk bit 1, which neither the row's low bits nor the chunk pair use).  At d = 64 two rows share
+    // the 64 banks, so row bit 0 is left to the row stride.
+    auto swz = [](int r) {
+        return NCH == 16 ? (4 * (r & 3)) | (2 * ((r >> 2) & 1)) | ((r >> 3) & 1)
+                         : (4 * ((r >> 1) & 1)) | (2 * ((r >> 2) & 1)) | ((r >> 3) & 1);
+    };
+    auto kq = [swz](int r, int cc) { return r * DH + (((cc >> 3) ^ swz(r)) << 3) + (cc & 7); };
     // descriptor over rows [r0, min(r0 + n, T)) of a [T][heads][DH] tensor; rows past T read as zeros
     auto rows_rsrc = [&](const bf16_t* base, long rs, int r0, int n) {
         const int m = min(n, T - r0);
