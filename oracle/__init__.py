@@ -175,11 +175,44 @@ def decode_step(q, k, v, g, beta, S, *, scale=1.0, n_threads=0):
 
 
 def max_rel_err(x, ref) -> float:
-    """max|x - ref| / max|ref| over one output tensor (the parity metric)."""
+    """max|x - ref| / max|ref| over one output tensor: the parity metric, the reading taken of
+    the relative error section 3.2 quotes without a definition.  When ref is all zeros it is the
+    absolute error max|x - ref|; empty tensors give 0.  x and ref must have the same shape."""
     x = np.asarray(x, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
-    den = float(np.max(np.abs(ref))) if ref.size else 0.0
-    num = float(np.max(np.abs(x - ref))) if ref.size else 0.0
+    if x.shape != ref.shape:
+        raise ValueError("max_rel_err: shapes differ %s vs %s" % (x.shape, ref.shape))
+    if ref.size == 0:
+        return 0.0
+    den = float(np.max(np.abs(ref)))
+    num = float(np.max(np.abs(x - ref)))
     if den == 0.0:
         return num
     return num / den
+
+
+def max_rel_err_slices(x, ref, index) -> float:
+    """The largest :func:`max_rel_err` over the slices ``x[i], ref[i]`` for i in ``index`` (each
+    slice against its own largest reference value); empty slices are skipped."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if x.shape != ref.shape:
+        raise ValueError("max_rel_err_slices: shapes differ %s vs %s" % (x.shape, ref.shape))
+    worst = 0.0
+    for i in index:
+        if ref[i].size:
+            worst = max(worst, max_rel_err(x[i], ref[i]))
+    return worst
+
+
+def p99_rel_err(x, ref) -> float:
+    """99th percentile over elements of |x - ref| / (|ref| + 1e-3 rms(ref)): reported beside the
+    parity metric for information (it is not a bar)."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if x.shape != ref.shape:
+        raise ValueError("p99_rel_err: shapes differ %s vs %s" % (x.shape, ref.shape))
+    if ref.size == 0:
+        return 0.0
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return float(np.percentile(np.abs(x - ref) / (np.abs(ref) + 1e-3 * rms), 99))

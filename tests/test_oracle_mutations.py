@@ -107,3 +107,39 @@ def test_attention_pins_reject_a_planted_mistake(monkeypatch, name):
             failed.append(fn.__name__)
     print("%s: %d of %d pins fail" % (name, len(failed), len(ATT_PINS)))
     assert len(failed) >= 1, (name, failed)
+
+
+# ------------------------------------------------------------------ the parity metric
+import inspect  # noqa: E402
+
+import test_metric_pins as mpins  # noqa: E402
+
+METRIC_SRC = inspect.getsource(oracle.max_rel_err)
+METRIC_MUTATIONS = {
+    "abs dropped from the error": ("num = float(np.max(np.abs(x - ref)))", "num = float(np.max(x - ref))"),
+    "scale taken from the result": ("den = float(np.max(np.abs(ref)))", "den = float(np.max(np.abs(x)))"),
+    "abs dropped from the scale": ("den = float(np.max(np.abs(ref)))", "den = float(np.max(ref))"),
+    "mean error instead of the largest": ("num = float(np.max(np.abs(x - ref)))", "num = float(np.mean(np.abs(x - ref)))"),
+    "shape check dropped": ("if x.shape != ref.shape:", "if False:"),
+    "zero reference gives zero": ("        return num\n    return num / den", "        return 0.0\n    return num / den"),
+}
+METRIC_PINS = [getattr(mpins, n) for n in dir(mpins) if n.startswith("test_")]
+
+
+@pytest.mark.parametrize("name", sorted(METRIC_MUTATIONS))
+def test_metric_pins_reject_a_planted_mistake(monkeypatch, name):
+    import numpy as np
+    old, new = METRIC_MUTATIONS[name]
+    assert METRIC_SRC.count(old) == 1, name
+    ns = {"np": np}
+    exec(METRIC_SRC.replace(old, new), ns)
+    monkeypatch.setattr(oracle, "max_rel_err", ns["max_rel_err"])
+    failed = []
+    for fn in METRIC_PINS:
+        try:
+            fn()
+        except (KeyboardInterrupt, SystemExit):
+            raise
+        except BaseException:   # assertion errors and pytest.raises failures alike
+            failed.append(fn.__name__)
+    assert failed, "no metric pin caught: " + name
