@@ -44,11 +44,20 @@ def algorithmic(w, lens, dk, dv, H, io, s0, decode=False):
     return byts, flops * H
 
 
+def kernel_source_sha():
+    """sha256 over the library's kernel sources (every file of csrc/, in name order)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_14568_amd", "csrc")
+    for fn in sorted(os.listdir(csrc)):
+        h.update(fn.encode())
+        h.update(open(os.path.join(csrc, fn), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(workload):
     """HBM bytes per call from the committed rocprofv3 counter summary, if it was taken on this kernel source."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "%s_traffic.md" % workload)
-    src = os.path.join(ROOT, "paper_2607_14568_amd", "csrc", "gdn.hip")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -56,14 +65,24 @@ def measured_traffic(workload):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    sha = kernel_source_sha()
     if fields.get("kernel source sha256") != sha or "HBM bytes per call" not in fields:
         return None
     return float(fields["HBM bytes per call"])
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, x, budget_s):
-    """The fp64 oracle, as it stands, on this host's cores, on the same inputs."""
+    """The fp64 oracle, as it stands, on this host's cores, on the same inputs; and on one thread."""
     import oracle
     from paper_2607_14568_amd import inputs as I
     f = I.as_f64
@@ -92,8 +111,27 @@ def cpu_baseline(w, x, budget_s):
                 break
         tok = reps * int(x["q"].shape[0] * x["q"].shape[1])
         sample = "%d full call(s) of the same workload (all %d heads)" % (reps, w.H)
-    return {"value": tok / el, "unit": "tokens/s", "cores": oracle.max_threads(), "kind": "oracle",
-            "sample": sample, "seconds": round(el, 3)}
+    out = {"value": tok / el, "unit": "tokens/s", "cores": oracle.max_threads(), "kind": "oracle",
+           "sample": sample, "seconds": round(el, 3), "cpu_model": cpu_model()}
+    # one thread: a prefix of the same inputs (a bounded sample, a few seconds)
+    if w.decode:
+        t0 = time.perf_counter()
+        oracle.decode_step(*args, S, n_threads=1)
+        el1, tok1 = time.perf_counter() - t0, w.B
+        sample1 = "one decode step of the %d-sequence batch" % w.B
+    elif x["cu_seqlens"] is None:
+        n1 = min(int(x["q"].shape[1]), 512)
+        a1 = [a[:1, :n1] for a in args]
+        t0 = time.perf_counter()
+        oracle.recurrence(*a1, None if S0 is None else S0[:1], n_threads=1)
+        el1, tok1 = time.perf_counter() - t0, n1
+        sample1 = "the first %d tokens of one sequence (all %d heads)" % (n1, w.H)
+    else:
+        el1, tok1, sample1 = None, None, None
+    if el1:
+        out["value_1thread"] = tok1 / el1
+        out["sample_1thread"] = sample1
+    return out
 
 
 ATTN = {   # causal attention prefill workloads (the backbone's softmax-attention layers): B, T, H, H_kv, d
@@ -192,8 +230,10 @@ def main():
     ap.add_argument("--sets", type=int, default=4, help="rotating resident input sets")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--plan", default="auto", choices=["auto", "seq", "seg", "wide"],
+                    help="evaluation plan of the prefill (auto: the library chooses)")
     ap.add_argument("--segments", type=int, default=0,
-                    help="segments per sequence of the prefill (0 automatic, 1 sequential)")
+                    help="segments per sequence of a segmented plan (0: the plan's own count)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one plain device copy of MIB MiB before timing (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -215,7 +255,8 @@ def main():
     w = I.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    gdn.gdn_set_prefill_segments(args.segments)
+    plan_flags = {"auto": 0, "seq": gdn.GDN_PLAN_SEQUENTIAL, "seg": gdn.GDN_PLAN_SEGMENTED,
+                  "wide": gdn.GDN_PLAN_WIDE}[args.plan]
     stream = torch.cuda.current_stream(dev)
 
     x_host = I.make_workload(args.workload)
@@ -241,19 +282,21 @@ def main():
         lens = [int(a) for a in (cu[1:] - cu[:-1])] if cu is not None else [w.T] * w.B
         n_seqs = 0 if cu is None else len(lens)
         io_code = gdn.GDN_BF16 if w.io == "bf16" else gdn.GDN_F32
-        need = gdn.gdn_chunk_prefill_workspace_bytes(x_host["q"].shape[0], x_host["q"].shape[1], w.H, w.dk,
-                                                     w.dv, 64, n_seqs, io_code)
+        B_, T_ = x_host["q"].shape[0], x_host["q"].shape[1]
+        need = gdn.gdn_chunk_prefill_workspace_bytes_ex(B_, T_, w.H, w.dk, w.dv, 64, n_seqs, io_code, plan_flags,
+                                                        args.segments)
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-        segments = gdn.gdn_chunk_prefill_segments(x_host["q"].shape[0], x_host["q"].shape[1], w.H, w.dk, w.dv,
-                                                  n_seqs, io_code)
+        form, segments = gdn.gdn_chunk_prefill_plan(B_, T_, w.H, w.dk, w.dv, n_seqs, io_code, plan_flags,
+                                                    args.segments, need)
         for d in sets:
             d["o"] = torch.empty_like(d["v"])
             d["S_T"] = torch.empty_like(d["S0"]) if d["S0"] is not None else None
 
         def step(i):
             d = sets[i % len(sets)]
-            gdn.gdn_chunk_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], cu_seqlens=d["cu_seqlens"],
-                                  o=d["o"], S_T=d["S_T"], workspace=ws)
+            gdn.gdn_chunk_prefill_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], flags=plan_flags,
+                                     segments=args.segments, cu_seqlens=d["cu_seqlens"], o=d["o"], S_T=d["S_T"],
+                                     workspace=ws)
 
     for i in range(args.warmup):
         step(i)
@@ -294,11 +337,16 @@ def main():
     roof["traffic"] = None if w.decode else measured_traffic(w.name)
     if w.decode:
         roof["kernel"] = "one gdn_decode_step call"
+    elif form == gdn.GDN_PLAN_WIDE:
+        roof["kernel"] = ("one gdn_chunk_prefill call, wide segment-parallel form with %d segments (chunk terms, "
+                          "segment states, scan, output pass: four launches)" % segments)
     elif segments > 1:
         roof["kernel"] = ("one gdn_chunk_prefill call, segment-parallel form with %d segments (segment "
                           "setup, chunk terms, paired chain, scan, output pass)" % segments)
+    elif w.io == "bf16":
+        roof["kernel"] = "one gdn_chunk_prefill call, sequential form (k_prefill_fused_bf16, or chunk terms + chain)"
     else:
-        roof["kernel"] = "one gdn_chunk_prefill call (k_prefill_fused_bf16 for bf16 io)"
+        roof["kernel"] = "one gdn_chunk_prefill call, sequential form (k_chunk_terms + k_state_chain)"
     roof["alg_bytes"] = byts
     roof["alg_flops"] = flops
     roof["avg_call_us"] = avg_call_s * 1e6
@@ -313,6 +361,10 @@ def main():
                    "parallelism": "none (1 GPU)", "input_sets": len(sets)},
         "roofline": roof,
     }
+    if not w.decode:
+        out["config"]["plan"] = {gdn.GDN_PLAN_SEQUENTIAL: "sequential", gdn.GDN_PLAN_SEGMENTED: "segmented",
+                                 gdn.GDN_PLAN_WIDE: "wide"}.get(form, "?")
+        out["config"]["segments"] = segments
     if w.decode:
         out["metric"] = "gated-delta-rule decode-step tokens/s (B=%d,H=%d,d=%d)" % (w.B, w.H, w.dk)
     if not args.no_cpu_baseline:

@@ -54,10 +54,14 @@ typedef enum gdn_status {
 
 typedef enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
 
-/* Input transforms the _ex entry points apply inside their kernels (bit flags). */
+/* Bit flags of the _ex entry points: input transforms done inside the kernels,
+   and at most one evaluation plan (none: the library chooses). */
 typedef enum gdn_flags {
-    GDN_QK_L2NORM = 1,     /* q and k scaled per (token, head) to k / sqrt(|k|^2 + 1e-6)          */
-    GDN_GATE_LOGITS = 2    /* g and beta arrive as logits a, b: g = -softplus(a), beta = sigmoid(b) */
+    GDN_QK_L2NORM = 1,         /* q and k scaled per (token, head) to k / sqrt(|k|^2 + 1e-6)          */
+    GDN_GATE_LOGITS = 2,       /* g and beta arrive as logits a, b: g = -softplus(a), beta = sigmoid(b) */
+    GDN_PLAN_SEQUENTIAL = 16,  /* one chain over every chunk of a sequence                             */
+    GDN_PLAN_SEGMENTED = 32,   /* segment-parallel, narrow: one workgroup per 16 state rows             */
+    GDN_PLAN_WIDE = 64         /* segment-parallel, wide: a workgroup holds a whole state               */
 } gdn_flags;
 
 /* Library version, (major << 16) | minor. */
@@ -79,6 +83,16 @@ const char* gdn_last_error_message(void);
  */
 size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk, int dv, int chunk,
                                          int n_seqs, int io_dtype);
+
+/*
+ * Workspace for gdn_chunk_prefill_ex with this `flags` and `segments` (see the
+ * plans below): the bytes the plan needs on a 256-CU device, and never less than
+ * the sequential form's.  flags = segments = 0 is
+ * gdn_chunk_prefill_workspace_bytes.  Returns 0 for arguments the prefill would
+ * reject.  Pure host arithmetic.
+ */
+size_t gdn_chunk_prefill_workspace_bytes_ex(int B, int T, int H, int dk, int dv, int chunk,
+                                            int n_seqs, int io_dtype, int flags, int segments);
 
 /*
  * Chunked prefill (section 3.2).
@@ -127,7 +141,7 @@ gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
  *   H_k      1 <= H_k <= H and H_k divides H (GDN_ERR_INVALID_ARG otherwise);
  *            H_k = H is gdn_chunk_prefill exactly
  * All other arguments, the workspace (gdn_chunk_prefill_workspace_bytes with the
- * value-head count H), the segment-parallel setting and the errors are those of
+ * value-head count H), the automatic plan and the errors are those of
  * gdn_chunk_prefill.
  */
 gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v,
@@ -142,8 +156,8 @@ gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v
 /*
  * Chunked prefill with the per-position input transforms done in its kernels
  * (section 3 batches the per-position operations around the projections over
- * the whole chunk; these are the ones that feed the scan).  Arguments as
- * gdn_chunk_prefill_grouped, plus:
+ * the whole chunk; these are the ones that feed the scan) and a per-call
+ * evaluation plan.  Arguments as gdn_chunk_prefill_grouped, plus:
  *   flags  0 or a combination of
  *          GDN_QK_L2NORM    q and k are taken as given and each row (token, key
  *                           head) is used scaled to x / sqrt(|x|^2 + 1e-6); `scale`
@@ -151,17 +165,55 @@ gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, const void* v
  *          GDN_GATE_LOGITS  the `g` and `beta` arguments hold logits a and b:
  *                           log-decay g = -softplus(a) = -log(1 + exp(a)), write
  *                           strength beta = 1 / (1 + exp(-b)).
- *          Other bits: GDN_ERR_INVALID_ARG.  flags = 0 is gdn_chunk_prefill_grouped.
- * The workspace is the one gdn_chunk_prefill_workspace_bytes gives.
+ *          and at most one plan (none: the library chooses; results agree to
+ *          rounding whichever plan runs).  Section 3.2: the chunk map is affine in
+ *          the state, S_{c+1} = S_c M_c + N_c, so a sequence's chunks can be grouped
+ *          into segments whose maps compose.
+ *          GDN_PLAN_SEQUENTIAL  one chain walks every chunk of a sequence.
+ *          GDN_PLAN_SEGMENTED   narrow segment-parallel form: dense input is cut
+ *                           into segments; every segment's chain runs at once on the
+ *                           values from a zero state (segment 0: from S0) and on zero
+ *                           values from the identity (the segment's transition and
+ *                           how the state entering it reaches its outputs); a scan
+ *                           composes the entering states and a last pass adds each
+ *                           segment's entering-state term to its outputs.  Ragged
+ *                           input is never split (the plan is then sequential).
+ *          GDN_PLAN_WIDE        wide segment-parallel form (dense bf16 input, dk ==
+ *                           dv, without GDN_QK_L2NORM; GDN_ERR_UNSUPPORTED otherwise):
+ *                           each workgroup holds a whole state of one head; the
+ *                           segments' transitions (M_p, N_p) in one pass, a scan of
+ *                           the entering states in near-fp32 precision, and a rerun
+ *                           of every segment from its entering state with outputs.
+ *          Other bits, or two plans: GDN_ERR_INVALID_ARG.
+ *   segments  0: the plan's own count (the automatic plan chooses form and count
+ *          from the compute units of the stream's device and the sizes);
+ *          1: the sequential form; 2..64: that many segments per sequence (fewer
+ *          when a sequence has fewer chunks), with GDN_PLAN_SEGMENTED or
+ *          GDN_PLAN_WIDE only (GDN_ERR_INVALID_ARG otherwise, and outside 0..64).
+ * A call whose workspace is too small for the split it would make uses fewer
+ * segments, down to the sequential form.  flags = segments = 0 is
+ * gdn_chunk_prefill_grouped.  The workspace:
+ * gdn_chunk_prefill_workspace_bytes_ex(..., flags, segments).
  */
 gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v,
                                 const float* g, const float* beta, const float* S0,
                                 void* o, float* S_T,
                                 int B, int T, int H, int H_k, int dk, int dv, int chunk,
                                 const int32_t* cu_seqlens, int n_seqs,
-                                int io_dtype, float scale, int flags,
+                                int io_dtype, float scale, int flags, int segments,
                                 void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/*
+ * The plan gdn_chunk_prefill_ex would take for these arguments, given a
+ * workspace of `workspace_bytes` bytes and the compute units of the device of
+ * `stream` (NULL: the current device): returns the segments per sequence (1 for
+ * the sequential form, 0 for arguments the prefill would reject) and stores the
+ * plan's GDN_PLAN_* bit in *form (when form is not NULL; 0 on rejection).
+ * Queries the device's compute-unit count; enqueues nothing.
+ */
+int gdn_chunk_prefill_plan(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype, int flags,
+                           int segments, size_t workspace_bytes, void* stream, int* form);
 
 /*
  * Chunked prefill that also stores the state at chunk boundaries inside each
@@ -177,10 +229,9 @@ gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v,
  *               snapshot j of sequence s at [s, j - 1]; entries past a sequence's
  *               last snapshot are left as they were.  16-byte aligned; may be NULL
  *               when n_snap is 0.  Must not overlap any other argument.
- * The sequential form always (gdn_set_prefill_segments does not apply); the
- * workspace is the one gdn_chunk_prefill_workspace_bytes gives.  Errors as
- * gdn_chunk_prefill, and GDN_ERR_INVALID_ARG for snap_every < 1 or a missing or
- * misaligned snaps.
+ * The sequential form always; the workspace is the one
+ * gdn_chunk_prefill_workspace_bytes gives.  Errors as gdn_chunk_prefill, and
+ * GDN_ERR_INVALID_ARG for snap_every < 1 or a missing or misaligned snaps.
  */
 gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v,
                                        const float* g, const float* beta, const float* S0,
@@ -196,7 +247,8 @@ gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void*
  * Snapshots with grouped key heads and the in-kernel input transforms: arguments
  * as gdn_chunk_prefill_snapshots plus H_k (as gdn_chunk_prefill_grouped; q and k
  * [B, T, H_k, dk]) and flags (as gdn_chunk_prefill_ex).  H_k = H and flags = 0
- * is gdn_chunk_prefill_snapshots.
+ * is gdn_chunk_prefill_snapshots.  The plan bits of `flags` are not accepted
+ * (GDN_ERR_INVALID_ARG): snapshots always take the sequential form.
  */
 gdn_status gdn_chunk_prefill_snapshots_ex(const void* q, const void* k, const void* v,
                                           const float* g, const float* beta, const float* S0,
@@ -207,41 +259,6 @@ gdn_status gdn_chunk_prefill_snapshots_ex(const void* q, const void* k, const vo
                                           int snap_every, float* snaps,
                                           void* workspace, size_t workspace_bytes,
                                           void* stream);
-
-/*
- * Segment-parallel prefill (section 3.2: the chunk map is affine in the state,
- * S_{c+1}^T = M_c S_c^T + N_c, so a sequence's chunks can be grouped into
- * segments whose maps compose).  Dense input can be cut at chunk boundaries
- * into `segments` segments per sequence.  All segments' chains then run at once,
- * twice: on the values from a zero state (segment 0: from S0), and on zero
- * values from the identity, which gives each segment's transition and how the
- * state entering it reaches its outputs.  A scan over the segments composes
- * the entering states, and a last pass adds each segment's entering-state term
- * to its outputs.  This pays off when the sequential chain would leave most
- * compute units idle: few sequences times heads and many chunks.
- *   segments = 0  automatic (the default): the count (up to 16) that a time model
- *                 of both forms, fitted on MI355X, gives for the device's
- *                 compute-unit count, B, H, dk, dv, T and io_dtype; the sequential
- *                 form unless splitting wins by 10 %
- *   segments = 1  never split
- *   segments > 1  that many segments (fewer when a sequence has fewer chunks)
- * Ragged input is never split.  The setting is process-wide and read by both
- * gdn_chunk_prefill_workspace_bytes (which sizes the automatic case for a
- * 256-CU device) and gdn_chunk_prefill; a call whose workspace is too small for
- * the split it would choose uses fewer segments, down to the sequential form.
- * Results agree with the sequential form to rounding.  Returns the previous
- * setting, or -1 (and changes nothing) when segments < 0 or segments > 64.
- */
-int gdn_set_prefill_segments(int segments);
-
-/*
- * Segments per sequence that gdn_chunk_prefill would use for these sizes on the
- * current device under the current setting, given a workspace of
- * gdn_chunk_prefill_workspace_bytes(...) bytes: 1 for the sequential form, 0 for
- * arguments gdn_chunk_prefill would reject.  Queries the device's compute-unit
- * count (a HIP call); enqueues nothing.
- */
-int gdn_chunk_prefill_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype);
 
 /*
  * One decode step (the recurrence at T = 1; section 2.2, section 3.2): one

@@ -15,8 +15,9 @@ import torch
 
 __all__ = [
     "GDN_F32", "GDN_BF16", "GdnError", "lib", "gdn_version", "gdn_status_string",
-    "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill", "gdn_decode_step",
-    "gdn_set_prefill_segments", "gdn_chunk_prefill_segments", "gdn_chunk_prefill_snapshots",
+    "gdn_chunk_prefill_workspace_bytes", "gdn_chunk_prefill_workspace_bytes_ex", "gdn_chunk_prefill",
+    "gdn_decode_step", "gdn_chunk_prefill_plan", "gdn_chunk_prefill_snapshots",
+    "GDN_PLAN_SEQUENTIAL", "GDN_PLAN_SEGMENTED", "GDN_PLAN_WIDE",
     "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped", "gdn_chunk_prefill_ex", "gdn_decode_step_ex",
     "GDN_QK_L2NORM", "GDN_GATE_LOGITS", "gdn_attention_prefill", "gdn_chunk_prefill_snapshots_ex",
 ]
@@ -26,6 +27,7 @@ LIB_PATH = os.path.join(_HERE, "libgdn.so")
 
 GDN_F32, GDN_BF16 = 0, 1
 GDN_QK_L2NORM, GDN_GATE_LOGITS = 1, 2
+GDN_PLAN_SEQUENTIAL, GDN_PLAN_SEGMENTED, GDN_PLAN_WIDE = 16, 32, 64
 _IO = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
 _lib = None
 
@@ -50,11 +52,13 @@ def lib():
         L.gdn_last_error_message.restype = ctypes.c_char_p
         L.gdn_chunk_prefill_workspace_bytes.argtypes = [I, I, I, I, I, I, I, I]
         L.gdn_chunk_prefill_workspace_bytes.restype = S
+        L.gdn_chunk_prefill_workspace_bytes_ex.argtypes = [I] * 10
+        L.gdn_chunk_prefill_workspace_bytes_ex.restype = S
         L.gdn_chunk_prefill.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill.restype = I
         L.gdn_chunk_prefill_grouped.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, P, S, P]
         L.gdn_chunk_prefill_grouped.restype = I
-        L.gdn_chunk_prefill_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, P, S, P]
+        L.gdn_chunk_prefill_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, I, P, S, P]
         L.gdn_chunk_prefill_ex.restype = I
         L.gdn_chunk_prefill_snapshots.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, P, I, I, F, I, P, P, S,
                                                   P]
@@ -62,10 +66,8 @@ def lib():
         L.gdn_chunk_prefill_snapshots_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, I, P, P,
                                                      S, P]
         L.gdn_chunk_prefill_snapshots_ex.restype = I
-        L.gdn_chunk_prefill_segments.argtypes = [I] * 7
-        L.gdn_chunk_prefill_segments.restype = I
-        L.gdn_set_prefill_segments.argtypes = [I]
-        L.gdn_set_prefill_segments.restype = I
+        L.gdn_chunk_prefill_plan.argtypes = [I, I, I, I, I, I, I, I, I, S, P, ctypes.POINTER(I)]
+        L.gdn_chunk_prefill_plan.restype = I
         L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
         L.gdn_decode_step.restype = I
         L.gdn_decode_step_grouped.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P]
@@ -95,17 +97,25 @@ def gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk=64, n_seqs=0, io_dt
     return int(lib().gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io_dtype))
 
 
-def gdn_set_prefill_segments(segments: int) -> int:
-    """Segments per sequence of the segment-parallel prefill (0 automatic, 1 never); returns the previous setting."""
-    prev = int(lib().gdn_set_prefill_segments(int(segments)))
-    if prev < 0:
-        raise ValueError("segments=%d out of range [0, 64]" % segments)
-    return prev
+def gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk=64, n_seqs=0, io_dtype=GDN_BF16, flags=0,
+                                         segments=0) -> int:
+    return int(lib().gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk, n_seqs, io_dtype, int(flags),
+                                                          int(segments)))
 
 
-def gdn_chunk_prefill_segments(B, T, H, dk, dv, n_seqs=0, io_dtype=GDN_BF16) -> int:
-    """Segments per sequence a prefill of these sizes would use on the current device (1: sequential)."""
-    return int(lib().gdn_chunk_prefill_segments(B, T, H, dk, dv, n_seqs, io_dtype))
+def gdn_chunk_prefill_plan(B, T, H, dk, dv, n_seqs=0, io_dtype=GDN_BF16, flags=0, segments=0,
+                           workspace_bytes=None, device=None):
+    """``(form, segments)`` a prefill of these sizes would take on ``device`` (form: a GDN_PLAN_* bit).
+
+    ``workspace_bytes`` defaults to what ``gdn_chunk_prefill_workspace_bytes_ex`` gives.
+    """
+    if workspace_bytes is None:
+        workspace_bytes = gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, 64, n_seqs, io_dtype, flags, segments)
+    form = ctypes.c_int(0)
+    stream = _stream(torch.device("cuda", torch.cuda.current_device() if device is None else device))
+    n = int(lib().gdn_chunk_prefill_plan(B, T, H, dk, dv, n_seqs, io_dtype, int(flags), int(segments),
+                                         int(workspace_bytes), stream, ctypes.byref(form)))
+    return int(form.value), n
 
 
 def _dev(t, name, dtype=None):
@@ -126,7 +136,8 @@ def _stream(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=False):
+def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=False, flags=0,
+                  segments=0):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -158,7 +169,7 @@ def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, 
         S_T = torch.empty((n, H, dv, dk), device=q.device, dtype=torch.float32)
     elif S_T is not None:
         _dev(S_T, "S_T", torch.float32)
-    need = gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk, n_seqs, io)
+    need = gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk, n_seqs, io, flags, segments)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
     return dict(io=io, B=B, T=T, H=H, HK=HK, dk=dk, dv=dv, n=n, n_seqs=n_seqs, o=o, S_T=S_T, workspace=workspace)
@@ -196,18 +207,21 @@ def gdn_chunk_prefill_grouped(q, k, v, g, beta, S0=None, *, chunk=64, cu_seqlens
     return a["o"], a["S_T"]
 
 
-def gdn_chunk_prefill_ex(q, k, v, g, beta, S0=None, *, flags=0, chunk=64, cu_seqlens=None, scale=1.0,
+def gdn_chunk_prefill_ex(q, k, v, g, beta, S0=None, *, flags=0, segments=0, chunk=64, cu_seqlens=None, scale=1.0,
                          o=None, S_T=None, store_state=True, workspace=None):
-    """Prefill with in-kernel input transforms; see ``gdn_chunk_prefill_ex`` in include/gdn.h.
+    """Prefill with in-kernel input transforms and a per-call plan; see ``gdn_chunk_prefill_ex`` in include/gdn.h.
 
     Shapes as ``gdn_chunk_prefill_grouped``.  ``flags``: GDN_QK_L2NORM (q, k taken
-    unnormalised) and/or GDN_GATE_LOGITS (``g``, ``beta`` hold the logits a, b).
+    unnormalised) and/or GDN_GATE_LOGITS (``g``, ``beta`` hold the logits a, b), and at
+    most one of GDN_PLAN_SEQUENTIAL, GDN_PLAN_SEGMENTED, GDN_PLAN_WIDE; ``segments``
+    the segments per sequence of a segmented plan (0: the plan's own count).
     """
-    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=True)
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=True,
+                      flags=flags, segments=segments)
     _check(lib().gdn_chunk_prefill_ex(
         _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
         a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
-        float(scale), int(flags), _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
+        float(scale), int(flags), int(segments), _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
     return a["o"], a["S_T"]
 
 

@@ -38,6 +38,7 @@
 #include <string.h>
 #include <time.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "gdn.h"
@@ -2286,6 +2287,8 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
     }
 }
 
+#include "wide.hip"
+
 // ------------------------------------------------------------------ host side
 thread_local char g_err[512] = "";
 
@@ -2325,30 +2328,35 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Compute units of the current device (cached per device).
-int device_cus() {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cached[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
-        cached[dev] = n;
+// Compute units of the device a stream's work runs on (cached per device).
+int stream_cus(hipStream_t st) {
+    static std::atomic<int> cached[64];
+    int dev = -1;
+    if (st == nullptr || hipStreamGetDevice(st, &dev) != hipSuccess) {
+        (void)hipGetLastError();
+        if (hipGetDevice(&dev) != hipSuccess) return 0;
     }
-    return cached[dev];
+    if (dev < 0 || dev >= 64) return 0;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
+        cached[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
 }
 
 // Tag of one call's chunk-term flags: a per-process random high half and a call
 // counter, never 0 or all ones (what a cleared or 0xFF-filled workspace holds).
+// Safe to call from several host threads at once.
 uint64_t next_epoch() {
-    static uint64_t salt = 0;
-    static uint64_t counter = 0;
-    if (salt == 0) {
-        uint64_t x = (uint64_t)(uintptr_t)&counter ^ ((uint64_t)time(nullptr) << 20) ^ 0x9e3779b97f4a7c15ull;
+    static const uint64_t salt = [] {
+        static int anchor;
+        uint64_t x = (uint64_t)(uintptr_t)&anchor ^ ((uint64_t)time(nullptr) << 20) ^ 0x9e3779b97f4a7c15ull;
         x ^= x >> 33; x *= 0xff51afd7ed558ccdull; x ^= x >> 33;
-        salt = (x & 0x7ffffffeull) + 1;
-    }
-    return (salt << 32) | (uint32_t)(++counter);
+        return (x & 0x7ffffffeull) + 1;
+    }();
+    static std::atomic<uint64_t> counter{0};
+    return (salt << 32) | (uint32_t)(counter.fetch_add(1, std::memory_order_relaxed) + 1);
 }
 
 template <typename IO, int DK, bool SNAP = false, bool NORM = false>
@@ -2362,7 +2370,7 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         // (three workgroups per CU) and the chain after, longest sequence first
         const long nchain = (long)p.n_seq * p.H * (p.DV / SL);
         const long items = slots * p.H;
-        const long cus = device_cus();
+        const long cus = stream_cus(st);
         const long spare = cus - nchain;   // CUs the chain leaves free (one chain workgroup per CU)
         if (spare >= 8 && 4 * spare >= cus && items > 0) {
             p.npw = (int)std::min(spare, (items + 1) / 2);
@@ -2387,73 +2395,120 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         hipLaunchKernelGGL((k_state_chain<DK, SNAP>), grid, dim3(NT), 0, st, p);
 }
 
-// ---- segment-parallel form: plan, workspace, launches
-constexpr int SEG_AUTO_MAX = 16;   // most segments per sequence chosen automatically
+// ---- evaluation plans: sequential chain, segment-parallel (narrow and wide); workspace; launches
+constexpr int SEG_AUTO_MAX = 16;   // most segments per sequence the narrow split chooses by itself
 constexpr int SEG_MAX = 64;        // most segments per sequence accepted
 constexpr long PLAN_CUS = 256;     // compute units the workspace size assumes
-int g_segments = 0;                // 0: automatic, 1: never split, > 1: that many segments
+constexpr int PLAN_BITS = GDN_PLAN_SEQUENTIAL | GDN_PLAN_SEGMENTED | GDN_PLAN_WIDE;
+enum PlanForm { FORM_AUTO = 0, FORM_SEQ = 1, FORM_SEG = 2, FORM_WIDE = 3 };
 
 struct SegPlan {
+    int form = FORM_SEQ;
     int P = 1;   // segments per sequence (1: the sequential form)
     int L = 0;   // chunks per segment
 };
 
-// Time model of both forms (microseconds), fitted to timings at dk = dv = 128 on
-// a 256-CU MI355X.  The sequential form costs a fixed start and one chain step per
-// chunk.  The segmented form costs a fixed part (its launches, the chunk terms'
-// start), a part per token and head (chunk terms, the output pass), one chain
-// step per chunk of a segment and one scan step per segment.  A chain that needs
-// more workgroups than CUs (one per CU: its LDS) runs in rounds.
+int plan_form(int flags) {
+    switch (flags & PLAN_BITS) {
+        case GDN_PLAN_SEQUENTIAL: return FORM_SEQ;
+        case GDN_PLAN_SEGMENTED: return FORM_SEG;
+        case GDN_PLAN_WIDE: return FORM_WIDE;
+        default: return FORM_AUTO;
+    }
+}
+
+// Time model of the sequential and narrow segmented forms (microseconds), fitted
+// to timings at dk = dv = 128 on a 256-CU MI355X.  The sequential form costs a
+// fixed start and one chain step per chunk.  The segmented form costs a fixed
+// part (its launches, the chunk terms' start), a part per token and head (chunk
+// terms, the output pass), one chain step per chunk of a segment and one scan
+// step per segment.  A chain that needs more workgroups than CUs (one per CU:
+// its LDS) runs in rounds.
 struct SegCost {
     double seq_fixed, chunk, seg_fixed, per_token_head, per_segment;
 };
 constexpr SegCost COST_BF16 = {17.0, 0.73, 28.5, 3.6e-4, 1.4};
 constexpr SegCost COST_F32 = {12.0, 4.2, 35.5, 1.7e-3, 2.6};
 
-// Segments per sequence.  Ragged input keeps the sequential form.
-SegPlan plan_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io, long cus, int setting) {
-    SegPlan sp;
+SegPlan split_plan(int form, int nc, int P) {
+    SegPlan x;
+    P = std::min(P, nc);
+    if (P < 2) return x;
+    x.L = (nc + P - 1) / P;
+    x.P = (nc + x.L - 1) / x.L;   // every segment non-empty
+    if (x.P < 2) return SegPlan{};
+    x.form = form;
+    return x;
+}
+
+// The wide form applies to dense bf16 input with dk = dv, without the key
+// normalisation transform.
+bool wide_applies(int n_seqs, int io, int dk, int dv, int pre) {
+    return n_seqs == 0 && io == GDN_BF16 && dk == dv && !(pre & PRE_L2);
+}
+
+// Segments of the wide form by itself: about one workgroup per CU in each pass
+// (one per (sequence, segment, head)).
+int wide_auto_P(int B, int H, int nc) {
+    const long units = (long)B * H;
+    int P = (int)std::max(2L, std::min(16L, (256 + units - 1) / units));
+    return std::min(P, nc);
+}
+
+// The plan for a call.  form_req: FORM_* (FORM_AUTO chooses); seg_req: segments
+// (0: the form's own count).  Ragged input and snapshots keep the sequential form
+// (the caller rejects a forced wide plan that does not apply).
+SegPlan choose_plan(int B, int T, int H, int dk, int dv, int n_seqs, int io, int pre, int form_req, int seg_req,
+                    long cus) {
     const int nc = (T + CH - 1) / CH;
-    if (n_seqs > 0 || nc < 2 || setting == 1) return sp;
-    auto split = [&](int P) {
-        SegPlan x;
-        x.L = (nc + P - 1) / P;
-        x.P = (nc + x.L - 1) / x.L;   // every segment non-empty
-        return x;
-    };
-    if (setting > 1) {
-        const SegPlan x = split(std::min(setting, nc));
-        return x.P > 1 ? x : sp;
-    }
-    if (cus <= 0) return sp;
+    if (form_req == FORM_SEQ || seg_req == 1 || n_seqs > 0 || nc < 2) return SegPlan{};
+    const bool wide = wide_applies(n_seqs, io, dk, dv, pre);
+    if (form_req == FORM_WIDE) return wide ? split_plan(FORM_WIDE, nc, seg_req > 0 ? seg_req : wide_auto_P(B, H, nc))
+                                           : SegPlan{};
+    if (form_req == FORM_AUTO && wide && (long)B * H >= 8 && nc >= 32) return split_plan(FORM_WIDE, nc, wide_auto_P(B, H, nc));
+    if (form_req == FORM_SEG && seg_req > 1) return split_plan(FORM_SEG, nc, seg_req);
+    if (cus <= 0) return SegPlan{};
     const SegCost& k = io == GDN_BF16 ? COST_BF16 : COST_F32;
     auto rounds = [&](long wgs) { return (double)((wgs + cus - 1) / cus); };
     const double t_seq = k.seq_fixed + k.chunk * nc * rounds((long)B * H * (dv / SL));
-    double best = 0.9 * t_seq;   // splitting must win by a margin
+    SegPlan best_plan;
+    double best = form_req == FORM_SEG ? 1e300 : 0.9 * t_seq;   // splitting by itself must win by a margin
     for (int P = 2; P <= std::min(SEG_AUTO_MAX, nc); ++P) {
-        const SegPlan x = split(P);
+        const SegPlan x = split_plan(FORM_SEG, nc, P);
         if (x.P != P) continue;
         const double t = k.seg_fixed + k.per_token_head * B * H * (double)T +
                          k.chunk * x.L * rounds((long)B * P * H * ((dv + dk) / SL)) + k.per_segment * P;
-        if (t < best) { best = t; sp = x; }
+        if (t < best) { best = t; best_plan = x; }
     }
-    return sp;
+    return best_plan;
 }
 
 struct SegLayout {
-    Layout base;   // ragged layout over the nseq P segments
-    size_t S0seg, Iseg, N, M, X, Y, total;
+    Layout base;   // ragged layout over the nseq P segments (narrow) or the dense layout (wide)
+    size_t S0seg, Iseg, N, M, X, Y, Mlo, total;
 };
 
 bool seg_layout(int B, int T, int H, int dk, int dv, int io, const SegPlan& sp, SegLayout* S) {
     const long nseg = (long)B * sp.P;
     if ((long)B * T >= (1L << 31) || nseg >= (1L << 30)) return false;
-    if (!ws_layout(1, B * T, H, dk, dv, (int)nseg, io, &S->base)) return false;
     const size_t esz = io == GDN_BF16 ? 2 : 4;
     const size_t sv = (size_t)nseg * H * dv * dk * sizeof(float), sk = (size_t)nseg * H * dk * dk * sizeof(float);
-    const size_t tk = (size_t)B * T * H * dk * esz;
-    size_t off = round_up(S->base.total, 256);
+    size_t off = 0;
     auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, 256); return at; };
+    *S = SegLayout{};
+    if (sp.form == FORM_WIDE) {
+        if (!ws_layout(B, T, H, dk, dv, 0, io, &S->base)) return false;
+        off = round_up(S->base.total, 256);
+        S->N = take(sv);
+        S->M = take(sv / 2);     // high bf16 parts of the identity runs' states
+        S->Mlo = take(sv / 2);   // ... and the low parts
+        S->X = take(sv);
+        S->total = off;
+        return true;
+    }
+    if (!ws_layout(1, B * T, H, dk, dv, (int)nseg, io, &S->base)) return false;
+    const size_t tk = (size_t)B * T * H * dk * esz;
+    off = round_up(S->base.total, 256);
     S->S0seg = take(sv);
     S->Iseg = take(sk);
     S->N = take(sv);
@@ -2464,8 +2519,7 @@ bool seg_layout(int B, int T, int H, int dk, int dv, int io, const SegPlan& sp, 
     return true;
 }
 
-// Workspace bytes of the plan the setting and a device of `cus` CUs give
-// (the sequential form's when the plan does not split).
+// Workspace bytes of a plan (the sequential form's when the plan does not split).
 size_t plan_bytes(int B, int T, int H, int dk, int dv, int n_seqs, int io, const SegPlan& sp) {
     if (sp.P > 1) {
         SegLayout S;
@@ -2475,14 +2529,16 @@ size_t plan_bytes(int B, int T, int H, int dk, int dv, int n_seqs, int io, const
     return ws_layout(B, T, H, dk, dv, n_seqs, io, &L) ? L.total : 0;
 }
 
-// The plan a call takes: the setting's (automatic: for this device), with fewer
-// segments while the workspace cannot hold it or a grid would overflow.
-SegPlan plan_for_call(int B, int T, int H, int dk, int dv, int n_seqs, int io, size_t workspace_bytes, SegLayout* S) {
-    SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io, device_cus(), __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+// The plan a call takes on a device of `cus` CUs: the requested one, with fewer
+// segments while the workspace cannot hold it or a grid would overflow, down to
+// the sequential form.
+SegPlan plan_for_call(int B, int T, int H, int dk, int dv, int n_seqs, int io, int pre, int form_req, int seg_req,
+                      size_t workspace_bytes, long cus, SegLayout* S) {
+    SegPlan sp = choose_plan(B, T, H, dk, dv, n_seqs, io, pre, form_req, seg_req, cus);
     const long nc = (T + CH - 1) / CH;
     while (sp.P > 1 && !(seg_layout(B, T, H, dk, dv, io, sp, S) && S->total <= workspace_bytes &&
                          (long)B * sp.P * H * ((dv + dk) / SL) < (1L << 31) && (long)B * (nc + SEG_MAX + 8) * H < (1L << 31)))
-        sp = plan_segments(B, T, H, dk, dv, n_seqs, io, 0, sp.P - 1);
+        sp = split_plan(sp.form, (int)nc, sp.P - 1);
     return sp;
 }
 
@@ -2510,6 +2566,16 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
     const long cunits = (long)sq.nseq * (sq.P - 1) * sq.H;   // (sequence, segment, head) triples, each on one XCD
     hipLaunchKernelGGL((k_segment_correct<IO, DK>), dim3((unsigned)(8 * ((cunits + 7) / 8) * ((sq.L + 1) / 2))),
                        dim3(NT_CORR), 0, st, sq);
+}
+
+// The wide segment-parallel form: chunk terms over all chunks, then the three wide passes.
+template <int DK>
+void launch_wide(Params p, WideParams w, hipStream_t st) {
+    const long BH = (long)w.B * w.H;
+    hipLaunchKernelGGL((k_chunk_terms_bf16<DK, false>), dim3((unsigned)(BH * w.NC)), dim3(NT), 0, st, p);
+    hipLaunchKernelGGL((k_wide_states<DK>), dim3((unsigned)(BH * (w.P - 1))), dim3(4 * DK), 0, st, w);
+    hipLaunchKernelGGL((k_wide_scan<DK>), dim3((unsigned)(8 * ((BH + 7) / 8) * (w.D / 16))), dim3(DK * 4), 0, st, w);
+    hipLaunchKernelGGL((k_wide_out<DK>), dim3((unsigned)(BH * w.P)), dim3(4 * DK), 0, st, w);
 }
 
 template <typename IO, int DK>
@@ -2550,40 +2616,58 @@ static gdn_status check_dims(int dk, int dv) {
     return GDN_OK;
 }
 
-extern "C" size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk, int dv, int chunk,
-                                                    int n_seqs, int io_dtype) {
-    if (B < 1 || T < 0 || H < 1 || chunk != CH || n_seqs < 0 || (n_seqs > 0 && B != 1)) return 0;
-    if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return 0;
-    if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return 0;
+// Validation shared by the workspace and plan queries; false for arguments the prefill would reject.
+static bool sizes_ok(int B, int T, int H, int dk, int dv, int chunk, int n_seqs, int io_dtype, int flags, int segments) {
+    if (B < 1 || T < 0 || H < 1 || chunk != CH || n_seqs < 0 || (n_seqs > 0 && B != 1)) return false;
+    if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return false;
+    if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return false;
+    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS)) return false;
+    const int pb = flags & PLAN_BITS;
+    if (pb & (pb - 1)) return false;   // at most one plan
+    if (segments < 0 || segments > SEG_MAX) return false;
+    if (segments > 1 && plan_form(flags) != FORM_SEG && plan_form(flags) != FORM_WIDE) return false;
+    if (plan_form(flags) == FORM_WIDE && !wide_applies(n_seqs, io_dtype, dk, dv, flags & PRE_L2)) return false;
     Layout L;
-    if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L)) return 0;
-    const SegPlan sp = plan_segments(B, T, H, dk, dv, n_seqs, io_dtype, PLAN_CUS,
-                                     __atomic_load_n(&g_segments, __ATOMIC_RELAXED));
+    return ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L);
+}
+
+extern "C" size_t gdn_chunk_prefill_workspace_bytes_ex(int B, int T, int H, int dk, int dv, int chunk, int n_seqs,
+                                                       int io_dtype, int flags, int segments) {
+    if (!sizes_ok(B, T, H, dk, dv, chunk, n_seqs, io_dtype, flags, segments)) return 0;
+    Layout L;
+    ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L);
+    const SegPlan sp = choose_plan(B, T, H, dk, dv, n_seqs, io_dtype, flags & PRE_L2, plan_form(flags), segments, PLAN_CUS);
     return std::max(L.total, plan_bytes(B, T, H, dk, dv, n_seqs, io_dtype, sp));
 }
 
-extern "C" int gdn_chunk_prefill_segments(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype) {
-    if (B < 1 || T < 0 || H < 1 || n_seqs < 0 || (n_seqs > 0 && B != 1)) return 0;
-    if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return 0;
-    if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return 0;
-    Layout L;
-    if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L)) return 0;
-    SegLayout S;
-    return plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype,
-                         gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, CH, n_seqs, io_dtype), &S).P;
+extern "C" size_t gdn_chunk_prefill_workspace_bytes(int B, int T, int H, int dk, int dv, int chunk,
+                                                    int n_seqs, int io_dtype) {
+    return gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk, n_seqs, io_dtype, 0, 0);
 }
 
-extern "C" int gdn_set_prefill_segments(int segments) {
-    if (segments < 0 || segments > SEG_MAX) return -1;
-    return __atomic_exchange_n(&g_segments, segments, __ATOMIC_RELAXED);
+extern "C" int gdn_chunk_prefill_plan(int B, int T, int H, int dk, int dv, int n_seqs, int io_dtype, int flags,
+                                      int segments, size_t workspace_bytes, void* stream, int* form) {
+    if (form) *form = 0;
+    if (!sizes_ok(B, T, H, dk, dv, CH, n_seqs, io_dtype, flags, segments)) return 0;
+    SegLayout S;
+    const SegPlan sp = plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, flags & PRE_L2, plan_form(flags), segments,
+                                     workspace_bytes, stream_cus(reinterpret_cast<hipStream_t>(stream)), &S);
+    if (form) *form = sp.P > 1 ? (sp.form == FORM_WIDE ? GDN_PLAN_WIDE : GDN_PLAN_SEGMENTED) : GDN_PLAN_SEQUENTIAL;
+    return sp.P;
 }
 
 // The prefill behind both entry points: snap_every = 0 takes no snapshots.
 static gdn_status prefill(const void* q, const void* k, const void* v, const float* g, const float* beta,
                           const float* S0, void* o, float* S_T, int B, int T, int H, int HK, int dk, int dv, int chunk,
-                          const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int pre, int snap_every,
-                          float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
-    if (pre & ~(PRE_L2 | PRE_GATES)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", pre);
+                          const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int flags, int segments,
+                          int snap_every, float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
+    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", flags);
+    const int pb = flags & PLAN_BITS, pre = flags & (PRE_L2 | PRE_GATES), form_req = plan_form(flags);
+    if (pb & (pb - 1)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: more than one plan", flags);
+    if (segments < 0 || segments > SEG_MAX)
+        return fail(GDN_ERR_INVALID_ARG, "segments=%d out of range [0, %d]", segments, SEG_MAX);
+    if (segments > 1 && form_req != FORM_SEG && form_req != FORM_WIDE)
+        return fail(GDN_ERR_INVALID_ARG, "segments=%d needs GDN_PLAN_SEGMENTED or GDN_PLAN_WIDE", segments);
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16)
         return fail(GDN_ERR_INVALID_ARG, "io_dtype=%d is neither GDN_F32 nor GDN_BF16", io_dtype);
     if (B < 1 || H < 1 || T < 0) return fail(GDN_ERR_INVALID_ARG, "B=%d H=%d T=%d out of range", B, H, T);
@@ -2610,6 +2694,10 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     if ((long)B * T * H > (1L << 40)) return fail(GDN_ERR_UNSUPPORTED, "B*T*H too large");
     if ((long)H * (dk > dv ? dk : dv) > (1L << 24))   // 32-bit in-chunk offsets of 64 rows
         return fail(GDN_ERR_UNSUPPORTED, "H=%d too large", H);
+    if (form_req == FORM_WIDE && !wide_applies(n_seqs, io_dtype, dk, dv, pre))
+        return fail(GDN_ERR_UNSUPPORTED, "GDN_PLAN_WIDE needs dense bf16 input with dk == dv, without GDN_QK_L2NORM");
+    if (form_req == FORM_WIDE && snap_every > 0)
+        return fail(GDN_ERR_UNSUPPORTED, "GDN_PLAN_WIDE does not take snapshots");
     Layout L;
     if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L))
         return fail(GDN_ERR_UNSUPPORTED, "too many chunks x heads for one call");
@@ -2652,7 +2740,30 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     // segment-parallel form when the plan splits and the workspace holds it (never
     // with snapshots: the states inside segments are not formed)
     SegLayout S;
-    const SegPlan sp = p.n_snap > 0 ? SegPlan{} : plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, workspace_bytes, &S);
+    const SegPlan sp = p.n_snap > 0 ? SegPlan{}
+                                    : plan_for_call(B, T, H, dk, dv, n_seqs, io_dtype, pre, form_req, segments,
+                                                    workspace_bytes, stream_cus(hs), &S);
+    if (sp.P > 1 && sp.form == FORM_WIDE) {
+        WideParams w;
+        w.q = static_cast<const bf16_t*>(q); w.k = static_cast<const bf16_t*>(k); w.v = static_cast<const bf16_t*>(v);
+        w.wsG = reinterpret_cast<const float*>(ws + S.base.G);
+        w.wsT = reinterpret_cast<const bf16_t*>(ws + S.base.T);
+        w.wsP = reinterpret_cast<const bf16_t*>(ws + S.base.P);
+        w.o = static_cast<bf16_t*>(o);
+        w.S0 = S0;
+        w.N = reinterpret_cast<float*>(ws + S.N);
+        w.Mhi = reinterpret_cast<bf16_t*>(ws + S.M);
+        w.Mlo = reinterpret_cast<bf16_t*>(ws + S.Mlo);
+        w.X = reinterpret_cast<float*>(ws + S.X);
+        w.ST = S_T;
+        w.B = B; w.T = T; w.H = H; w.HK = HK; w.G = H / HK; w.D = dk; w.NC = p.NC; w.P = sp.P; w.L = sp.L;
+        w.scale = scale;
+        if (dk == 128) launch_wide<128>(p, w, hs);
+        else launch_wide<64>(p, w, hs);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+        return GDN_OK;
+    }
     if (sp.P > 1) {
         const int nseg = B * sp.P;
         SegParams sq;
@@ -2732,7 +2843,7 @@ extern "C" gdn_status gdn_chunk_prefill(const void* q, const void* k, const void
                                         int n_seqs, int io_dtype, float scale, void* workspace,
                                         size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
-    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0, 0,
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0, 0, 0,
                    nullptr, workspace, workspace_bytes, stream);
 }
 
@@ -2743,17 +2854,17 @@ extern "C" gdn_status gdn_chunk_prefill_grouped(const void* q, const void* k, co
                                                 void* workspace, size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
     return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, 0, 0,
-                   nullptr, workspace, workspace_bytes, stream);
+                   0, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v, const float* g,
                                            const float* beta, const float* S0, void* o, float* S_T, int B, int T,
                                            int H, int H_k, int dk, int dv, int chunk, const int32_t* cu_seqlens,
-                                           int n_seqs, int io_dtype, float scale, int flags, void* workspace,
-                                           size_t workspace_bytes, void* stream) {
+                                           int n_seqs, int io_dtype, float scale, int flags, int segments,
+                                           void* workspace, size_t workspace_bytes, void* stream) {
     g_err[0] = '\0';
     return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
-                   0, nullptr, workspace, workspace_bytes, stream);
+                   segments, 0, nullptr, workspace, workspace_bytes, stream);
 }
 
 static gdn_status snapshots(const void* q, const void* k, const void* v, const float* g, const float* beta,
@@ -2766,8 +2877,9 @@ static gdn_status snapshots(const void* q, const void* k, const void* v, const f
         if (!aligned(snaps, 16)) return fail(GDN_ERR_INVALID_ARG, "snaps %p is not 16-byte aligned", (void*)snaps);
     }
     if ((long)snap_every * CH > (1L << 30)) snap_every = (1 << 30) / CH;   // no snapshot falls inside any prompt
+    if (flags & PLAN_BITS) return fail(GDN_ERR_INVALID_ARG, "flags=%d: snapshots take no plan", flags);
     return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, HK, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
-                   snap_every, snaps, workspace, workspace_bytes, stream);
+                   0, snap_every, snaps, workspace, workspace_bytes, stream);
 }
 
 extern "C" gdn_status gdn_chunk_prefill_snapshots(const void* q, const void* k, const void* v, const float* g,

@@ -45,70 +45,83 @@ def test_version_and_status_strings(L):
 
 
 def test_workspace_bytes():
+    """The sequential plan's workspace: chunk terms per (chunk slot, head), and the ragged sequence table."""
     ws = gdn.gdn_chunk_prefill_workspace_bytes
-    a = ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_BF16)
+
+    def seq(*a):
+        return gdn.gdn_chunk_prefill_workspace_bytes_ex(*a, gdn.GDN_PLAN_SEQUENTIAL, 0)
+    a = seq(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_BF16)
     slots = 160 * 16
     assert a >= slots * (128 * 4 + 2 * 6 * 64 * 8 * 2)      # decay vectors + T, P fragments
-    assert a % 256 == 0
-    assert ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_F32) > a
-    assert ws(1, 10241, 16, 128, 128, 64, 0, gdn.GDN_BF16) > a       # a partial chunk adds a slot
-    assert ws(1, 20000, 16, 128, 128, 64, 8, gdn.GDN_BF16) > ws(1, 20000, 16, 128, 128, 64, 0, gdn.GDN_BF16)
+    assert a % 256 == 0 and ws(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_BF16) % 256 == 0
+    assert seq(1, 10240, 16, 128, 128, 64, 0, gdn.GDN_F32) > a
+    assert seq(1, 10241, 16, 128, 128, 64, 0, gdn.GDN_BF16) > a       # a partial chunk adds a slot
+    assert seq(1, 20000, 16, 128, 128, 64, 8, gdn.GDN_BF16) > seq(1, 20000, 16, 128, 128, 64, 0, gdn.GDN_BF16)
     assert ws(1, 0, 16, 128, 128, 64, 0, gdn.GDN_BF16) == 0
     for bad in [(0, 10, 1, 64, 64, 64, 0, 0), (1, 10, 1, 96, 64, 64, 0, 0), (1, 10, 1, 64, 64, 32, 0, 0),
                 (2, 10, 1, 64, 64, 64, 3, 0), (1, 10, 1, 64, 64, 64, 0, 7), (1, -1, 1, 64, 64, 64, 0, 0)]:
         assert ws(*bad) == 0, bad
 
 
-def test_segment_setting_and_workspace():
-    """gdn_set_prefill_segments: range, previous value, and the workspace it implies
-    (pure host arithmetic; the automatic plan assumes a 256-CU device)."""
-    ws = gdn.gdn_chunk_prefill_workspace_bytes
-    set_ = gdn.gdn_set_prefill_segments
-    prev = set_(0)
-    try:
-        assert set_(0) == 0
-        with pytest.raises(ValueError):
-            set_(-1)
-        with pytest.raises(ValueError):
-            set_(65)
-        assert set_(1) == 0 and set_(0) == 1
-        bf, f32 = gdn.GDN_BF16, gdn.GDN_F32
-        auto = {(io, H): ws(1, 10240, H, 128, 128, 64, 0, io) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
-        set_(1)
-        seq = {(io, H): ws(1, 10240, H, 128, 128, 64, 0, io) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
-        set_(0)
-        # few heads split (the chain would leave most of 256 CUs idle); H = 16 does not
-        # (two runs of every segment would not fit beside each other)
-        for key in [(bf, 1), (bf, 2), (bf, 4), (f32, 1), (f32, 2), (f32, 4), (f32, 8)]:
-            assert auto[key] > seq[key], key
-        for key in [(bf, 16), (f32, 16)]:
-            assert auto[key] == seq[key], key
-        # short bf16 prompts stay sequential (the split's fixed costs outweigh its gain)
-        set_(1)
-        short_seq = ws(1, 2048, 2, 128, 128, 64, 0, bf)
-        set_(0)
-        assert ws(1, 2048, 2, 128, 128, 64, 0, bf) == short_seq
-        # forced: more segments, more workspace; ragged input never splits
-        set_(2)
-        two = ws(1, 4096, 2, 128, 128, 64, 0, bf)
-        rag2 = ws(1, 4096, 2, 128, 128, 64, 3, bf)
-        set_(8)
-        assert ws(1, 4096, 2, 128, 128, 64, 0, bf) > two
-        assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
-        set_(1)
-        assert ws(1, 4096, 2, 128, 128, 64, 3, bf) == rag2
-        # the count a call would use: forced counts need no device; invalid sizes give 0
-        q = gdn.gdn_chunk_prefill_segments
-        set_(3)
-        assert q(1, 4096, 2, 128, 128, 0, bf) == 3
-        assert q(1, 4096, 2, 128, 128, 3, bf) == 1           # ragged: sequential
-        assert q(1, 100, 2, 128, 128, 0, bf) == 2            # two chunks: at most two segments
-        set_(1)
-        assert q(1, 4096, 2, 128, 128, 0, bf) == 1
-        for bad in [(0, 10, 1, 64, 64, 0, 0), (1, 10, 1, 96, 64, 0, 0), (2, 10, 1, 64, 64, 3, 0), (1, 10, 1, 64, 64, 0, 7)]:
-            assert q(*bad) == 0, bad
-    finally:
-        set_(prev)
+def _plan(L, B, T, H, dk, dv, n_seqs, io, flags=0, segments=0, ws_bytes=None):
+    """(form, segments) gdn_chunk_prefill_plan gives; with no device the automatic plan sees 0 CUs."""
+    if ws_bytes is None:
+        ws_bytes = L.gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, 64, n_seqs, io, flags, segments)
+    form = ctypes.c_int(-1)
+    n = L.gdn_chunk_prefill_plan(B, T, H, dk, dv, n_seqs, io, flags, segments, ws_bytes, None, ctypes.byref(form))
+    return form.value, n
+
+
+def test_plans_and_workspace():
+    """The per-call plan (flags + segments) and the workspace each plan needs (pure host arithmetic; the
+    workspace functions size the automatic plan for a 256-CU device)."""
+    L = gdn.lib()
+    ws, wsx = gdn.gdn_chunk_prefill_workspace_bytes, gdn.gdn_chunk_prefill_workspace_bytes_ex
+    bf, f32 = gdn.GDN_BF16, gdn.GDN_F32
+    SEQ, SEG, WIDE = gdn.GDN_PLAN_SEQUENTIAL, gdn.GDN_PLAN_SEGMENTED, gdn.GDN_PLAN_WIDE
+    seq = {(io, H): wsx(1, 10240, H, 128, 128, 64, 0, io, SEQ, 0) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
+    auto = {(io, H): ws(1, 10240, H, 128, 128, 64, 0, io) for io in (bf, f32) for H in (1, 2, 4, 8, 16)}
+    # few heads split (the chain would leave most of 256 CUs idle), and so do 16 bf16 heads (the wide form);
+    # 16 fp32 heads stay sequential (two runs of every segment would not fit beside each other)
+    for key in [(bf, 1), (bf, 2), (bf, 4), (bf, 16), (f32, 1), (f32, 2), (f32, 4), (f32, 8)]:
+        assert auto[key] > seq[key], key
+    assert auto[(f32, 16)] == seq[(f32, 16)]
+    assert wsx(1, 10240, 16, 128, 128, 64, 0, bf, 0, 0) == auto[(bf, 16)]
+    assert auto[(bf, 16)] == wsx(1, 10240, 16, 128, 128, 64, 0, bf, WIDE, 0)
+    # short bf16 prompts stay sequential (the split's fixed costs outweigh its gain)
+    assert ws(1, 2048, 2, 128, 128, 64, 0, bf) == wsx(1, 2048, 2, 128, 128, 64, 0, bf, SEQ, 0)
+    # forced: more segments, more workspace; ragged input never splits
+    two = wsx(1, 4096, 2, 128, 128, 64, 0, bf, SEG, 2)
+    assert wsx(1, 4096, 2, 128, 128, 64, 0, bf, SEG, 8) > two
+    rag = wsx(1, 4096, 2, 128, 128, 64, 3, bf, SEQ, 0)
+    assert wsx(1, 4096, 2, 128, 128, 64, 3, bf, SEG, 8) == rag
+    assert wsx(1, 4096, 4, 128, 128, 64, 0, bf, WIDE, 16) > wsx(1, 4096, 4, 128, 128, 64, 0, bf, WIDE, 4)
+    # the plan a call takes: forced plans need no device
+    assert _plan(L, 1, 10240, 16, 128, 128, 0, bf, WIDE) == (WIDE, 16)
+    assert _plan(L, 1, 10240, 16, 128, 128, 0, bf, WIDE, 5) == (WIDE, 5)
+    assert _plan(L, 1, 10240, 16, 64, 64, 0, bf, WIDE | gdn.GDN_GATE_LOGITS, 3) == (WIDE, 3)
+    assert _plan(L, 1, 4096, 2, 128, 128, 0, bf, SEG, 3) == (SEG, 3)
+    assert _plan(L, 1, 4096, 2, 128, 128, 3, bf, SEG, 3) == (SEQ, 1)      # ragged: sequential
+    assert _plan(L, 1, 100, 2, 128, 128, 0, bf, SEG, 3) == (SEG, 2)       # two chunks: at most two segments
+    assert _plan(L, 1, 64, 2, 128, 128, 0, bf, WIDE, 3) == (SEQ, 1)       # one chunk: nothing to split
+    assert _plan(L, 1, 4096, 2, 128, 128, 0, bf, SEQ) == (SEQ, 1)
+    assert _plan(L, 1, 4096, 2, 128, 128, 0, bf, 0, 1) == (SEQ, 1)
+    # a workspace too small for the split: fewer segments, down to the sequential form
+    small = wsx(1, 10240, 16, 128, 128, 64, 0, bf, SEQ, 0)
+    assert _plan(L, 1, 10240, 16, 128, 128, 0, bf, WIDE, 8, ws_bytes=small) == (SEQ, 1)
+    mid = wsx(1, 10240, 16, 128, 128, 64, 0, bf, WIDE, 4)
+    assert _plan(L, 1, 10240, 16, 128, 128, 0, bf, WIDE, 8, ws_bytes=mid) == (WIDE, 4)
+    # rejected: the wide form needs dense bf16 input with dk == dv and no key normalisation; one plan at a
+    # time; segment counts only with a segmented plan and within 0..64; bad sizes
+    for bad in [(1, 4096, 2, 128, 128, 0, f32, WIDE, 0), (1, 4096, 2, 128, 128, 3, bf, WIDE, 0),
+                (1, 4096, 2, 128, 64, 0, bf, WIDE, 0), (1, 4096, 2, 128, 128, 0, bf, WIDE | gdn.GDN_QK_L2NORM, 0),
+                (1, 4096, 2, 128, 128, 0, bf, SEG | WIDE, 0), (1, 4096, 2, 128, 128, 0, bf, 0, 3),
+                (1, 4096, 2, 128, 128, 0, bf, SEQ, 3), (1, 4096, 2, 128, 128, 0, bf, SEG, 65),
+                (1, 4096, 2, 128, 128, 0, bf, SEG, -1), (1, 4096, 2, 128, 128, 0, bf, 128, 0),
+                (0, 10, 1, 64, 64, 0, bf, 0, 0), (1, 10, 1, 96, 64, 0, bf, 0, 0), (2, 10, 1, 64, 64, 3, bf, 0, 0),
+                (1, 10, 1, 64, 64, 0, 7, 0, 0)]:
+        assert _plan(L, *bad, ws_bytes=1 << 40) == (0, 0), bad
+        assert wsx(bad[0], bad[1], bad[2], bad[3], bad[4], 64, bad[5], bad[6], bad[7], bad[8]) == 0, bad
 
 
 def _prefill(L, **kw):
@@ -248,15 +261,21 @@ def test_binding_grouped_shapes():
 
 def _prefill_ex(L, **kw):
     a = dict(q=A, k=A, v=A, g=A, beta=A, S0=None, o=A, ST=A, B=1, T=128, H=4, Hk=2, dk=64, dv=64, chunk=64,
-             cu=None, n_seqs=0, io=0, scale=1.0, flags=3, ws=A, ws_bytes=1 << 40, stream=None)
+             cu=None, n_seqs=0, io=0, scale=1.0, flags=3, segments=0, ws=A, ws_bytes=1 << 40, stream=None)
     a.update(kw)
     return L.gdn_chunk_prefill_ex(a["q"], a["k"], a["v"], a["g"], a["beta"], a["S0"], a["o"], a["ST"],
                                   a["B"], a["T"], a["H"], a["Hk"], a["dk"], a["dv"], a["chunk"], a["cu"],
-                                  a["n_seqs"], a["io"], a["scale"], a["flags"], a["ws"], a["ws_bytes"], a["stream"])
+                                  a["n_seqs"], a["io"], a["scale"], a["flags"], a["segments"], a["ws"], a["ws_bytes"],
+                                  a["stream"])
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(flags=4), INVALID), (dict(flags=-1), INVALID), (dict(flags=8 | 1), INVALID),
+    (dict(flags=16 | 32), INVALID), (dict(flags=32 | 64), INVALID), (dict(flags=128), INVALID),
+    (dict(segments=-1), INVALID), (dict(segments=65), INVALID), (dict(segments=4), INVALID),
+    (dict(flags=16, segments=4), INVALID),
+    (dict(flags=64, io=0), UNSUPPORTED), (dict(flags=64 | 1, io=1), UNSUPPORTED), (dict(flags=64, io=1, dv=128),
+                                                                                   UNSUPPORTED),
     (dict(Hk=3), INVALID), (dict(dk=96), UNSUPPORTED), (dict(chunk=128), UNSUPPORTED),
     (dict(q=None), INVALID), (dict(ws_bytes=10), WORKSPACE), (dict(io=7), INVALID),
 ])
@@ -313,6 +332,8 @@ def test_snapshots_ex_argument_checks(L):
     assert call(snap_every=0) == INVALID
     assert call(snaps=None) == INVALID
     assert call(flags=4) == INVALID
+    assert call(flags=16) == INVALID           # snapshots take no plan
+    assert call(flags=64) == INVALID
     assert call(Hk=3) == INVALID
     assert call(chunk=32) == UNSUPPORTED
     assert call(ws_bytes=100) == WORKSPACE

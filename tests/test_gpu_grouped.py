@@ -19,22 +19,19 @@ TOL = {"f32": 2e-4, "bf16": 2e-2}
 f64 = inputs.as_f64
 
 
-@pytest.fixture
-def segments():
-    prev = gdn.gdn_set_prefill_segments(0)
-    yield gdn.gdn_set_prefill_segments
-    gdn.gdn_set_prefill_segments(prev)
-
-
 def _dev(x):
     return {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in x.items()}
 
 
-def _check(x, io, label):
+def _check(x, io, label, flags=None, segments=0):
     print("case:", label, flush=True)
     d = _dev(x)
-    o, ST = gdn.gdn_chunk_prefill_grouped(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"],
-                                          cu_seqlens=d["cu_seqlens"])
+    if flags is None:
+        o, ST = gdn.gdn_chunk_prefill_grouped(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"],
+                                              cu_seqlens=d["cu_seqlens"])
+    else:
+        o, ST = gdn.gdn_chunk_prefill_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], flags=flags,
+                                         segments=segments, cu_seqlens=d["cu_seqlens"])
     torch.cuda.synchronize()
     cu = None if x["cu_seqlens"] is None else x["cu_seqlens"].numpy()
     o_ref, ST_ref = oracle.recurrence_grouped(f64(x["q"]), f64(x["k"]), f64(x["v"]), f64(x["g"]), f64(x["beta"]),
@@ -73,11 +70,10 @@ def test_grouped_full_size_one_launch():
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
-def test_grouped_segment_parallel(segments, io):
+def test_grouped_segment_parallel(io):
     """The split form over two value heads sharing one key head (forced to 4 segments)."""
-    segments(4)
     x = inputs.make_prefill(B=1, T=64 * 40 + 9, H=2, H_k=1, dk=128, dv=128, io=io, seed=312, s0_std=0.05)
-    _check(x, io, "grouped segments=4 T=%d H=2 H_k=1 %s" % (64 * 40 + 9, io))
+    _check(x, io, "grouped segments=4 T=%d H=2 H_k=1 %s" % (64 * 40 + 9, io), flags=gdn.GDN_PLAN_SEGMENTED, segments=4)
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])

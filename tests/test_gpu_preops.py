@@ -20,22 +20,15 @@ f64 = inputs.as_f64
 L2, GATES = gdn.GDN_QK_L2NORM, gdn.GDN_GATE_LOGITS
 
 
-@pytest.fixture
-def segments():
-    prev = gdn.gdn_set_prefill_segments(0)
-    yield gdn.gdn_set_prefill_segments
-    gdn.gdn_set_prefill_segments(prev)
-
-
 def _dev(x):
     return {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in x.items()}
 
 
-def _check(x, io, flags, label):
+def _check(x, io, flags, label, segments=0):
     print("case:", label, "flags=%d" % flags, flush=True)
     d = _dev(x)
     o, ST = gdn.gdn_chunk_prefill_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], flags=flags,
-                                     cu_seqlens=d["cu_seqlens"])
+                                     segments=segments, cu_seqlens=d["cu_seqlens"])
     torch.cuda.synchronize()
     cu = None if x["cu_seqlens"] is None else x["cu_seqlens"].numpy()
     o_ref, ST_ref = oracle.recurrence_ex(f64(x["q"]), f64(x["k"]), f64(x["v"]), f64(x["g"]), f64(x["beta"]),
@@ -88,10 +81,9 @@ def test_preops_two_launches():
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
-def test_preops_segment_parallel(segments, io):
-    segments(4)
+def test_preops_segment_parallel(io):
     x = _raw(L2 | GATES, B=1, T=64 * 30 + 5, H=2, dk=128, dv=128, io=io, seed=413, s0_std=0.05)
-    _check(x, io, L2 | GATES, "ex segments=4 T=%d H=2 %s" % (64 * 30 + 5, io))
+    _check(x, io, L2 | GATES | gdn.GDN_PLAN_SEGMENTED, "ex segments=4 T=%d H=2 %s" % (64 * 30 + 5, io), segments=4)
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])

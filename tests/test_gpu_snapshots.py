@@ -84,20 +84,19 @@ def test_snapshots_ragged_and_untouched_rows(io):
     assert oracle.max_rel_err(f64(ST), ST_ref) < TOL[io]
 
 
-def test_snapshots_ignore_the_segment_setting():
-    """A split would not form the states inside segments: the snapshot call stays sequential."""
-    prev = gdn.gdn_set_prefill_segments(4)
-    try:
-        x = inputs.make_prefill(B=1, T=1100, H=2, dk=128, dv=128, io="bf16", seed=43, s0_std=0.05)
-        print("case: snapshots with 4 segments requested", flush=True)
-        o, ST, sn = _snap(x, 4)
-        for j in range(1, sn.shape[1] + 1):
-            assert oracle.max_rel_err(f64(sn[0, j - 1]), _prefix_state(x, 0, j * 256)) < TOL["bf16"], j
-        o_ref, ST_ref = oracle.recurrence(*(f64(x[k]) for k in TOKEN), f64(x["S0"]))
-        assert oracle.max_rel_err(f64(o), o_ref) < TOL["bf16"]
-        assert oracle.max_rel_err(f64(ST), ST_ref) < TOL["bf16"]
-    finally:
-        gdn.gdn_set_prefill_segments(prev)
+def test_snapshots_stay_sequential_where_the_automatic_plan_splits():
+    """A split would not form the states inside segments: on a prompt whose plain call the automatic plan
+    splits (T=4133, two heads), the snapshot call still takes the sequential form and every snapshot is right."""
+    assert gdn.gdn_chunk_prefill_plan(1, 4133, 2, 128, 128, 0, gdn.GDN_BF16)[1] > 1
+    x = inputs.make_prefill(B=1, T=4133, H=2, dk=128, dv=128, io="bf16", seed=43, s0_std=0.05)
+    print("case: snapshots where the automatic plan splits", flush=True)
+    o, ST, sn = _snap(x, 16)
+    assert sn.shape[1] == 4
+    for j in range(1, sn.shape[1] + 1):
+        assert oracle.max_rel_err(f64(sn[0, j - 1]), _prefix_state(x, 0, j * 1024)) < TOL["bf16"], j
+    o_ref, ST_ref = oracle.recurrence(*(f64(x[k]) for k in TOKEN), f64(x["S0"]))
+    assert oracle.max_rel_err(f64(o), o_ref) < TOL["bf16"]
+    assert oracle.max_rel_err(f64(ST), ST_ref) < TOL["bf16"]
 
 
 def test_snapshots_full_size_one_launch():
