@@ -205,6 +205,37 @@ gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const void* v,
                                 void* stream);
 
 /*
+ * Bytes of device scratch that gdn_chunk_prefill_noalloc holds per device.
+ */
+#define GDN_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * gdn_chunk_prefill_ex without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It calls no hipMalloc, hipFree or other
+ * allocating routine: its scratch is a device array of GDN_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) inside the library, one per device, held from the library's first use
+ * on that device until the process ends; its address is looked up on the first
+ * call on each device (the device of `stream`, made current for the lookup).
+ * Arguments, results, plans and errors as gdn_chunk_prefill_ex, with the plan
+ * chosen for a workspace of GDN_NOALLOC_SCRATCH_BYTES; the caller still passes
+ * every input and output.  Sizes whose sequential form needs more scratch than
+ * that (gdn_chunk_prefill_workspace_bytes_ex(..., GDN_PLAN_SEQUENTIAL, 0) >
+ * GDN_NOALLOC_SCRATCH_BYTES): GDN_ERR_WORKSPACE, nothing enqueued.  Nothing in
+ * the scratch needs to start cleared.  Every call on one device shares that
+ * device's scratch: calls that overlap in time on one device (different streams,
+ * or host threads without ordering between their streams) race and give wrong
+ * results; calls ordered on one stream are safe.
+ */
+gdn_status gdn_chunk_prefill_noalloc(const void* q, const void* k, const void* v,
+                                     const float* g, const float* beta, const float* S0,
+                                     void* o, float* S_T,
+                                     int B, int T, int H, int H_k, int dk, int dv, int chunk,
+                                     const int32_t* cu_seqlens, int n_seqs,
+                                     int io_dtype, float scale, int flags, int segments,
+                                     void* stream);
+
+/*
  * The plan gdn_chunk_prefill_ex would take for these arguments, given a
  * workspace of `workspace_bytes` bytes and the compute units of the device of
  * `stream` (NULL: the current device): returns the segments per sequence (1 for

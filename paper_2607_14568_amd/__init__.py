@@ -66,6 +66,8 @@ def lib():
         L.gdn_chunk_prefill_snapshots_ex.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, I, P, P,
                                                      S, P]
         L.gdn_chunk_prefill_snapshots_ex.restype = I
+        L.gdn_chunk_prefill_noalloc.argtypes = [P, P, P, P, P, P, P, P, I, I, I, I, I, I, I, P, I, I, F, I, I, P]
+        L.gdn_chunk_prefill_noalloc.restype = I
         L.gdn_chunk_prefill_plan.argtypes = [I, I, I, I, I, I, I, I, I, S, P, ctypes.POINTER(I)]
         L.gdn_chunk_prefill_plan.restype = I
         L.gdn_decode_step.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, F, P]
@@ -137,7 +139,7 @@ def _stream(device):
 
 
 def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, workspace, grouped=False, flags=0,
-                  segments=0):
+                  segments=0, with_workspace=True):
     if q.dtype not in _IO:
         raise TypeError("q must be float32 or bfloat16")
     io = _IO[q.dtype]
@@ -169,6 +171,8 @@ def _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, 
         S_T = torch.empty((n, H, dv, dk), device=q.device, dtype=torch.float32)
     elif S_T is not None:
         _dev(S_T, "S_T", torch.float32)
+    if not with_workspace:
+        return dict(io=io, B=B, T=T, H=H, HK=HK, dk=dk, dv=dv, n=n, n_seqs=n_seqs, o=o, S_T=S_T)
     need = gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk, n_seqs, io, flags, segments)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
@@ -222,6 +226,23 @@ def gdn_chunk_prefill_ex(q, k, v, g, beta, S0=None, *, flags=0, segments=0, chun
         _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
         a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
         float(scale), int(flags), int(segments), _ptr(a["workspace"]), a["workspace"].numel(), _stream(q.device)))
+    return a["o"], a["S_T"]
+
+
+GDN_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def gdn_chunk_prefill_noalloc(q, k, v, g, beta, S0=None, *, flags=0, segments=0, chunk=64, cu_seqlens=None,
+                              scale=1.0, o=None, S_T=None, store_state=True):
+    """``gdn_chunk_prefill_ex`` on the library's own per-device scratch (no workspace, no device
+    allocation inside the call); see ``gdn_chunk_prefill_noalloc`` in include/gdn.h.  Pass ``o``
+    (and ``S_T``, or ``store_state=False``) to allocate nothing here either."""
+    a = _prefill_args(q, k, v, g, beta, S0, chunk, cu_seqlens, o, S_T, store_state, None, grouped=True,
+                      flags=flags, segments=segments, with_workspace=False)
+    _check(lib().gdn_chunk_prefill_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(a["o"]), _ptr(a["S_T"]),
+        a["B"], a["T"], a["H"], a["HK"], a["dk"], a["dv"], chunk, _ptr(cu_seqlens), a["n_seqs"], a["io"],
+        float(scale), int(flags), int(segments), _stream(q.device)))
     return a["o"], a["S_T"]
 
 

@@ -2328,15 +2328,24 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Compute units of the device a stream's work runs on (cached per device).
-int stream_cus(hipStream_t st) {
-    static std::atomic<int> cached[64];
+// The device a stream's work runs on (NULL: the current device); -1 when there is none.
+int stream_device(hipStream_t st) {
     int dev = -1;
     if (st == nullptr || hipStreamGetDevice(st, &dev) != hipSuccess) {
         (void)hipGetLastError();
-        if (hipGetDevice(&dev) != hipSuccess) return 0;
+        if (hipGetDevice(&dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return -1;
+        }
     }
-    if (dev < 0 || dev >= 64) return 0;
+    return dev >= 0 && dev < 64 ? dev : -1;
+}
+
+// Compute units of the device a stream's work runs on (cached per device).
+int stream_cus(hipStream_t st) {
+    static std::atomic<int> cached[64];
+    const int dev = stream_device(st);
+    if (dev < 0) return 0;
     int n = cached[dev].load(std::memory_order_relaxed);
     if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
@@ -2865,6 +2874,58 @@ extern "C" gdn_status gdn_chunk_prefill_ex(const void* q, const void* k, const v
     g_err[0] = '\0';
     return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
                    segments, 0, nullptr, workspace, workspace_bytes, stream);
+}
+
+// Scratch of gdn_chunk_prefill_noalloc: one copy per device, held by the loaded
+// code object until the process ends.  Host code never uses this name as an
+// address (on the host it is a stand-in); it uses what noalloc_scratch returns.
+static __device__ __align__(256) unsigned char scratch[GDN_NOALLOC_SCRATCH_BYTES];
+
+// Device address of `scratch` on device `dev`, looked up once per device with that
+// device current (each device holds its own copy at its own address); nullptr
+// when the lookup fails.
+static void* noalloc_scratch(int dev) {
+    static std::atomic<void*> addr[64];
+    if (dev < 0 || dev >= 64) return nullptr;
+    void* ptr = addr[dev].load(std::memory_order_acquire);
+    if (ptr != nullptr) return ptr;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || ptr == nullptr) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    addr[dev].store(ptr, std::memory_order_release);
+    return ptr;
+}
+
+extern "C" gdn_status gdn_chunk_prefill_noalloc(const void* q, const void* k, const void* v, const float* g,
+                                                const float* beta, const float* S0, void* o, float* S_T, int B,
+                                                int T, int H, int H_k, int dk, int dv, int chunk,
+                                                const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale,
+                                                int flags, int segments, void* stream) {
+    g_err[0] = '\0';
+    // the least any plan needs is the sequential form's workspace; 0 means arguments
+    // the prefill rejects, which it then reports itself
+    const size_t need = gdn_chunk_prefill_workspace_bytes_ex(B, T, H, dk, dv, chunk, n_seqs, io_dtype,
+                                                            GDN_PLAN_SEQUENTIAL, 0);
+    if (need > GDN_NOALLOC_SCRATCH_BYTES)
+        return fail(GDN_ERR_WORKSPACE, "these sizes need %zu bytes of scratch; gdn_chunk_prefill_noalloc holds %zu",
+                    need, (size_t)GDN_NOALLOC_SCRATCH_BYTES);
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    void* ws = noalloc_scratch(stream_device(hs));
+    if (ws == nullptr) return fail(GDN_ERR_HIP, "no device scratch for the stream's device");
+    return prefill(q, k, v, g, beta, S0, o, S_T, B, T, H, H_k, dk, dv, chunk, cu_seqlens, n_seqs, io_dtype, scale, flags,
+                   segments, 0, nullptr, ws, GDN_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 static gdn_status snapshots(const void* q, const void* k, const void* v, const float* g, const float* beta,
