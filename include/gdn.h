@@ -49,7 +49,9 @@ typedef enum gdn_status {
     GDN_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size or dtype      */
     GDN_ERR_UNSUPPORTED = 2,   /* valid but not implemented (dk, dv, chunk)       */
     GDN_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required      */
-    GDN_ERR_HIP = 4            /* a HIP launch/runtime call failed                */
+    GDN_ERR_HIP = 4,           /* a HIP launch/runtime call failed                */
+    GDN_ERR_WAIT = 5           /* a bounded wait between the library's own
+                                  workgroups gave up (gdn_workspace_status)       */
 } gdn_status;
 
 typedef enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
@@ -61,7 +63,8 @@ typedef enum gdn_flags {
     GDN_GATE_LOGITS = 2,       /* g and beta arrive as logits a, b: g = -softplus(a), beta = sigmoid(b) */
     GDN_PLAN_SEQUENTIAL = 16,  /* one chain over every chunk of a sequence                             */
     GDN_PLAN_SEGMENTED = 32,   /* segment-parallel, narrow: one workgroup per 16 state rows             */
-    GDN_PLAN_WIDE = 64         /* segment-parallel, wide: a workgroup holds a whole state               */
+    GDN_PLAN_WIDE = 64,        /* segment-parallel, wide: a workgroup holds a whole state               */
+    GDN_TEST_WITHHOLD = 256    /* test only: forces the failure path of the one-launch form's wait      */
 } gdn_flags;
 
 /* Library version, (major << 16) | minor. */
@@ -72,6 +75,32 @@ const char* gdn_status_string(int status);
 
 /* Thread-local description of the last non-OK status on this thread ("" if none). */
 const char* gdn_last_error_message(void);
+
+/*
+ * Status of the calls made with this workspace (its first 8 bytes), for the
+ * one-launch form of the bf16 sequential prefill.  There the chunk-terms
+ * workgroups publish each chunk's terms with a per-call tag and the chain
+ * workgroups of the same launch wait for it, polling at most 2^22 times per
+ * call (seconds).  The chunk-terms workgroups never wait and are dispatched
+ * first, so the bound is reached only when they cannot run (the device held by
+ * other work for that long).  A chain that gives up stores the call's tag in
+ * the workspace's status word and writes NaN to the rest of its outputs and to
+ * its final state; the call itself has already returned GDN_OK.
+ *
+ * This function waits for `stream` (NULL: the default stream), reads the word,
+ * and returns GDN_ERR_WAIT if a call of this process on this workspace gave up
+ * since the last check (and clears the word), else GDN_OK.  `workspace` NULL
+ * checks the scratch of gdn_chunk_prefill_noalloc on the device of `stream`.
+ * A workspace of fewer than 8 bytes (calls that needed none) is always GDN_OK.
+ * GDN_ERR_HIP if a HIP call fails.  Not for use under graph capture.
+ *
+ * GDN_TEST_WITHHOLD (a flag of the _ex entry points, for tests of this path):
+ * in the one-launch form the chunk-terms workgroups publish nothing and the
+ * chain polls at most 1024 times, so every chain gives up, every kernel still
+ * exits normally, the outputs are NaN and this function reports GDN_ERR_WAIT.
+ * Calls that do not take the one-launch form ignore it.
+ */
+gdn_status gdn_workspace_status(const void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Workspace (device scratch, bytes) that gdn_chunk_prefill needs for these
@@ -116,7 +145,8 @@ size_t gdn_chunk_prefill_workspace_bytes_ex(int B, int T, int H, int dk, int dv,
  *   scale    multiplies q (o_t = S_t (scale q_t)); 1.0f gives the plain rule
  *   workspace / workspace_bytes   device scratch of at least
  *            gdn_chunk_prefill_workspace_bytes(...) bytes, 256-byte aligned; its
- *            contents on entry are ignored and on exit are unspecified.
+ *            contents on entry are ignored, except its first 8 bytes (the
+ *            status word of gdn_workspace_status), and on exit are unspecified.
  */
 gdn_status gdn_chunk_prefill(const void* q, const void* k, const void* v,
                              const float* g, const float* beta, const float* S0,

@@ -20,6 +20,7 @@ __all__ = [
     "GDN_PLAN_SEQUENTIAL", "GDN_PLAN_SEGMENTED", "GDN_PLAN_WIDE",
     "gdn_chunk_prefill_grouped", "gdn_decode_step_grouped", "gdn_chunk_prefill_ex", "gdn_decode_step_ex",
     "GDN_QK_L2NORM", "GDN_GATE_LOGITS", "gdn_attention_prefill", "gdn_chunk_prefill_snapshots_ex",
+    "gdn_workspace_status", "GDN_ERR_WAIT", "GDN_TEST_WITHHOLD",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -28,6 +29,8 @@ LIB_PATH = os.path.join(_HERE, "libgdn.so")
 GDN_F32, GDN_BF16 = 0, 1
 GDN_QK_L2NORM, GDN_GATE_LOGITS = 1, 2
 GDN_PLAN_SEQUENTIAL, GDN_PLAN_SEGMENTED, GDN_PLAN_WIDE = 16, 32, 64
+GDN_TEST_WITHHOLD = 256
+GDN_ERR_WAIT = 5
 _IO = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
 _lib = None
 
@@ -78,6 +81,8 @@ def lib():
         L.gdn_decode_step_ex.restype = I
         L.gdn_attention_prefill.argtypes = [P, P, P, P, I, I, I, I, I, P, I, I, F, P]
         L.gdn_attention_prefill.restype = I
+        L.gdn_workspace_status.argtypes = [P, S, P]
+        L.gdn_workspace_status.restype = I
         _lib = L
     return _lib
 
@@ -93,6 +98,19 @@ def gdn_status_string(status: int) -> str:
 def _check(status):
     if status != 0:
         raise GdnError(status, lib().gdn_last_error_message().decode())
+
+
+def gdn_workspace_status(workspace=None, device=None):
+    """Waits for the current stream and raises GdnError(GDN_ERR_WAIT) if a one-launch prefill on ``workspace``
+    (a uint8 CUDA tensor; None: the scratch of ``gdn_chunk_prefill_noalloc``) gave up waiting for its chunk terms
+    since the last check (the word is then cleared)."""
+    if workspace is None:
+        dev = torch.device("cuda", torch.cuda.current_device() if device is None else device)
+        _check(lib().gdn_workspace_status(None, 0, _stream(dev)))
+    else:
+        _dev(workspace, "workspace")
+        _check(lib().gdn_workspace_status(_ptr(workspace), workspace.numel() * workspace.element_size(),
+                                          _stream(workspace.device)))
 
 
 def gdn_chunk_prefill_workspace_bytes(B, T, H, dk, dv, chunk=64, n_seqs=0, io_dtype=GDN_BF16) -> int:

@@ -130,6 +130,9 @@ struct Params {
     void* wsP;           // [slot][H][64][64] io type
     uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
     uint64_t epoch;      // per-call tag of those flags
+    uint64_t* status;    // fused bf16 launch: the workspace's status word (= epoch when a wait gave up)
+    int wait_bound;      // fused bf16 launch: most flag polls of one chain workgroup in the call
+    int withhold;        // fused bf16 launch: chunk terms publish nothing (GDN_TEST_WITHHOLD)
     int npw;             // fused bf16 launch: chunk-terms workgroups ahead of the chain workgroups
     int xcd_items;       // fused bf16 launch: chunk-terms items assigned by XCD (dense, 8 | H, 8 | npw)
     float scale;
@@ -846,6 +849,7 @@ template <int DK> struct ChainLds {
     bf16x8 sRf[2][2][64];
     floatx4 sY[2][2][64];         // each chain wave's share of X_{c+1} for the other wave's token tiles
     bf16_t sQ[2][2][32 * DK];     // Q rows of each output wave, by chunk parity
+    int failed;                   // one launch: a wait for chunk terms gave up (set by the flag poller)
 };
 
 // Chain workgroup `bid`.  FUSED: the chunk terms come from workgroups of the
@@ -918,8 +922,22 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
         // loaders wait on their own copies only): chunks 0..2 before barrier P,
         // chunk 3 before the first chunk, chunk c+4 during chunk c.  The loaders'
         // copies of a chunk follow its observation through the barriers.
-        int spins = 1 << 22;   // one bound on the polls of the whole call (each a memory round trip and a short
-                               // sleep: seconds in all); the chunk-terms workgroups never wait, so it is not reached
+        // One bound on the polls of the whole call (each a memory round trip and a
+        // short sleep: seconds in all at the default 2^22).  The chunk-terms
+        // workgroups never wait and come first in the grid, so it is reached only
+        // when they cannot run; then this workgroup reports instead of computing on
+        // unpublished terms: the call's tag goes to the workspace's status word and
+        // the output and chain waves, which read `failed` after the next barrier,
+        // write NaN from there on.
+        // The flag is a relaxed atomic: ordering comes from the cache-bypassing
+        // (sc0 sc1) accesses on both sides -- the writer drains its bypassing stores
+        // (vmcnt 0) before a barrier and the flag store, and the loaders read the terms
+        // with bypassing loads after a barrier that follows this wave's observation
+        // (lds_barrier is also a compiler memory barrier).  Acquire/release at agent
+        // scope would add an L2 invalidate per poll and an L2 writeback per publication
+        // on top of that; measured on the 10k 16-head call, 252 and 212 us against 141.
+        int spins = p.wait_bound;
+        if (lane == 0) lds.failed = 0;
         auto seen = [&](int c) {
             return __hip_atomic_load(&p.flags[slot(c)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == p.epoch;
         };
@@ -928,6 +946,10 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                 --spins;
                 __builtin_amdgcn_s_sleep(2);
                 ok = seen(c);
+            }
+            if (!ok && lane == 0) {
+                lds.failed = 1;
+                __hip_atomic_store(p.status, p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
             }
         };
         if (FUSED && nc > 0)
@@ -1200,6 +1222,9 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
 #pragma unroll
                     for (int e = 0; e < 4; ++e) st[(long)(chan(w * HMD + m) + e) * DV] = from_f<bf16_t>(acc[m][e]);
             } else if (p.ST) {
+                if (FUSED && lds.failed)
+#pragma unroll
+                    for (int m = 0; m < HMD; ++m) acc[m] = floatx4{__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf("")};
 #pragma unroll
                 for (int m = 0; m < HMD; ++m)
                     *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(w * HMD + m)) = acc[m];
@@ -1285,7 +1310,8 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
                         op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf0, pa[2 * i], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
                         op = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rf1, pa[2 * i + 1], op, 0, 0, 0);
                     }
-                    const floatx4 ov = p.scale * (gm * oq + op);   // value channels 4 lg .. 4 lg + 3 of token tok
+                    floatx4 ov = p.scale * (gm * oq + op);   // value channels 4 lg .. 4 lg + 3 of token tok
+                    if (FUSED && lds.failed) ov = floatx4{__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf("")};
                     ovs[i] = __builtin_bit_cast(int2v, __builtin_convertvector(ov, bf16x4));
                     if constexpr (!FUSED) store_o(i);
                 }
@@ -1670,7 +1696,8 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     if constexpr (FUSED) {   // publish: every wave's stores are complete before the flag is set
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        if (tid == 0 && store) __hip_atomic_store(&p.flags[slot], p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (tid == 0 && store && !p.withhold)   // (relaxed: see the flag poller of state_chain_bf16)
+            __hip_atomic_store(&p.flags[slot], p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 
@@ -2316,8 +2343,12 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     L->slots = n_seqs > 0 ? cpt + n_seqs : (long)B * cpt;
     if (L->slots * (long)H > (1L << 24)) return false;
     const size_t per = (size_t)L->slots * H;
-    L->meta = 0;
-    L->G = n_seqs > 0 ? round_up(((size_t)4 * (n_seqs + 1) + 2 * (size_t)(cpt + 2)) * sizeof(int32_t), 256) : 0;
+    if (per == 0) {   // no chunk: nothing to keep (not even the status word)
+        L->meta = L->G = L->T = L->P = L->F = L->total = 0;
+        return true;
+    }
+    L->meta = 256;   // bytes [0, 8): the status word (gdn_workspace_status)
+    L->G = L->meta + (n_seqs > 0 ? round_up(((size_t)4 * (n_seqs + 1) + 2 * (size_t)(cpt + 2)) * sizeof(int32_t), 256) : 0);
     L->T = L->G + round_up(per * GS * sizeof(float), 256);
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
@@ -2357,15 +2388,18 @@ int stream_cus(hipStream_t st) {
 // Tag of one call's chunk-term flags: a per-process random high half and a call
 // counter, never 0 or all ones (what a cleared or 0xFF-filled workspace holds).
 // Safe to call from several host threads at once.
-uint64_t next_epoch() {
+uint64_t epoch_salt() {
     static const uint64_t salt = [] {
         static int anchor;
         uint64_t x = (uint64_t)(uintptr_t)&anchor ^ ((uint64_t)time(nullptr) << 20) ^ 0x9e3779b97f4a7c15ull;
         x ^= x >> 33; x *= 0xff51afd7ed558ccdull; x ^= x >> 33;
         return (x & 0x7ffffffeull) + 1;
     }();
+    return salt;
+}
+uint64_t next_epoch() {
     static std::atomic<uint64_t> counter{0};
-    return (salt << 32) | (uint32_t)(counter.fetch_add(1, std::memory_order_relaxed) + 1);
+    return (epoch_salt() << 32) | (uint32_t)(counter.fetch_add(1, std::memory_order_relaxed) + 1);
 }
 
 template <typename IO, int DK, bool SNAP = false, bool NORM = false>
@@ -2438,6 +2472,14 @@ struct SegCost {
 };
 constexpr SegCost COST_BF16 = {17.0, 0.73, 28.5, 3.6e-4, 1.4};
 constexpr SegCost COST_F32 = {12.0, 4.2, 35.5, 1.7e-3, 2.6};
+// The wide form (dense bf16, 16 segments, every pass one workgroup per
+// (sequence, segment, head)): a fixed part (four launches, each pass's first
+// loads) and a cost per chunk of a sequence that grows with the units it runs
+// beside, from timings at T = 2048..10240 and B H = 1..16.
+struct WideCost {
+    double fixed, chunk, chunk_per_unit;
+};
+constexpr WideCost COST_WIDE = {46.0, 0.30, 0.019};
 
 SegPlan split_plan(int form, int nc, int P) {
     SegPlan x;
@@ -2474,7 +2516,6 @@ SegPlan choose_plan(int B, int T, int H, int dk, int dv, int n_seqs, int io, int
     const bool wide = wide_applies(n_seqs, io, dk, dv, pre);
     if (form_req == FORM_WIDE) return wide ? split_plan(FORM_WIDE, nc, seg_req > 0 ? seg_req : wide_auto_P(B, H, nc))
                                            : SegPlan{};
-    if (form_req == FORM_AUTO && wide && (long)B * H >= 8 && nc >= 32) return split_plan(FORM_WIDE, nc, wide_auto_P(B, H, nc));
     if (form_req == FORM_SEG && seg_req > 1) return split_plan(FORM_SEG, nc, seg_req);
     if (cus <= 0) return SegPlan{};
     const SegCost& k = io == GDN_BF16 ? COST_BF16 : COST_F32;
@@ -2488,6 +2529,10 @@ SegPlan choose_plan(int B, int T, int H, int dk, int dv, int n_seqs, int io, int
         const double t = k.seg_fixed + k.per_token_head * B * H * (double)T +
                          k.chunk * x.L * rounds((long)B * P * H * ((dv + dk) / SL)) + k.per_segment * P;
         if (t < best) { best = t; best_plan = x; }
+    }
+    if (form_req == FORM_AUTO && wide) {
+        const double t = COST_WIDE.fixed + nc * (COST_WIDE.chunk + COST_WIDE.chunk_per_unit * (double)B * H);
+        if (t < best) best_plan = split_plan(FORM_WIDE, nc, wide_auto_P(B, H, nc));
     }
     return best_plan;
 }
@@ -2612,6 +2657,7 @@ extern "C" const char* gdn_status_string(int s) {
         case GDN_ERR_UNSUPPORTED: return "GDN_ERR_UNSUPPORTED";
         case GDN_ERR_WORKSPACE: return "GDN_ERR_WORKSPACE";
         case GDN_ERR_HIP: return "GDN_ERR_HIP";
+        case GDN_ERR_WAIT: return "GDN_ERR_WAIT";
         default: return "unknown status";
     }
 }
@@ -2630,7 +2676,7 @@ static bool sizes_ok(int B, int T, int H, int dk, int dv, int chunk, int n_seqs,
     if (B < 1 || T < 0 || H < 1 || chunk != CH || n_seqs < 0 || (n_seqs > 0 && B != 1)) return false;
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return false;
     if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return false;
-    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS)) return false;
+    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS | GDN_TEST_WITHHOLD)) return false;
     const int pb = flags & PLAN_BITS;
     if (pb & (pb - 1)) return false;   // at most one plan
     if (segments < 0 || segments > SEG_MAX) return false;
@@ -2670,7 +2716,8 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
                           const float* S0, void* o, float* S_T, int B, int T, int H, int HK, int dk, int dv, int chunk,
                           const int32_t* cu_seqlens, int n_seqs, int io_dtype, float scale, int flags, int segments,
                           int snap_every, float* snaps, void* workspace, size_t workspace_bytes, void* stream) {
-    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", flags);
+    if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS | GDN_TEST_WITHHOLD))
+        return fail(GDN_ERR_INVALID_ARG, "flags=%d: unknown bits", flags);
     const int pb = flags & PLAN_BITS, pre = flags & (PRE_L2 | PRE_GATES), form_req = plan_form(flags);
     if (pb & (pb - 1)) return fail(GDN_ERR_INVALID_ARG, "flags=%d: more than one plan", flags);
     if (segments < 0 || segments > SEG_MAX)
@@ -2724,7 +2771,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.NC = (T + CH - 1) / CH;
     p.cu = cu_seqlens;
     char* ws = reinterpret_cast<char*>(workspace);
-    p.seq_start = p.ragged ? reinterpret_cast<int32_t*>(ws) : nullptr;
+    p.seq_start = p.ragged ? reinterpret_cast<int32_t*>(ws + L.meta) : nullptr;
     p.seq_len = p.ragged ? p.seq_start + (n_seqs + 1) : nullptr;
     p.chunk_off = p.ragged ? p.seq_len + (n_seqs + 1) : nullptr;
     p.seq_perm = p.ragged ? p.chunk_off + (n_seqs + 1) : nullptr;
@@ -2735,6 +2782,9 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.wsP = ws + L.P;
     p.flags = reinterpret_cast<uint64_t*>(ws + L.F);
     p.epoch = 0;
+    p.status = reinterpret_cast<uint64_t*>(ws);
+    p.wait_bound = (flags & GDN_TEST_WITHHOLD) ? 1 << 10 : 1 << 22;
+    p.withhold = (flags & GDN_TEST_WITHHOLD) != 0;
     p.npw = 0;
     p.xcd_items = 0;
     p.scale = scale;
@@ -2742,7 +2792,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.snaps = snaps;
     p.snap_every = snap_every;
     p.n_snap = snap_every > 0 ? (T - 1) / (snap_every * CH) : 0;
-    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.flags = nullptr; }
+    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.flags = nullptr; p.status = nullptr; }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
@@ -2792,7 +2842,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
         r.cpt = (r.T + CH - 1) / CH; r.NC = r.cpt;
         r.cu = nullptr;
         r.S0 = sq.S0seg; r.ST = const_cast<float*>(sq.N);
-        r.seq_start = reinterpret_cast<int32_t*>(ws);
+        r.seq_start = reinterpret_cast<int32_t*>(ws + S.base.meta);
         r.seq_len = r.seq_start + (nseg + 1);
         r.chunk_off = r.seq_len + (nseg + 1);
         r.seq_perm = r.chunk_off + (nseg + 1);
@@ -2906,6 +2956,29 @@ static void* noalloc_scratch(int dev) {
     }
     addr[dev].store(ptr, std::memory_order_release);
     return ptr;
+}
+
+extern "C" gdn_status gdn_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    const void* ws = workspace;
+    if (ws == nullptr) {
+        const int dev = stream_device(hs);
+        ws = dev >= 0 ? noalloc_scratch(dev) : nullptr;
+        if (ws == nullptr) return fail(GDN_ERR_HIP, "no device scratch for the stream's device");
+    } else if (workspace_bytes < sizeof(uint64_t)) {
+        return GDN_OK;
+    }
+    uint64_t word = 0;
+    hipError_t e = hipMemcpyAsync(&word, ws, sizeof(word), hipMemcpyDeviceToHost, hs);
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return fail(GDN_ERR_HIP, "reading the status word: %s", hipGetErrorString(e));
+    if ((word >> 32) != epoch_salt()) return GDN_OK;   // no call of this process gave up here
+    e = hipMemsetAsync(const_cast<void*>(ws), 0, sizeof(word), hs);
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return fail(GDN_ERR_HIP, "clearing the status word: %s", hipGetErrorString(e));
+    return fail(GDN_ERR_WAIT, "a chain workgroup of call %u gave up waiting for chunk terms; its outputs are NaN",
+                (unsigned)(word & 0xffffffffu));
 }
 
 extern "C" gdn_status gdn_chunk_prefill_noalloc(const void* q, const void* k, const void* v, const float* g,

@@ -48,7 +48,7 @@ struct WideParams {
     bf16_t* o;
     const float* S0;      // [B, H, D, D] or null (zero)
     float* N;             // [B, P, H, D, D]: value runs' final states
-    bf16_t* Mhi;          // [B, P, H, D, D]: identity runs' final states transposed (key channel, identity row)
+    bf16_t* Mhi;          // [B, P, H, D, D]: identity runs' final states transposed, in the scan's operand order
     bf16_t* Mlo;          //   ... the part the high bf16 part leaves
     float* X;             // [B, P, H, D, D]: states entering the segments (X_0 = S0)
     float* ST;            // [B, H, D, D] or null
@@ -395,10 +395,16 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
         }
         lds_barrier();
         if (run == WIDE_IDENT && active) {
+            // stored in the scan's operand order: 16-byte piece j of the matrix is lane j % 64 of
+            // block j / 64 = (column tile w, contraction block kk); that lane's 8 values are
+            // M_p^T[16 w + lane % 16][32 kk + 8 (lane / 16) ..], so every scan load is 1 KB contiguous
             const long base = ((long)(b * p.P + seg) * H + h) * mat;
-            for (int i = tid - 64 * (NW / 2); i < DK * DK / 8; i += 64 * (NW / 2)) {
-                *reinterpret_cast<bf16x8*>(p.Mhi + base + 8 * i) = *reinterpret_cast<const bf16x8*>(tH + 8 * i);
-                *reinterpret_cast<bf16x8*>(p.Mlo + base + 8 * i) = *reinterpret_cast<const bf16x8*>(tL + 8 * i);
+            for (int j = tid - 64 * (NW / 2); j < DK * DK / 8; j += 64 * (NW / 2)) {
+                const int blk = j >> 6, ln = j & 63;
+                const int c = 16 * (blk / NKD) + (ln & 15), q = 4 * (blk % NKD) + (ln >> 4);
+                const int i = c * (DK / 8) + q;   // piece of the [key channel][identity row] transpose
+                *reinterpret_cast<bf16x8*>(p.Mhi + base + 8 * j) = *reinterpret_cast<const bf16x8*>(tH + 8 * i);
+                *reinterpret_cast<bf16x8*>(p.Mlo + base + 8 * j) = *reinterpret_cast<const bf16x8*>(tL + 8 * i);
             }
         }
     }
@@ -426,8 +432,10 @@ __global__ __launch_bounds__(4 * DK) __attribute__((amdgpu_waves_per_eu(1, 2))) 
 // states X (16 x DK fp32) sit in LDS; wave w forms column tile w of
 // X_p M_p + N_p.  A product of an fp32 X and M_p = M_hi + M_lo is taken as
 // X_hi M_hi + X_hi M_lo + X_lo M_hi on bf16 MFMA (X_lo = X - X_hi): each term
-// rounds at about 2^-16 relative, far below bf16.  M_p arrives transposed, so a
-// lane's operand is one 16-byte run.  All 16-row slices of one (sequence, head)
+// rounds at about 2^-16 relative, far below bf16.  M_p arrives transposed and in
+// operand order, so a lane's operand is one 16-byte run and a wave's load one
+// contiguous kilobyte (lanes reading 16 different rows would touch 16 cache lines
+// per load, which runs the load path at a third of its rate).  All 16-row slices of one (sequence, head)
 // run on one XCD, whose L2 serves their reads of M_p.
 template <int DK>
 __global__ __launch_bounds__(DK * 4) void k_wide_scan(WideParams p) {
@@ -464,12 +472,12 @@ __global__ __launch_bounds__(DK * 4) void k_wide_scan(WideParams p) {
     auto load = [&](int seg, auto D) {
         constexpr int d = decltype(D)::value;
         seg = max(1, min(seg, P - 2));
-        const bf16_t* mh = p.Mhi + at(seg) + (long)col * DK;
-        const bf16_t* ml = p.Mlo + at(seg) + (long)col * DK;
+        const bf16_t* mh = p.Mhi + at(seg) + (long)(wave * NKD * 64 + lane) * 8;
+        const bf16_t* ml = p.Mlo + at(seg) + (long)(wave * NKD * 64 + lane) * 8;
 #pragma unroll
         for (int kk = 0; kk < NKD; ++kk) {
-            bh[d][kk] = *reinterpret_cast<const bf16x8*>(mh + 32 * kk + 8 * lg);
-            bl[d][kk] = *reinterpret_cast<const bf16x8*>(ml + 32 * kk + 8 * lg);
+            bh[d][kk] = *reinterpret_cast<const bf16x8*>(mh + kk * 64 * 8);
+            bl[d][kk] = *reinterpret_cast<const bf16x8*>(ml + kk * 64 * 8);
         }
         const float* np = p.N + at(seg) + rows0;
 #pragma unroll
@@ -483,7 +491,8 @@ __global__ __launch_bounds__(DK * 4) void k_wide_scan(WideParams p) {
     int cur = 0;
     auto step = [&](int seg, auto D) {   // X_{seg+1} = X_seg M_seg + N_seg
         constexpr int d = decltype(D)::value;
-        floatx4 acc = nf[d];
+        // three independent accumulations (high x high, high x low, low x high), summed at the end
+        floatx4 acc = nf[d], a1 = {0.f, 0.f, 0.f, 0.f}, a2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < NKD; ++kk) {
             const floatx4 x0 = *reinterpret_cast<const floatx4*>(&sX[cur][l16][32 * kk + 8 * lg]);
@@ -497,9 +506,10 @@ __global__ __launch_bounds__(DK * 4) void k_wide_scan(WideParams p) {
             }
             const bf16x8 xl = pack_bf16(r0, r1);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, bh[d][kk], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, bl[d][kk], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl, bh[d][kk], acc, 0, 0, 0);
+            a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, bl[d][kk], a1, 0, 0, 0);
+            a2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl, bh[d][kk], a2, 0, 0, 0);
         }
+        acc += a1 + a2;
         load(seg + R, D);
 #pragma unroll
         for (int e = 0; e < 4; ++e) sX[cur ^ 1][4 * lg + e][col] = acc[e];

@@ -106,10 +106,12 @@ def test_segmented_in_place_state():
 
 
 def test_headline_shape_plans():
-    """16 heads at T=10240: bf16 io takes the wide form; fp32 io stays sequential (two runs of two narrow
-    segments would not fit beside each other); the narrow split alone is not chosen for either."""
-    assert gdn.gdn_chunk_prefill_plan(1, 10240, 16, 128, 128, 0, gdn.GDN_BF16) == (gdn.GDN_PLAN_WIDE, 16)
+    """16 heads at T=10240 stay sequential in both io types (the split forms' extra work outweighs the CUs
+    they would fill); 8 bf16 heads take the wide form, 2 take the narrow split."""
+    assert gdn.gdn_chunk_prefill_plan(1, 10240, 16, 128, 128, 0, gdn.GDN_BF16) == (gdn.GDN_PLAN_SEQUENTIAL, 1)
     assert gdn.gdn_chunk_prefill_plan(1, 10240, 16, 128, 128, 0, gdn.GDN_F32) == (gdn.GDN_PLAN_SEQUENTIAL, 1)
+    assert gdn.gdn_chunk_prefill_plan(1, 10240, 8, 128, 128, 0, gdn.GDN_BF16) == (gdn.GDN_PLAN_WIDE, 16)
+    assert gdn.gdn_chunk_prefill_plan(1, 10240, 2, 128, 128, 0, gdn.GDN_BF16)[0] == gdn.GDN_PLAN_SEGMENTED
 
 
 def test_segmented_agrees_with_sequential():

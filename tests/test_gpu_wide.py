@@ -90,9 +90,11 @@ def test_wide_grouped_keys_and_gate_logits():
 
 
 def test_wide_headline_shape():
-    """T=10240, H=16, d=128 bf16 (the timed workload) through the wide plan, and the automatic plan picks it."""
-    form, P = gdn.gdn_chunk_prefill_plan(1, 10240, 16, 128, 128, 0, gdn.GDN_BF16)
+    """T=10240, H=16, d=128 bf16 (the timed workload) through the wide plan, forced (the automatic plan keeps
+    16 heads sequential); at 8 heads the automatic plan takes the wide form by itself."""
+    form, P = gdn.gdn_chunk_prefill_plan(1, 10240, 16, 128, 128, 0, gdn.GDN_BF16, gdn.GDN_PLAN_WIDE)
     assert form == gdn.GDN_PLAN_WIDE and P == 16, (form, P)
+    assert gdn.gdn_chunk_prefill_plan(1, 10240, 8, 128, 128, 0, gdn.GDN_BF16) == (gdn.GDN_PLAN_WIDE, 16)
     _check(inputs.make_workload("prefill_10k_bf16"), 0, "wide prefill_10k_bf16")
 
 
