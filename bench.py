@@ -25,8 +25,8 @@ if ROOT not in sys.path:
 PEAK = {"hbm": 8.0e12, "bf16": 2.5e15, "f32": 157.3e12}   # MI355X published peaks
 
 
-def algorithmic(w, lens, dk, dv, H, io, s0, decode=False):
-    """Bytes and flops the method must move / perform (no padding, no re-reads)."""
+def algorithmic(w, lens, dk, dv, H, io, s0, decode=False, chunk=64):
+    """Bytes and flops the method must move / perform (no padding, no re-reads), for chunks of ``chunk`` tokens."""
     s_io = 2 if io == "bf16" else 4
     ntok = sum(lens)
     if decode:
@@ -37,8 +37,8 @@ def algorithmic(w, lens, dk, dv, H, io, s0, decode=False):
     byts = ntok * H * ((2 * dk + 2 * dv) * s_io + 8) + len(lens) * H * 4 * dv * dk * (2 if s0 else 1)
     flops = 0
     for L in lens:
-        for c0 in range(0, L, 64):
-            n = min(64, L - c0)
+        for c0 in range(0, L, chunk):
+            n = min(chunk, L - c0)
             flops += (n * (n - 1) * dk + n * (n + 1) * dk + n * (n - 1) * (dk + dv) + n * (n + 1) * dv
                       + 6 * n * dk * dv)
     return byts, flops * H
@@ -232,6 +232,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plan", default="auto", choices=["auto", "seq", "seg", "wide"],
                     help="evaluation plan of the prefill (auto: the library chooses)")
+    ap.add_argument("--chunk", type=int, default=64, choices=[16, 32, 64, 128],
+                    help="chunk length of the prefill (64: the tuned kernels; others: the generic path)")
     ap.add_argument("--segments", type=int, default=0,
                     help="segments per sequence of a segmented plan (0: the plan's own count)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -283,11 +285,17 @@ def main():
         n_seqs = 0 if cu is None else len(lens)
         io_code = gdn.GDN_BF16 if w.io == "bf16" else gdn.GDN_F32
         B_, T_ = x_host["q"].shape[0], x_host["q"].shape[1]
-        need = gdn.gdn_chunk_prefill_workspace_bytes_ex(B_, T_, w.H, w.dk, w.dv, 64, n_seqs, io_code, plan_flags,
-                                                        args.segments)
+        need = gdn.gdn_chunk_prefill_workspace_bytes_ex(B_, T_, w.H, w.dk, w.dv, args.chunk, n_seqs, io_code,
+                                                        plan_flags, args.segments)
+        if need == 0 and T_ > 0:
+            print("bench.py: chunk=%d does not take plan %s" % (args.chunk, args.plan), file=sys.stderr)
+            sys.exit(2)
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-        form, segments = gdn.gdn_chunk_prefill_plan(B_, T_, w.H, w.dk, w.dv, n_seqs, io_code, plan_flags,
-                                                    args.segments, need)
+        if args.chunk == 64:
+            form, segments = gdn.gdn_chunk_prefill_plan(B_, T_, w.H, w.dk, w.dv, n_seqs, io_code, plan_flags,
+                                                        args.segments, need)
+        else:   # other chunk lengths: the generic path, sequential
+            form, segments = gdn.GDN_PLAN_SEQUENTIAL, 1
         for d in sets:
             d["o"] = torch.empty_like(d["v"])
             d["S_T"] = torch.empty_like(d["S0"]) if d["S0"] is not None else None
@@ -295,8 +303,8 @@ def main():
         def step(i):
             d = sets[i % len(sets)]
             gdn.gdn_chunk_prefill_ex(d["q"], d["k"], d["v"], d["g"], d["beta"], d["S0"], flags=plan_flags,
-                                     segments=args.segments, cu_seqlens=d["cu_seqlens"], o=d["o"], S_T=d["S_T"],
-                                     workspace=ws)
+                                     segments=args.segments, chunk=args.chunk, cu_seqlens=d["cu_seqlens"], o=d["o"],
+                                     S_T=d["S_T"], workspace=ws)
 
     for i in range(args.warmup):
         step(i)
@@ -324,7 +332,7 @@ def main():
 
     ntok = sum(lens)
     value = ntok / (ms_per_step * 1e-3)
-    byts, flops = algorithmic(w, lens, w.dk, w.dv, w.H, w.io, w.s0_std > 0, decode=w.decode)
+    byts, flops = algorithmic(w, lens, w.dk, w.dv, w.H, w.io, w.s0_std > 0, decode=w.decode, chunk=args.chunk)
     t_hbm = byts / PEAK["hbm"]
     t_mfma = flops / PEAK[w.io]
     bound = "hbm" if t_hbm >= t_mfma else "mfma"
@@ -334,12 +342,15 @@ def main():
         roof = {"bound": "mfma", "achieved": flops / avg_call_s / 1e12, "peak": PEAK[w.io] / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None if w.decode else measured_traffic(w.name)
+    roof["traffic"] = None if (w.decode or args.chunk != 64) else measured_traffic(w.name)
     if w.decode:
         roof["kernel"] = "one gdn_decode_step call"
     elif form == gdn.GDN_PLAN_WIDE:
         roof["kernel"] = ("one gdn_chunk_prefill call, wide segment-parallel form with %d segments (chunk terms, "
                           "segment states, scan, output pass: four launches)" % segments)
+    elif args.chunk != 64:
+        roof["kernel"] = ("one gdn_chunk_prefill call at chunk %d, generic path (decay-masked products, forward "
+                          "substitution, chain: three launches)" % args.chunk)
     elif segments > 1:
         roof["kernel"] = ("one gdn_chunk_prefill call, segment-parallel form with %d segments (segment "
                           "setup, chunk terms, paired chain, scan, output pass)" % segments)
@@ -357,7 +368,7 @@ def main():
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.io, "data": "synthetic",
         "config": {"workload": w.name, "B": len(lens) if w.ragged else w.B, "T": ntok if w.ragged else w.T,
-                   "H": w.H, "dk": w.dk, "dv": w.dv, "chunk": 64, "io": w.io, "state": "fp32",
+                   "H": w.H, "dk": w.dk, "dv": w.dv, "chunk": args.chunk, "io": w.io, "state": "fp32",
                    "parallelism": "none (1 GPU)", "input_sets": len(sets)},
         "roofline": roof,
     }

@@ -141,7 +141,15 @@ size_t gdn_chunk_prefill_workspace_bytes_ex(int B, int T, int H, int dk, int dv,
  *   S0       [n, H, dv, dk] fp32 or NULL    initial state (NULL = zeros); n = B or n_seqs
  *   o        [B, T, H, dv]  io_dtype        output (written)
  *   S_T      [n, H, dv, dk] fp32 or NULL    final state (written unless NULL; may == S0)
- *   dk, dv   64 or 128;  chunk must be 64;  T >= 0;  B, H >= 1
+ *   dk, dv   64 or 128;  T >= 0;  B, H >= 1
+ *   chunk    tokens per chunk: 64 runs the tuned kernels (every plan and
+ *            snapshots); 16, 32 and 128 run a generic path (section 3.2 leaves the
+ *            chunk length free; the result equals the recurrence at every length):
+ *            per (chunk, head) the decay-masked products and the forward
+ *            substitution in fp32, then one chain per (sequence, head, 16 state
+ *            rows) on the vector units -- sequential plan only, no snapshots
+ *            (GDN_ERR_UNSUPPORTED), workspace per (chunk slot, head) of
+ *            16 chunk + 8 chunk^2 bytes; other lengths GDN_ERR_UNSUPPORTED
  *   scale    multiplies q (o_t = S_t (scale q_t)); 1.0f gives the plain rule
  *   workspace / workspace_bytes   device scratch of at least
  *            gdn_chunk_prefill_workspace_bytes(...) bytes, 256-byte aligned; its

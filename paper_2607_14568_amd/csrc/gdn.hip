@@ -117,6 +117,7 @@ struct Params {
     int n_seq;         // dense: B; ragged: number of packed sequences
     int ragged;
     int NC;            // dense: chunks per sequence
+    int C;             // chunk length of the generic path (chunks other than 64)
     const int32_t* cu; // ragged: raw offsets (device)
     int32_t* seq_start;
     int32_t* seq_len;
@@ -225,7 +226,7 @@ __device__ void block_scan(int32_t* x, int n, bool reverse, int* part) {
 // of NSET threads.
 __global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_seq, int T, int32_t* seq_start,
                                                       int32_t* seq_len, int32_t* chunk_off, int32_t* perm,
-                                                      int32_t* prefix, int32_t* ghist, int cpt) {
+                                                      int32_t* prefix, int32_t* ghist, int cpt, int ch) {
     __shared__ int part[NSET];
     __shared__ int scu[NSET + 1];
     __shared__ int shist[8192];
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_
                 const int e = min(max(scu[i + 1], b), T);
                 seq_start[s0 + i] = b;
                 seq_len[s0 + i] = e - b;
-                acc += (e - b + CH - 1) / CH;
+                acc += (e - b + ch - 1) / ch;
                 chunk_off[s0 + i + 1] = acc;
                 b = e;
             }
@@ -256,13 +257,13 @@ __global__ __launch_bounds__(NSET) void k_ragged_setup(const int32_t* cu, int n_
     }
     for (int c = t; c <= cpt + 1; c += NSET) hist[c] = 0;
     __syncthreads();
-    for (int s = t; s < n_seq; s += NSET) atomicAdd(&hist[(seq_len[s] + CH - 1) / CH], 1);   // counts <= cpt
+    for (int s = t; s < n_seq; s += NSET) atomicAdd(&hist[(seq_len[s] + ch - 1) / ch], 1);   // counts <= cpt
     __syncthreads();
     // first rank of each chunk count, longest first: hist[n] <- #sequences with more than n chunks
     block_scan(hist, cpt + 1, true, part);
     for (int c = t; c <= cpt; c += NSET) prefix[c] = hist[c];
     __syncthreads();
-    for (int s = t; s < n_seq; s += NSET) perm[atomicAdd(&hist[(seq_len[s] + CH - 1) / CH], 1)] = s;
+    for (int s = t; s < n_seq; s += NSET) perm[atomicAdd(&hist[(seq_len[s] + ch - 1) / ch], 1)] = s;
     block_scan(prefix, cpt + 1, false, part);
 }
 
@@ -2315,6 +2316,7 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
 }
 
 #include "wide.hip"
+#include "generic.hip"
 
 // ------------------------------------------------------------------ host side
 thread_local char g_err[512] = "";
@@ -2358,6 +2360,50 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Chunk lengths and workspace of the generic path (chunk != 64): the status word,
+// the ragged table, and per (chunk slot, head) 4 C floats (gamma, D, s_k, s_q)
+// and two C x C fp32 matrices (A then W; P then P').
+bool gen_chunk(int chunk) { return chunk == 16 || chunk == 32 || chunk == 128; }
+
+bool gen_layout(int B, int T, int H, int C, int n_seqs, Layout* L) {
+    const long cpt = ((long)T + C - 1) / C;
+    L->slots = n_seqs > 0 ? cpt + n_seqs : (long)B * cpt;
+    if (L->slots * (long)H > (1L << 24)) return false;
+    const size_t per = (size_t)L->slots * H;
+    if (per == 0) {
+        L->meta = L->G = L->T = L->P = L->F = L->total = 0;
+        return true;
+    }
+    L->meta = 256;
+    L->G = L->meta + (n_seqs > 0 ? round_up(((size_t)4 * (n_seqs + 1) + 2 * (size_t)(cpt + 2)) * sizeof(int32_t), 256) : 0);
+    L->T = L->G + round_up(per * 4 * C * sizeof(float), 256);
+    L->P = L->T + round_up(per * C * C * sizeof(float), 256);
+    L->F = L->P + round_up(per * C * C * sizeof(float), 256);
+    L->total = L->F;
+    return true;
+}
+
+template <typename IO, int C, int DK>
+void launch_generic_c(const Params& p, long slots, hipStream_t st) {
+    if (p.ragged)
+        hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start, p.seq_len,
+                           p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt, C);
+    if (slots > 0 && p.T > 0) {
+        hipLaunchKernelGGL((k_gen_gram<IO, C, DK>), dim3((unsigned)(slots * p.H)), dim3(GEN_NT), 0, st, p);
+        hipLaunchKernelGGL((k_gen_solve<C>), dim3((unsigned)(slots * p.H)), dim3(GEN_NT), 0, st, p);
+    }
+    hipLaunchKernelGGL((k_gen_chain<IO, C, DK>), dim3((unsigned)(p.n_seq * p.H * (p.DV / GEN_RS))), dim3(GEN_NT), 0, st, p);
+}
+
+template <typename IO, int DK>
+void launch_generic(const Params& p, long slots, hipStream_t st) {
+    switch (p.C) {
+        case 16: launch_generic_c<IO, 16, DK>(p, slots, st); break;
+        case 32: launch_generic_c<IO, 32, DK>(p, slots, st); break;
+        default: launch_generic_c<IO, 128, DK>(p, slots, st); break;
+    }
+}
 
 // The device a stream's work runs on (NULL: the current device); -1 when there is none.
 int stream_device(hipStream_t st) {
@@ -2406,7 +2452,7 @@ template <typename IO, int DK, bool SNAP = false, bool NORM = false>
 void launch_prefill(Params p, long slots, hipStream_t st) {
     if (p.ragged)
         hipLaunchKernelGGL(k_ragged_setup, dim3(1), dim3(NSET), 0, st, p.cu, p.n_seq, p.T, p.seq_start,
-                           p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt);
+                           p.seq_len, p.chunk_off, p.seq_perm, p.cprefix, p.cprefix + (p.cpt + 2), p.cpt, CH);
     if constexpr (sizeof(IO) == 2) {
         // one launch with the chunk terms formed beside the chain when it leaves
         // a quarter of the compute units free; otherwise the chunk terms first
@@ -2673,7 +2719,8 @@ static gdn_status check_dims(int dk, int dv) {
 
 // Validation shared by the workspace and plan queries; false for arguments the prefill would reject.
 static bool sizes_ok(int B, int T, int H, int dk, int dv, int chunk, int n_seqs, int io_dtype, int flags, int segments) {
-    if (B < 1 || T < 0 || H < 1 || chunk != CH || n_seqs < 0 || (n_seqs > 0 && B != 1)) return false;
+    if (B < 1 || T < 0 || H < 1 || (chunk != CH && !gen_chunk(chunk)) || n_seqs < 0 || (n_seqs > 0 && B != 1))
+        return false;
     if (io_dtype != GDN_F32 && io_dtype != GDN_BF16) return false;
     if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128)) return false;
     if (flags & ~(PRE_L2 | PRE_GATES | PLAN_BITS | GDN_TEST_WITHHOLD)) return false;
@@ -2683,6 +2730,9 @@ static bool sizes_ok(int B, int T, int H, int dk, int dv, int chunk, int n_seqs,
     if (segments > 1 && plan_form(flags) != FORM_SEG && plan_form(flags) != FORM_WIDE) return false;
     if (plan_form(flags) == FORM_WIDE && !wide_applies(n_seqs, io_dtype, dk, dv, flags & PRE_L2)) return false;
     Layout L;
+    if (chunk != CH)   // the generic path: sequential only
+        return (plan_form(flags) == FORM_AUTO || plan_form(flags) == FORM_SEQ) && segments <= 1 &&
+               gen_layout(B, T, H, chunk, n_seqs, &L);
     return ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L);
 }
 
@@ -2690,6 +2740,10 @@ extern "C" size_t gdn_chunk_prefill_workspace_bytes_ex(int B, int T, int H, int 
                                                        int io_dtype, int flags, int segments) {
     if (!sizes_ok(B, T, H, dk, dv, chunk, n_seqs, io_dtype, flags, segments)) return 0;
     Layout L;
+    if (chunk != CH) {
+        gen_layout(B, T, H, chunk, n_seqs, &L);
+        return L.total;
+    }
     ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L);
     const SegPlan sp = choose_plan(B, T, H, dk, dv, n_seqs, io_dtype, flags & PRE_L2, plan_form(flags), segments, PLAN_CUS);
     return std::max(L.total, plan_bytes(B, T, H, dk, dv, n_seqs, io_dtype, sp));
@@ -2732,7 +2786,12 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     gdn_status st = check_dims(dk, dv);
     if (st != GDN_OK) return st;
     if (chunk < 1) return fail(GDN_ERR_INVALID_ARG, "chunk=%d must be positive", chunk);
-    if (chunk != CH) return fail(GDN_ERR_UNSUPPORTED, "chunk=%d: only 64 is implemented", chunk);
+    if (chunk != CH && !gen_chunk(chunk))
+        return fail(GDN_ERR_UNSUPPORTED, "chunk=%d: the chunk length must be 16, 32, 64 or 128", chunk);
+    if (chunk != CH && (form_req == FORM_SEG || form_req == FORM_WIDE || segments > 1))
+        return fail(GDN_ERR_UNSUPPORTED, "chunk=%d: only the sequential plan (the segmented plans need chunk 64)", chunk);
+    if (chunk != CH && snap_every > 0)
+        return fail(GDN_ERR_UNSUPPORTED, "chunk=%d: snapshots need chunk 64", chunk);
     if ((cu_seqlens == nullptr) != (n_seqs == 0))
         return fail(GDN_ERR_INVALID_ARG, "cu_seqlens and n_seqs=%d must be given together", n_seqs);
     if (n_seqs < 0) return fail(GDN_ERR_INVALID_ARG, "n_seqs=%d is negative", n_seqs);
@@ -2754,8 +2813,9 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
         return fail(GDN_ERR_UNSUPPORTED, "GDN_PLAN_WIDE needs dense bf16 input with dk == dv, without GDN_QK_L2NORM");
     if (form_req == FORM_WIDE && snap_every > 0)
         return fail(GDN_ERR_UNSUPPORTED, "GDN_PLAN_WIDE does not take snapshots");
+    const int C = chunk;
     Layout L;
-    if (!ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L))
+    if (!(C == CH ? ws_layout(B, T, H, dk, dv, n_seqs, io_dtype, &L) : gen_layout(B, T, H, C, n_seqs, &L)))
         return fail(GDN_ERR_UNSUPPORTED, "too many chunks x heads for one call");
     if (workspace_bytes < L.total || (L.total > 0 && workspace == nullptr))
         return fail(GDN_ERR_WORKSPACE, "workspace of %zu bytes at %p; %zu bytes needed", workspace_bytes, workspace,
@@ -2768,7 +2828,8 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.HK = HK; p.G = H / HK;
     p.n_seq = n_seq;
     p.ragged = n_seqs > 0;
-    p.NC = (T + CH - 1) / CH;
+    p.NC = (T + C - 1) / C;
+    p.C = C;
     p.cu = cu_seqlens;
     char* ws = reinterpret_cast<char*>(workspace);
     p.seq_start = p.ragged ? reinterpret_cast<int32_t*>(ws + L.meta) : nullptr;
@@ -2776,7 +2837,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.chunk_off = p.ragged ? p.seq_len + (n_seqs + 1) : nullptr;
     p.seq_perm = p.ragged ? p.chunk_off + (n_seqs + 1) : nullptr;
     p.cprefix = p.ragged ? p.seq_perm + (n_seqs + 1) : nullptr;
-    p.cpt = (T + CH - 1) / CH;
+    p.cpt = (T + C - 1) / C;
     p.wsG = reinterpret_cast<float*>(ws + L.G);
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
@@ -2796,6 +2857,18 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
+    if (C != CH) {   // chunk lengths other than 64: the generic path (sequential)
+        if (io_dtype == GDN_BF16) {
+            if (dk == 128) launch_generic<bf16_t, 128>(p, L.slots, hs);
+            else launch_generic<bf16_t, 64>(p, L.slots, hs);
+        } else {
+            if (dk == 128) launch_generic<float, 128>(p, L.slots, hs);
+            else launch_generic<float, 64>(p, L.slots, hs);
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fail(GDN_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+        return GDN_OK;
+    }
     // segment-parallel form when the plan splits and the workspace holds it (never
     // with snapshots: the states inside segments are not formed)
     SegLayout S;

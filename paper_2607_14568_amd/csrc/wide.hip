@@ -186,6 +186,9 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
     // group of products has its LDS reads issued before the products of the
     // group before it, so that their latency hides behind MFMA work.
     auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
+    // carried from a chunk's products to its state update: the K^T operands, D U and gamma_n
+    bf16x8 ka[NMD][2], db[NRT][2];
+    float gn = 0.f;
     auto step = [&](int c, int sl, auto RUN) {
         constexpr int MODE = decltype(RUN)::value;
         const bf16_t* sK = lds.sK[sl];
@@ -254,7 +257,7 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
             fence();
         }
         // W fragments and the first half of the K^T operands of the state update
-        bf16x8 wf[NFRAG], ka[NMD][2];
+        bf16x8 wf[NFRAG];
         auto read_kt = [&](int m0) {
 #pragma unroll
             for (int md = m0; md < m0 + NMD / 2; ++md)
@@ -283,7 +286,6 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
             rb[rt][1] = pack_bf16(r[2], r[3]);
         }
         // D U = W R' (lower triangular: token tile mt takes blocks kk2 <= mt/2)
-        bf16x8 db[NRT][2];
 #pragma unroll
         for (int rt = 0; rt < NRT; ++rt) {
             floatx4 du[4];
@@ -317,21 +319,19 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
         }
         fence();
         read_kt(NMD / 2);
+        gn = lds.sG[sl][CH - 1];
         fence();
-        // S^T <- gamma_n S^T + K^T (D U)
-        const float gn = lds.sG[sl][CH - 1];
-        auto supdate = [&](int m0) {
+    };
+    // S^T <- gamma_n S^T + K^T (D U), from the registers the step left
+    auto supdate = [&] {
 #pragma unroll
-            for (int md = m0; md < m0 + NMD / 2; ++md)
+        for (int md = 0; md < NMD; ++md)
 #pragma unroll
-                for (int rt = 0; rt < NRT; ++rt) {
-                    acc[rt][md] *= gn;
-                    acc[rt][md] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[md][0], db[rt][0], acc[rt][md], 0, 0, 0);
-                    acc[rt][md] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[md][1], db[rt][1], acc[rt][md], 0, 0, 0);
-                }
-        };
-        supdate(0);
-        supdate(NMD / 2);
+            for (int rt = 0; rt < NRT; ++rt) {
+                acc[rt][md] *= gn;
+                acc[rt][md] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[md][0], db[rt][0], acc[rt][md], 0, 0, 0);
+                acc[rt][md] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[md][1], db[rt][1], acc[rt][md], 0, 0, 0);
+            }
     };
 
     // ---- the chunk loop: chunks 0 .. RING-2 ahead of the first (past the last
@@ -340,17 +340,25 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
 #pragma unroll
     for (int j = 0; j < RING - 1; ++j) issue(min(j, nc - 1), j);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI * (RING - 2)) : "memory");
+    // Half of the waves run one phase behind: a chunk's state update goes after the
+    // next barrier (its operands are in registers, so the ring slot may be refilled),
+    // so the two waves sharing a SIMD are in different phases of a chunk (products
+    // beside the update, the R' and D U work beside the products) instead of in step.
+    const bool rot = wave >= NW / 2;
     for (int c = 0; c < nc; ++c) {
         const int sl = c % RING;
         lds_barrier();   // chunk c resident; chunk c-1's slot free
         issue(min(c + RING - 1, nc - 1), (c + RING - 1) % RING);
+        if (rot && c > 0 && active) supdate();   // chunk c-1's
         if (OUT) step(c, sl, Ic<WIDE_OUT>{});
         else if (run == WIDE_VALUE) step(c, sl, Ic<WIDE_VALUE>{});
         else if (active) step(c, sl, Ic<WIDE_IDENT>{});
+        if (!rot && active) supdate();
         // chunk c+1's copies landed (this chunk's output stores were issued after them)
         if (active) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI * (RING - 2) + NSTORE) : "memory");
         else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NI * (RING - 2)) : "memory");
     }
+    if (rot && nc > 0 && active) supdate();
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
     // ---- final states

@@ -58,7 +58,7 @@ def test_workspace_bytes():
     assert seq(1, 10241, 16, 128, 128, 64, 0, gdn.GDN_BF16) > a       # a partial chunk adds a slot
     assert seq(1, 20000, 16, 128, 128, 64, 8, gdn.GDN_BF16) > seq(1, 20000, 16, 128, 128, 64, 0, gdn.GDN_BF16)
     assert ws(1, 0, 16, 128, 128, 64, 0, gdn.GDN_BF16) == 0
-    for bad in [(0, 10, 1, 64, 64, 64, 0, 0), (1, 10, 1, 96, 64, 64, 0, 0), (1, 10, 1, 64, 64, 32, 0, 0),
+    for bad in [(0, 10, 1, 64, 64, 64, 0, 0), (1, 10, 1, 96, 64, 64, 0, 0), (1, 10, 1, 64, 64, 48, 0, 0),
                 (2, 10, 1, 64, 64, 64, 3, 0), (1, 10, 1, 64, 64, 64, 0, 7), (1, -1, 1, 64, 64, 64, 0, 0)]:
         assert ws(*bad) == 0, bad
 
@@ -145,8 +145,8 @@ def _prefill(L, **kw):
     (dict(dk=32, dv=32), UNSUPPORTED),
     (dict(H=1 << 19), UNSUPPORTED),
     (dict(chunk=0), INVALID),
-    (dict(chunk=32), UNSUPPORTED),
-    (dict(chunk=128), UNSUPPORTED),
+    (dict(chunk=48), UNSUPPORTED),
+    (dict(chunk=256), UNSUPPORTED),
     (dict(q=None), INVALID),
     (dict(k=None), INVALID),
     (dict(v=None), INVALID),
@@ -221,7 +221,7 @@ def _prefill_grouped(L, **kw):
     (dict(H=6, Hk=4), INVALID),
     (dict(H=0, Hk=1), INVALID),
     (dict(dk=96), UNSUPPORTED),               # the prefill's own checks still apply
-    (dict(chunk=32), UNSUPPORTED),
+    (dict(chunk=48), UNSUPPORTED),
     (dict(q=A + 8), INVALID),
     (dict(ws_bytes=1000), WORKSPACE),
 ])
@@ -276,7 +276,9 @@ def _prefill_ex(L, **kw):
     (dict(flags=16, segments=4), INVALID),
     (dict(flags=64, io=0), UNSUPPORTED), (dict(flags=64 | 1, io=1), UNSUPPORTED), (dict(flags=64, io=1, dv=128),
                                                                                    UNSUPPORTED),
-    (dict(Hk=3), INVALID), (dict(dk=96), UNSUPPORTED), (dict(chunk=128), UNSUPPORTED),
+    (dict(Hk=3), INVALID), (dict(dk=96), UNSUPPORTED), (dict(chunk=96), UNSUPPORTED),
+    (dict(chunk=32, flags=32), UNSUPPORTED), (dict(chunk=128, flags=64, io=1, dk=128, dv=128), UNSUPPORTED),
+    (dict(chunk=16, flags=16, segments=2), INVALID),
     (dict(q=None), INVALID), (dict(ws_bytes=10), WORKSPACE), (dict(io=7), INVALID),
 ])
 def test_ex_prefill_argument_checks(L, kw, code):
@@ -376,3 +378,28 @@ def test_product_package_does_not_reach_the_oracle():
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in text, fn
     assert "import oracle" not in open(os.path.join(pkg, "inputs.py")).read()
+
+
+def test_generic_chunk_workspace():
+    """Chunk lengths 16, 32 and 128 take the generic path: per (chunk slot, head) 4 C floats and two C x C fp32
+    matrices after the status word (and the ragged table), sequential plan only."""
+    wsx = gdn.gdn_chunk_prefill_workspace_bytes_ex
+    bf, f32 = gdn.GDN_BF16, gdn.GDN_F32
+    rnd = lambda x: (x + 255) // 256 * 256
+    for C in (16, 32, 128):
+        for T, H in ((10240, 16), (1000, 3), (1, 1), (C, 2), (C + 1, 2)):
+            items = -(-T // C) * H
+            want = 256 + rnd(items * 4 * C * 4) + 2 * rnd(items * C * C * 4)
+            for io in (bf, f32):
+                assert wsx(1, T, H, 128, 128, C, 0, io, 0, 0) == want, (C, T, H)
+                assert wsx(1, T, H, 64, 64, C, 0, io, gdn.GDN_PLAN_SEQUENTIAL, 0) == want
+        assert gdn.gdn_chunk_prefill_workspace_bytes(1, 0, 4, 128, 128, C, 0, bf) == 0
+        cpt = -(-1000 // C)
+        items = (cpt + 3) * 2
+        table = rnd((4 * 4 + 2 * (cpt + 2)) * 4)
+        assert wsx(1, 1000, 2, 128, 128, C, 3, bf, 0, 0) == 256 + table + rnd(items * 4 * C * 4) + 2 * rnd(
+            items * C * C * 4)
+        for fl, seg in ((gdn.GDN_PLAN_SEGMENTED, 0), (gdn.GDN_PLAN_WIDE, 0), (gdn.GDN_PLAN_SEGMENTED, 4)):
+            assert wsx(1, 1000, 2, 128, 128, C, 0, bf, fl, seg) == 0, (C, fl, seg)
+    for bad in (0, 8, 48, 96, 256):
+        assert wsx(1, 1000, 2, 128, 128, bad, 0, bf, 0, 0) == 0, bad
