@@ -2,17 +2,13 @@
 
 TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
-This follows the order of the method as the paper describes it in section 3.2
-("A chunked delta-rule scan for the recurrent layers"), in the paper's own
+The steps run in the order of the chunked scan of section 3.2, in the paper's
 state orientation S_p in R^{dk x dv} (the transpose of the [dv, dk] storage
-used everywhere else):
-
-1. inside a chunk of n tokens, two token-token products, K K^T and Q K^T;
-2. a lower-triangular system whose right-hand sides do not depend on the
-   incoming state, resolved by forward substitution;
-3. a few matrix products assembling the per-chunk correction and output;
-4. across chunks the short affine recurrence S_p <- M_c S_p + N_c, with every
-   (M_c, N_c) formed before the recurrence runs.
+used everywhere else).  Per chunk of n tokens: the key-key and query-key
+products; the unit-lower-triangular solve by forward substitution, which needs
+nothing from the state entering the chunk; the products that form the
+correction and the outputs.  Then, once every chunk's (M_c, N_c) exists, the
+inter-chunk step S_p <- M_c S_p + N_c walks the chunks in order.
 
 Derivation (per state column, i.e. per value channel): with
 G_r = sum_{j<=r} g_j, gamma_r = exp(G_r) and Gamma_{ri} = exp(G_r - G_i) for i <= r,
