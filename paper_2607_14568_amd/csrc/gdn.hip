@@ -127,8 +127,9 @@ struct Params {
     int cpt;             // chunks of the longest possible sequence
     float* wsG;          // [slot][H][GS]: gamma_r = exp(G_r), D_r = exp(G_n - G_r) (times s_k,r with PRE_L2
                          // in fp32 io), and with PRE_L2 gamma_r s_k,r and gamma_r s_q,r (s = 1 / |row|)
-    void* wsT;           // [slot][H][64][64] io type
-    void* wsP;           // [slot][H][64][64] io type
+    void* wsT;           // [slot][H]: bf16 io W fragments; fp32 io T as high and low bf16 64 x 64 tiles
+    void* wsP;           // [slot][H]: bf16 io P' fragments; fp32 io P as high and low bf16 64 x 64 tiles
+    void* wsKQ;          // fp32 io: [slot][H][4][64][dk] bf16, K and Q as high and low parts (chain LDS order)
     uint64_t* flags;     // fused bf16 launch: [slot][H], = epoch once the slot's chunk terms are stored
     uint64_t epoch;      // per-call tag of those flags
     uint64_t* status;    // fused bf16 launch: the workspace's status word (= epoch when a wait gave up)
@@ -297,6 +298,96 @@ __device__ __forceinline__ void stage_rows2(IO (*dA)[LD], const IO* sA, IO (*dB)
     }
 }
 
+// ------------------------------------------------------------------ bf16 operand helpers
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef int int4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+constexpr int NT_CHAIN = 512;
+constexpr int RING = 4;
+template <int N> struct Ic { static constexpr int value = N; };
+
+__device__ __forceinline__ bf16x8 pack_bf16(floatx4 a, floatx4 b) {
+    const floatx8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_convertvector(x, bf16x8);
+}
+__device__ __forceinline__ bf16x8 join4(short4v a, short4v b) {
+    const short8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8, x);
+}
+// whole-register select (a runtime index into a register array would be
+// lowered element by element)
+__device__ __forceinline__ bf16x8 sel(bool c, bf16x8 a, bf16x8 b) {
+    return __builtin_bit_cast(bf16x8, c ? __builtin_bit_cast(int4v, a) : __builtin_bit_cast(int4v, b));
+}
+// Transpose read: within each 16-lane group, lane i element e receives element
+// i%4 of the 8 bytes addressed by lane 4e + i/4 of the group.
+__device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
+    typedef __attribute__((address_space(3))) short4v lds_short4v;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(ptr));
+}
+__device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)(uint16_t)x << 16); }
+// Buffer resource over [base, base + bytes); loads past the end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+// AUX: cache policy of the access (0: default; 17 = sc0 sc1: system coherent,
+// bypassing the caches that other workgroups' data could be stale in)
+template <int AUX = 0> __device__ __forceinline__ bf16x8 bload16(__amdgpu_buffer_rsrc_t r, int voff) {
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, AUX));
+}
+// global -> LDS without registers: lane l's 16 (4) bytes land at dst + 16 l (4 l)
+template <int AUX = 0> __device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, 0, 0, AUX);
+}
+template <int AUX = 0> __device__ __forceinline__ void bdma4(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, 0, 0, AUX);
+}
+template <int AUX = 0> __device__ __forceinline__ void bstore16(bf16x8 v, __amdgpu_buffer_rsrc_t r, int voff) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff, 0, AUX);
+}
+template <int AUX = 0> __device__ __forceinline__ void bstore4(float v, __amdgpu_buffer_rsrc_t r, int voff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, AUX);
+}
+// Workgroup barrier ordering LDS traffic only: the wave's own LDS operations
+// complete, the compiler moves no memory access across it, and -- unlike
+// __syncthreads() -- it does not wait for outstanding global loads or stores.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// x = hi + lo with hi = bf16(x), lo = bf16(x - hi): a product of two such pairs
+// taken as hi*hi + hi*lo + lo*hi (the lo*lo term is below 2^-16 of it) gives fp32
+// operands a relative error near 2^-16 from bf16 MFMA with fp32 accumulation
+__device__ __forceinline__ void split8(floatx4 a, floatx4 b, bf16x8& hi, bf16x8& lo) {
+    hi = pack_bf16(a, b);
+    floatx4 ra, rb;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        ra[e] = a[e] - (float)hi[e];
+        rb[e] = b[e] - (float)hi[4 + e];
+    }
+    lo = pack_bf16(ra, rb);
+}
+// The product of two split operands, its three terms into three accumulators (a sum
+// over blocks is then three independent chains, not one): the product is a[0] + a[1] + a[2]
+__device__ __forceinline__ void mma3x(bf16x8 ah, bf16x8 al, bf16x8 bh, bf16x8 bl, floatx4 (&a)[3]) {
+    a[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, a[0], 0, 0, 0);
+    a[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, a[1], 0, 0, 0);
+    a[2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, a[2], 0, 0, 0);
+}
+
+// ------------------------------------------------------------------ fp32 io: operand images
+// The fp32 chain takes K, Q, T and P as high and low bf16 parts, copied from the
+// workspace straight into LDS; the chunk terms write them in the LDS order.
+// K and Q (64 x dk): the 16-byte pieces of row r sit XOR-swizzled by f32_kq_swz(r),
+// so the row reads (16 rows) and the transpose reads (4 rows, 4 pieces) of the chain
+// meet no bank twice.  T and P (64 x 64): piece j of row r at j ^ (r % 8).
+template <int DK> __device__ __forceinline__ int f32_kq_swz(int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (DK / 8 - 1); }
+template <int DK> __device__ __forceinline__ int f32_kq_at(int r, int cc) {
+    return r * DK + (((cc >> 3) ^ f32_kq_swz<DK>(r)) << 3) + (cc & 7);
+}
+__device__ __forceinline__ int f32_tp_at(int r, int cc) { return r * CH + (((cc >> 3) ^ (r & 7)) << 3) + (cc & 7); }
+
 // ------------------------------------------------------------------ fp32 chunk terms
 // One workgroup per (chunk slot, head), fp32 io: G, T = (I+A)^{-1} and P for one chunk.
 template <int DK>
@@ -342,8 +433,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const long slot = (long)gc * H + h;
-    IO* Tg = reinterpret_cast<IO*>(p.wsT) + slot * tp_elems<IO>();
-    IO* Pg = reinterpret_cast<IO*>(p.wsP) + slot * tp_elems<IO>();
+    bf16_t* Tg = reinterpret_cast<bf16_t*>(p.wsT) + slot * 2 * CH * CH;   // [hi | lo]
+    bf16_t* Pg = reinterpret_cast<bf16_t*>(p.wsP) + slot * 2 * CH * CH;
 
     if (wave == 0) {
         float gv = 0.f, bv = 0.f;   // padded rows: no decay, no write
@@ -387,6 +478,19 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         if (l2) {
             p.wsG[slot * GS + 2 * CH + tid] = gam * sSk[tid];
             p.wsG[slot * GS + 3 * CH + tid] = gam * sSq[tid];
+        }
+    }
+
+    {   // K and Q for the chain: high and low bf16 parts, in its LDS order (f32_kq_at)
+        bf16_t* kq = reinterpret_cast<bf16_t*>(p.wsKQ) + slot * 4 * CH * DK;   // [K hi | K lo | Q hi | Q lo]
+        for (int i = tid; i < 2 * CH * DK / 8; i += NT) {
+            const int t = i / (CH * DK / 8), pc = i % (CH * DK / 8), r = pc / (DK / 8);
+            const int col = 8 * ((pc % (DK / 8)) ^ f32_kq_swz<DK>(r));
+            const IO(*X)[DK + PAD] = t ? sQ : sK;
+            bf16x8 hi, lo;
+            split8(f4(&X[r][col]), f4(&X[r][col + 4]), hi, lo);
+            *reinterpret_cast<bf16x8*>(kq + (2 * t) * CH * DK + 8 * pc) = hi;
+            *reinterpret_cast<bf16x8*>(kq + (2 * t + 1) * CH * DK + 8 * pc) = lo;
         }
     }
 
@@ -474,266 +578,297 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
         __syncthreads();
     }
-    // T and P as row-major squares, zero above the diagonal blocks
-    for (int i = tid; i < CH * CH; i += NT) {
-        const int r = i / CH, cc = i % CH;
-        const bool up = (cc >> 4) > (r >> 4);
-        Tg[i] = up ? 0.f : sTi[r][cc];
-        Pg[i] = up ? 0.f : sP[r][cc];
+    // T and P for the chain: high and low bf16 parts in its LDS order (f32_tp_at), zero above the diagonal blocks
+    for (int i = tid; i < CH * CH / 8; i += NT) {
+        const int r = i / (CH / 8), col = 8 * ((i % (CH / 8)) ^ (r & 7));
+        const bool up = (col >> 4) > (r >> 4);
+        const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+        bf16x8 hi, lo;
+        split8(up ? z : f4(&sTi[r][col]), up ? z : f4(&sTi[r][col + 4]), hi, lo);
+        *reinterpret_cast<bf16x8*>(Tg + 8 * i) = hi;
+        *reinterpret_cast<bf16x8*>(Tg + CH * CH + 8 * i) = lo;
+        split8(up ? z : f4(&sP[r][col]), up ? z : f4(&sP[r][col + 4]), hi, lo);
+        *reinterpret_cast<bf16x8*>(Pg + 8 * i) = hi;
+        *reinterpret_cast<bf16x8*>(Pg + CH * CH + 8 * i) = lo;
     }
 }
 
 // ------------------------------------------------------------------ fp32 state chain
-// One workgroup per (sequence, head, 16-row slice of S); chunks in order.
-template <int DK, bool SNAP = false>
-__device__ __forceinline__ void state_chain_f32(const Params& p, const int bid) {
-    using IO = float;
-    constexpr int PAD = 16 / sizeof(IO);
-    constexpr int NMT = DK / 16;          // 16-row tiles of S^T
-    const int H = p.H, DV = p.DV, nsl = DV / SL;
-    const int js = bid % nsl;
-    const int h = (bid / nsl) % H;
-    const int s = bid / (nsl * H);
+// One workgroup of 8 waves per (sequence, head, 16-row slice of S); chunks in
+// order (section 3.2): with S_c the state entering chunk c,
+//   X = K S_c^T,  R = diag(beta) (V - diag(gamma_k) X),  U = T R,
+//   S_{c+1}^T = gamma_n S_c^T + K^T diag(D) U,
+//   O = scale (diag(gamma_q) Q S_c^T + P U).
+// Waves 0-3 compute (wave w: token tile w of X, R, U and O, and the key tiles
+// w + 4 m of the state update); waves 4-7 copy each chunk's operands into LDS
+// with buffer loads to LDS: K, Q, T and P as the high and low bf16 parts the
+// chunk terms left in the workspace (in the LDS order), the V slice, the decay
+// vectors and beta.  Four barriers per chunk:
+//   A_c  chunk c resident; the compute waves read every tile operand they need
+//        (K rows and K^T fragments, Q, T, P) into registers;
+//   A'_c the copy waves issue chunk c+1's copies of K and Q into the same tiles;
+//        the compute waves form X, R;
+//   B_c  the copy waves issue the copies of T, P, V and the decay vectors (V and
+//        the decay vectors alternate by chunk parity); the compute waves form U;
+//   C_c  the compute waves update the state and form O.
+// The copy waves wait for their copies before A_{c+1}.  The state slice stays in
+// the compute waves' fp32 accumulators; S, R, U and D U go through LDS as high and
+// low bf16 parts, split once by the wave that forms them.
+// Every fp32 product is three bf16 MFMA products of high and low parts (mma3x);
+// accumulation is fp32.
+template <int DK> struct __attribute__((aligned(16))) F32ChainLds {
+    bf16_t kq[4][CH * DK];                            // K hi, K lo, Q hi, Q lo (f32_kq_at)
+    bf16_t tp[4][CH * CH];                            // T hi, T lo, P hi, P lo (f32_tp_at)
+    bf16_t Sb[2][2][SL][DK + 8];                      // the slice of S, high and low parts, by chunk parity
+    float V[2][CH * SL];                              // [token][value channel of the slice], by chunk parity
+    float g[2][5 * CH];                               // gamma, D, gamma s_k, gamma s_q, beta; by chunk parity
+    bf16_t Rb[2][SL][CH + 8];                         // R transposed, high and low parts
+    bf16_t Ub[4][SL][CH + 8];                         // U and D U transposed, high and low parts
+};
 
+template <int DK, bool SNAP = false>
+__device__ __forceinline__ void state_chain_f32(const Params& p, const int bid, F32ChainLds<DK>& lds) {
+    constexpr int NKD = DK / 32;          // 32-long contraction blocks over the key channels
+    constexpr int NMW = DK / 64;          // 16-key tiles of S^T per compute wave in the state update
+    const int H = p.H, DV = p.DV, nsl = DV / SL;
+    // slice-major: the slices of one (sequence, head) are congruent modulo H, so with
+    // 8 | H they share an XCD (dispatch deals workgroups to the 8 XCDs in turn) and
+    // its L2 copy of the head's operands
+    const int s = bid / (nsl * H);
+    const int js = (bid % (nsl * H)) / H;
+    const int h = bid % H;
     long start;
     int len, cbase;
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
 
-    __shared__ __attribute__((aligned(16))) float sS[2][SL][DK + 4];   // rows js*16.. of S, by chunk parity
-    __shared__ __attribute__((aligned(16))) IO sK[CH][DK + PAD];
-    __shared__ __attribute__((aligned(16))) IO sQ[CH][DK + PAD];
-    __shared__ __attribute__((aligned(16))) IO sT[CH][CH + PAD];
-    __shared__ __attribute__((aligned(16))) IO sP[CH][CH + PAD];
-    __shared__ float sV[CH][SL + 1];
-    __shared__ __attribute__((aligned(16))) float sRt[SL][CH + 4], sUt[SL][CH + 4];   // R, U transposed
-    __shared__ __attribute__((aligned(16))) float sGam[CH], sDec[CH], sBeta[CH], sGk[CH], sGq[CH];
-
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
 
-    for (int i = tid; i < SL * DK; i += NT)
-        sS[0][i / DK][i % DK] = p.S0 ? p.S0[srow0 + i] : 0.f;
-
-    IO* go = reinterpret_cast<IO*>(p.o);
-
-    // One chunk's inputs, this thread's share, held in registers: the next
-    // chunk's loads are issued while the current chunk computes (K and Q after
-    // its first product, the rest after its second), so their latency and the
-    // issue of 100 KB of loads per workgroup overlap the arithmetic.
-    constexpr int VE = 16 / sizeof(IO);             // elements per 16-byte load
-    constexpr int NKV = CH * (DK / VE) / NT;        // K (and Q) loads per thread
-    constexpr int NTV = CH * (CH / VE) / NT;        // T (and P) loads per thread
-    constexpr int VPV = SL / VE;                    // loads per V row slice
-    constexpr int NVV = (CH * VPV + NT - 1) / NT;   // V loads per thread
-    static_assert(CH * (DK / VE) % NT == 0 && CH * (CH / VE) % NT == 0, "loads per thread");
-    struct Pre {
-        uint4 k[NKV], q[NKV], t[NTV], pp[NTV], v[NVV];
-        float gam, dec, beta, gk, gq;   // gk, gq: the decay applied to K S^T and to Q S^T
-    };
-    // buffer loads: one lane offset per tensor, rows past the chunk end read as zeros
-    auto rs = [](const void* base, long bytes) {
-        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (uint32_t)bytes, 0x00020000);
-    };
-    auto ld = [](__amdgpu_buffer_rsrc_t r, int voff) {   // the whole offset in voff: it is what the range check sees
-        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-    };
-    const int HK = p.HK, hk = h / p.G;   // q and k rows of this head
-    const int kvo = ((tid / (DK / VE)) * HK * DK + (tid % (DK / VE)) * VE) * (int)sizeof(IO);
-    const int vvo = ((tid / VPV) * H * DV + js * SL + (tid % VPV) * VE) * (int)sizeof(IO);
-    auto load_kq = [&](int c, Pre& x) {
-        const long t0 = start + (long)c * CH;
-        const long rb = (long)(min(CH, len - c * CH) - 1) * HK + 1;   // rows of the key head's chunk, in [T][HK] rows
-        const auto rk = rs(reinterpret_cast<const IO*>(p.k) + (t0 * HK + hk) * DK, rb * DK * sizeof(IO));
-        const auto rq = rs(reinterpret_cast<const IO*>(p.q) + (t0 * HK + hk) * DK, rb * DK * sizeof(IO));
+    if (wave >= 4) {
+        // ------------------------------------------------ copy waves
+        const int li = wave - 4;
+        constexpr int KQB = 4 * CH * DK * 2, TPB = 2 * CH * CH * 2;   // bytes per (slot, head)
+        // K (hi, lo) and then Q (hi, lo): half of the KQB bytes each
+        auto issue_kq = [&](int c, int half) {
+            const long slot = (long)(cbase + c) * H + h;
+            const auto rkq = rsrc(reinterpret_cast<const char*>(p.wsKQ) + slot * KQB, KQB);
 #pragma unroll
-        for (int j = 0; j < NKV; ++j) {
-            const int so = (NT / (DK / VE)) * j * HK * DK * (int)sizeof(IO);
-            x.k[j] = ld(rk, kvo + so);
-            x.q[j] = ld(rq, kvo + so);
-        }
-    };
-    auto load_rest = [&](int c, Pre& x) {
-        const long t0 = start + (long)c * CH;
-        const int n = min(CH, len - c * CH);
-        const long slot = (long)(cbase + c) * H + h;
-        const long rb = (long)(n - 1) * H + 1;
-        const auto rt = rs(reinterpret_cast<const IO*>(p.wsT) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
-        const auto rp = rs(reinterpret_cast<const IO*>(p.wsP) + slot * tp_elems<IO>(), tp_elems<IO>() * sizeof(IO));
-#pragma unroll
-        for (int j = 0; j < NTV; ++j) {
-            x.t[j] = ld(rt, tid * 16 + NT * 16 * j);
-            x.pp[j] = ld(rp, tid * 16 + NT * 16 * j);
-        }
-        // no value tensor reads as zeros (a descriptor of no bytes)
-        const auto rv = p.v ? rs(reinterpret_cast<const IO*>(p.v) + (t0 * H + h) * DV, rb * DV * sizeof(IO)) : rs(p.k, 0);
-#pragma unroll
-        for (int j = 0; j < NVV; ++j)
-            x.v[j] = tid + NT * j < CH * VPV ? ld(rv, vvo + (NT / VPV) * j * H * DV * (int)sizeof(IO)) : make_uint4(0, 0, 0, 0);
-        // (prefetch only: nothing here may read a loaded value, or the wait for it
-        // would also wait for every load issued before)
-        if (tid < CH) {
-            x.gam = p.wsG[slot * GS + tid];
-            x.dec = p.wsG[slot * GS + CH + tid];
-            if (p.pre & PRE_L2) {
-                x.gk = p.wsG[slot * GS + 2 * CH + tid];
-                x.gq = p.wsG[slot * GS + 3 * CH + tid];
+            for (int i = li; i < KQB / 2048; i += 4) {
+                const int o = half * (KQB / 2) + i * 1024;
+                bdma16(rkq, reinterpret_cast<char*>(&lds.kq[0][0]) + o, o + lane * 16);
             }
-            // padded rows write nothing: beta = 0, or a logit whose sigmoid is 0
-            x.beta = tid < n ? p.beta[(t0 + tid) * H + h] : ((p.pre & PRE_GATES) ? -INFINITY : 0.f);
-        }
-    };
-    auto store = [&](const Pre& x) {
+        };
+        auto issue_rest = [&](int c) {
+            const long slot = (long)(cbase + c) * H + h, t0 = start + (long)c * CH;
+            const int n = min(CH, len - c * CH);
+            const auto rt = rsrc(reinterpret_cast<const char*>(p.wsT) + slot * TPB, TPB);
+            const auto rp = rsrc(reinterpret_cast<const char*>(p.wsP) + slot * TPB, TPB);
 #pragma unroll
-        for (int j = 0; j < NKV; ++j) {
-            const int i = tid + NT * j, r = i / (DK / VE), cv = i % (DK / VE);
-            *reinterpret_cast<uint4*>(&sK[r][cv * VE]) = x.k[j];
-            *reinterpret_cast<uint4*>(&sQ[r][cv * VE]) = x.q[j];
-        }
-#pragma unroll
-        for (int j = 0; j < NTV; ++j) {
-            const int i = tid + NT * j, r = i / (CH / VE), cv = i % (CH / VE);
-            *reinterpret_cast<uint4*>(&sT[r][cv * VE]) = x.t[j];
-            *reinterpret_cast<uint4*>(&sP[r][cv * VE]) = x.pp[j];
-        }
-#pragma unroll
-        for (int j = 0; j < NVV; ++j) {
-            const int i = tid + NT * j, r = i / VPV, cv = i % VPV;
-            if (i < CH * VPV) {
-                const IO* e = reinterpret_cast<const IO*>(&x.v[j]);
-#pragma unroll
-                for (int u = 0; u < VE; ++u) sV[r][cv * VE + u] = to_f(e[u]);
+            for (int i = li; i < TPB / 1024; i += 4) {
+                bdma16(rt, reinterpret_cast<char*>(&lds.tp[0][0]) + i * 1024, i * 1024 + lane * 16);
+                bdma16(rp, reinterpret_cast<char*>(&lds.tp[2][0]) + i * 1024, i * 1024 + lane * 16);
             }
+            // V rows 16 li .. 16 li + 15 of the slice (no value tensor: zeros); rows past the chunk read as zeros
+            const long rb = (long)(n - 1) * H + 1;
+            const auto rv = p.v ? rsrc(reinterpret_cast<const float*>(p.v) + (t0 * H + h) * DV, (uint32_t)(rb * DV * 4))
+                                : rsrc(p.k, 0u);
+            bdma16(rv, &lds.V[c & 1][16 * li * SL], ((16 * li + lane / 4) * H * DV + js * SL + 4 * (lane % 4)) * 4);
+            if (li == 0) bdma16(rsrc(p.wsG + slot * GS, GS * 4), &lds.g[c & 1][0], lane * 16);
+            if (li == 1) bdma4(rsrc(p.beta + t0 * H + h, (uint32_t)(rb * 4)), &lds.g[c & 1][4 * CH], lane * H * 4);
+        };
+        if (nc > 0) {
+            issue_kq(0, 0);
+            issue_kq(0, 1);
+            issue_rest(0);
         }
-        if (tid < CH) {
-            const bool l2 = p.pre & PRE_L2;
-            sGam[tid] = x.gam;
-            sDec[tid] = x.dec;
-            sBeta[tid] = (p.pre & PRE_GATES) ? gate_beta(x.beta) : x.beta;
-            sGk[tid] = l2 ? x.gk : x.gam;
-            sGq[tid] = l2 ? x.gq : x.gam;
+        // the copies of chunk c+1 go out over chunk c's phases (issuing the 100 KB takes
+        // about as long as their arithmetic; of the splits measured, K and Q after A'_c and
+        // the rest after B_c was the fastest)
+        for (int c = 0; c < nc; ++c) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            lds_barrier();   // A_c
+            lds_barrier();   // A'_c
+            if (c + 1 < nc) {
+                issue_kq(c + 1, 0);
+                issue_kq(c + 1, 1);
+            }
+            lds_barrier();   // B_c
+            if (c + 1 < nc) issue_rest(c + 1);
+            lds_barrier();   // C_c
         }
-    };
-
-    Pre pre;
-    if (nc > 0) {
-        load_kq(0, pre);
-        load_rest(0, pre);
+        lds_barrier();   // F
+        return;
     }
+
+    // ------------------------------------------------ compute waves
+    // S^T key tiles md = wave + 4 m stay in this wave's fp32 accumulators (element e of lane
+    // group lg: key channel chan(md) + e, state row l16); each chunk publishes S as high and low
+    // bf16 parts for every wave's B operands.
+    auto chan = [&](int md) { return 32 * (md >> 1) + 8 * lg + 4 * (md & 1); };
+    floatx4 acc[NMW];
+#pragma unroll
+    for (int m = 0; m < NMW; ++m)
+        acc[m] = p.S0 ? *reinterpret_cast<const floatx4*>(p.S0 + srow0 + l16 * DK + chan(wave + 4 * m))
+                      : floatx4{0.f, 0.f, 0.f, 0.f};
+    auto put_split4 = [](bf16_t* hi, bf16_t* lo, floatx4 v) {   // 4 values -> 8 bytes of each part
+        const bf16x4 h4 = __builtin_convertvector(v, bf16x4);
+        floatx4 r;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = v[e] - (float)h4[e];
+        *reinterpret_cast<bf16x4*>(hi) = h4;
+        *reinterpret_cast<bf16x4*>(lo) = __builtin_convertvector(r, bf16x4);
+    };
+    auto publish_s = [&](int par) {
+#pragma unroll
+        for (int m = 0; m < NMW; ++m) put_split4(&lds.Sb[par][0][l16][chan(wave + 4 * m)], &lds.Sb[par][1][l16][chan(wave + 4 * m)], acc[m]);
+    };
+    if (nc > 0) publish_s(0);
+    const bool l2 = p.pre & PRE_L2, gates = p.pre & PRE_GATES;
+    const int row = wave * 16 + l16;   // token row of this lane's A operands
+    const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < nc; ++c) {
         const long t0 = start + (long)c * CH;
         const int n = min(CH, len - c * CH);
-        const float(*sSc)[DK + 4] = sS[c & 1];
-        __syncthreads();   // previous chunk done with every tile
+        const float* G = lds.g[c & 1];
+        lds_barrier();   // A_c
         if constexpr (SNAP) {   // S_c, the state after c chunks
             if (c > 0 && c % p.snap_every == 0) {
-                float* sn = p.snaps + (((long)s * p.n_snap + c / p.snap_every - 1) * H + h) * (long)DV * DK + (long)js * SL * DK;
-                for (int i = tid; i < SL * DK; i += NT) sn[i] = sSc[i / DK][i % DK];
+                float* sn = p.snaps + (((long)s * p.n_snap + c / p.snap_every - 1) * H + h) * (long)DV * DK +
+                            (long)(js * SL + l16) * DK;
+#pragma unroll
+                for (int m = 0; m < NMW; ++m) *reinterpret_cast<floatx4*>(sn + chan(wave + 4 * m)) = acc[m];
             }
         }
-        store(pre);
-        __syncthreads();
-
-        // fp32 MFMA (contraction 4 per instruction): in instruction 4 j + e, lane
-        // group lg carries contraction index 16 j + 4 lg + e, so a lane reads its
-        // operands for four instructions with one 16-byte LDS read.
-        // X = K S^T (tokens of tile `wave` x 16 value channels)
-        floatx4 x = {0.f, 0.f, 0.f, 0.f};
+        // this chunk's tile operands into registers before A'_c (the copy waves refill the tiles after it)
+        bf16x8 kh[NKD], kl[NKD], qh[NKD], ql[NKD], th[2], tl[2], ph[2], pl[2], kth[NMW][2], ktl[NMW][2];
 #pragma unroll
-        for (int j = 0; j < DK / 16; ++j) {
-            const floatx4 a4 = f4(&sK[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sSc[l16][16 * j + 4 * lg]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) x = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], x, 0, 0, 0);
+        for (int kk = 0; kk < NKD; ++kk) {
+            const int at = f32_kq_at<DK>(row, 32 * kk + 8 * lg);
+            kh[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[0][at]);
+            kl[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[1][at]);
+            qh[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[2][at]);
+            ql[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[3][at]);
         }
-        // R = diag(beta) (V - diag(gamma) X), stored transposed
-        {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int at = f32_tp_at(row, 32 * kk + 8 * lg);
+            th[kk] = *reinterpret_cast<const bf16x8*>(&lds.tp[0][at]);
+            tl[kk] = *reinterpret_cast<const bf16x8*>(&lds.tp[1][at]);
+            ph[kk] = *reinterpret_cast<const bf16x8*>(&lds.tp[2][at]);
+            pl[kk] = *reinterpret_cast<const bf16x8*>(&lds.tp[3][at]);
+        }
+        // K^T fragments of key tiles md = wave + 4 m (transpose reads); contraction element j
+        // of lane group lg in block kk is token 32 kk + 16 (j / 4) + 4 lg + j % 4
+#pragma unroll
+        for (int m = 0; m < NMW; ++m) {
+            const int md = wave + 4 * m, col = 32 * (md >> 1) + 8 * (l16 & 3) + 4 * (md & 1);
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int o0 = f32_kq_at<DK>(32 * kk + 4 * lg + (l16 >> 2), col);
+                const int o1 = f32_kq_at<DK>(32 * kk + 16 + 4 * lg + (l16 >> 2), col);
+                kth[m][kk] = join4(lds_tr8(&lds.kq[0][o0]), lds_tr8(&lds.kq[0][o1]));
+                ktl[m][kk] = join4(lds_tr8(&lds.kq[1][o0]), lds_tr8(&lds.kq[1][o1]));
+            }
+        }
+        lds_barrier();   // A'_c
+        // X = K S_c^T, S_c as B operands (key channel 32 kk + 8 lg + j, state row l16)
+        bf16x8 sbh[NKD], sbl[NKD];
+        floatx4 xa[3] = {z4, z4, z4};
+#pragma unroll
+        for (int kk = 0; kk < NKD; ++kk) {
+            sbh[kk] = *reinterpret_cast<const bf16x8*>(&lds.Sb[c & 1][0][l16][32 * kk + 8 * lg]);
+            sbl[kk] = *reinterpret_cast<const bf16x8*>(&lds.Sb[c & 1][1][l16][32 * kk + 8 * lg]);
+            mma3x(kh[kk], kl[kk], sbh[kk], sbl[kk], xa);
+        }
+        {   // R = diag(beta) (V - diag(gamma_k) X) for tokens 16 wave + 4 lg + e; rows past the chunk: beta = 0
+            const floatx4 x = xa[0] + xa[1] + xa[2];
             floatx4 rv;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int r = wave * 16 + 4 * lg + e;
-                rv[e] = sBeta[r] * (sV[r][l16] - sGk[r] * x[e]);
+                const float braw = G[4 * CH + r];
+                const float b = r < n ? (gates ? gate_beta(braw) : braw) : 0.f;
+                rv[e] = b * (lds.V[c & 1][r * SL + l16] - (l2 ? G[2 * CH + r] : G[r]) * x[e]);
             }
-            *reinterpret_cast<floatx4*>(&sRt[l16][wave * 16 + 4 * lg]) = rv;
+            put_split4(&lds.Rb[0][l16][wave * 16 + 4 * lg], &lds.Rb[1][l16][wave * 16 + 4 * lg], rv);
         }
-        __syncthreads();
+        lds_barrier();   // B_c
 
-        if (c + 1 < nc) load_kq(c + 1, pre);
-        // U = T R
-        floatx4 u = {0.f, 0.f, 0.f, 0.f};
+        // U = T R (k = token 32 kk + 8 lg + j); published as U and as D U
+        {
+            floatx4 ua[3] = {z4, z4, z4};
 #pragma unroll
-        for (int j = 0; j < CH / 16; ++j) {
-            const floatx4 a4 = f4(&sT[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sRt[l16][16 * j + 4 * lg]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) u = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], u, 0, 0, 0);
+            for (int kk = 0; kk < 2; ++kk)
+                mma3x(th[kk], tl[kk], *reinterpret_cast<const bf16x8*>(&lds.Rb[0][l16][32 * kk + 8 * lg]),
+                      *reinterpret_cast<const bf16x8*>(&lds.Rb[1][l16][32 * kk + 8 * lg]), ua);
+            const floatx4 u = ua[0] + ua[1] + ua[2];
+            put_split4(&lds.Ub[0][l16][wave * 16 + 4 * lg], &lds.Ub[1][l16][wave * 16 + 4 * lg], u);
+            put_split4(&lds.Ub[2][l16][wave * 16 + 4 * lg], &lds.Ub[3][l16][wave * 16 + 4 * lg],
+                       f4(&G[CH + wave * 16 + 4 * lg]) * u);
         }
-        *reinterpret_cast<floatx4*>(&sUt[l16][wave * 16 + 4 * lg]) = u;
-        __syncthreads();
+        lds_barrier();   // C_c
 
-        if (c + 1 < nc) load_rest(c + 1, pre);
-        // O = scale (diag(gamma) Q S^T + P U)
-        floatx4 oq = {0.f, 0.f, 0.f, 0.f}, op = {0.f, 0.f, 0.f, 0.f};
+        // S^T <- gamma_n S^T + K^T (D U)
+        {
+            const float gn = G[CH - 1];
+            bf16x8 dh[2], dl[2];
 #pragma unroll
-        for (int j = 0; j < DK / 16; ++j) {
-            const floatx4 a4 = f4(&sQ[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sSc[l16][16 * j + 4 * lg]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) oq = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], oq, 0, 0, 0);
-        }
-#pragma unroll
-        for (int j = 0; j < CH / 16; ++j) {
-            const floatx4 a4 = f4(&sP[wave * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sUt[l16][16 * j + 4 * lg]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) op = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], op, 0, 0, 0);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = wave * 16 + 4 * lg + e;
-            if (r < n)
-                go[((t0 + r) * H + h) * (long)DV + js * SL + l16] =
-                    from_f<IO>(p.scale * (sGq[r] * oq[e] + op[e]));
-        }
-
-        // S^T <- gamma_n S^T + K^T D U   (tiles of 16 key channels)
-        const float gn = sGam[CH - 1];
-        floatx4 acc[(NMT + 3) / 4];
-#pragma unroll
-        for (int m = 0; m < (NMT + 3) / 4; ++m) {
-            const int mt = wave + 4 * m;
-            acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
-            if (mt < NMT) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) acc[m][e] = gn * sSc[l16][mt * 16 + 4 * lg + e];
-#pragma unroll
-                for (int j = 0; j < CH / 16; ++j) {
-                    const floatx4 u4 = f4(&sUt[l16][16 * j + 4 * lg]), d4 = f4(&sDec[16 * j + 4 * lg]);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(to_f(sK[16 * j + 4 * lg + e][mt * 16 + l16]),
-                                                                      d4[e] * u4[e], acc[m], 0, 0, 0);
-                }
+            for (int kk = 0; kk < 2; ++kk) {
+                dh[kk] = join4(*reinterpret_cast<const short4v*>(&lds.Ub[2][l16][32 * kk + 4 * lg]),
+                               *reinterpret_cast<const short4v*>(&lds.Ub[2][l16][32 * kk + 16 + 4 * lg]));
+                dl[kk] = join4(*reinterpret_cast<const short4v*>(&lds.Ub[3][l16][32 * kk + 4 * lg]),
+                               *reinterpret_cast<const short4v*>(&lds.Ub[3][l16][32 * kk + 16 + 4 * lg]));
             }
+#pragma unroll
+            for (int m = 0; m < NMW; ++m) {
+                floatx4 sa[3] = {gn * acc[m], z4, z4};
+#pragma unroll
+                for (int kk = 0; kk < 2; ++kk) mma3x(kth[m][kk], ktl[m][kk], dh[kk], dl[kk], sa);
+                acc[m] = sa[0] + sa[1] + sa[2];
+            }
+            publish_s((c + 1) & 1);
         }
-        // the new state into the other buffer: the old one may still be read
+        // O = scale (diag(gamma_q) Q S_c^T + P U)
+        floatx4 qa[3] = {z4, z4, z4}, pa[3] = {z4, z4, z4};
 #pragma unroll
-        for (int m = 0; m < (NMT + 3) / 4; ++m) {
-            const int mt = wave + 4 * m;
-            if (mt < NMT) {
+        for (int kk = 0; kk < NKD; ++kk) mma3x(qh[kk], ql[kk], sbh[kk], sbl[kk], qa);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) sS[(c + 1) & 1][l16][mt * 16 + 4 * lg + e] = acc[m][e];
+        for (int kk = 0; kk < 2; ++kk)
+            mma3x(ph[kk], pl[kk], *reinterpret_cast<const bf16x8*>(&lds.Ub[0][l16][32 * kk + 8 * lg]),
+                  *reinterpret_cast<const bf16x8*>(&lds.Ub[1][l16][32 * kk + 8 * lg]), pa);
+        {   // rows past the chunk fall outside the descriptor and are dropped
+            const floatx4 oq = qa[0] + qa[1] + qa[2], op = pa[0] + pa[1] + pa[2];
+            const auto ro = rsrc(reinterpret_cast<float*>(p.o) + (t0 * H + h) * DV, (uint32_t)((((long)n - 1) * H + 1) * DV * 4));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = wave * 16 + 4 * lg + e;
+                const float ov = p.scale * ((l2 ? G[3 * CH + r] : G[r]) * oq[e] + op[e]);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(ov), ro, (r * H * DV + js * SL + l16) * 4, 0, 0);
             }
         }
     }
-    __syncthreads();
-    if (p.ST)
-        for (int i = tid; i < SL * DK; i += NT) {
-            const long at = p.st_t ? srow0 - (long)js * SL * DK + (long)(i % DK) * DV + js * SL + i / DK : srow0 + i;
-            p.ST[at] = sS[nc & 1][i / DK][i % DK];
+    lds_barrier();   // F
+    if (p.ST) {
+#pragma unroll
+        for (int m = 0; m < NMW; ++m) {
+            if (p.st_t) {   // [n, H, dk, DV]
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    p.ST[srow0 - (long)js * SL * DK + (long)(chan(wave + 4 * m) + e) * DV + js * SL + l16] = acc[m][e];
+            } else {
+                *reinterpret_cast<floatx4*>(p.ST + srow0 + l16 * DK + chan(wave + 4 * m)) = acc[m];
+            }
         }
+    }
 }
 
+// One workgroup per CU (its LDS): two waves per SIMD.
 template <int DK, bool SNAP = false>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain(Params p) {
-    state_chain_f32<DK, SNAP>(p, blockIdx.x);
+__global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain(Params p) {
+    __shared__ F32ChainLds<DK> lds;
+    state_chain_f32<DK, SNAP>(p, blockIdx.x, lds);
 }
 
 // ------------------------------------------------------------------ bf16 state chain
@@ -782,61 +917,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 // before it.  Barriers order LDS traffic only, so global loads and stores stay
 // in flight across them.
 // The chunk loop is unrolled by the ring depth so ring slots are constants.
-typedef float floatx8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef short short4v __attribute__((ext_vector_type(4)));
-typedef int int4v __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-constexpr int NT_CHAIN = 512;
-constexpr int RING = 4;
-template <int N> struct Ic { static constexpr int value = N; };
-
-__device__ __forceinline__ bf16x8 pack_bf16(floatx4 a, floatx4 b) {
-    const floatx8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-    return __builtin_convertvector(x, bf16x8);
-}
-__device__ __forceinline__ bf16x8 join4(short4v a, short4v b) {
-    const short8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-    return __builtin_bit_cast(bf16x8, x);
-}
-// whole-register select (a runtime index into a register array would be
-// lowered element by element)
-__device__ __forceinline__ bf16x8 sel(bool c, bf16x8 a, bf16x8 b) {
-    return __builtin_bit_cast(bf16x8, c ? __builtin_bit_cast(int4v, a) : __builtin_bit_cast(int4v, b));
-}
-// Transpose read: within each 16-lane group, lane i element e receives element
-// i%4 of the 8 bytes addressed by lane 4e + i/4 of the group.
-__device__ __forceinline__ short4v lds_tr8(const bf16_t* ptr) {
-    typedef __attribute__((address_space(3))) short4v lds_short4v;
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(ptr));
-}
-__device__ __forceinline__ float bf(short x) { return __uint_as_float((uint32_t)(uint16_t)x << 16); }
-// Buffer resource over [base, base + bytes); loads past the end return zeros.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
-}
-// AUX: cache policy of the access (0: default; 17 = sc0 sc1: system coherent,
-// bypassing the caches that other workgroups' data could be stale in)
-template <int AUX = 0> __device__ __forceinline__ bf16x8 bload16(__amdgpu_buffer_rsrc_t r, int voff) {
-    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, AUX));
-}
-// global -> LDS without registers: lane l's 16 (4) bytes land at dst + 16 l (4 l)
-template <int AUX = 0> __device__ __forceinline__ void bdma16(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, voff, 0, 0, AUX);
-}
-template <int AUX = 0> __device__ __forceinline__ void bdma4(__amdgpu_buffer_rsrc_t r, void* dst, int voff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 4, voff, 0, 0, AUX);
-}
-template <int AUX = 0> __device__ __forceinline__ void bstore16(bf16x8 v, __amdgpu_buffer_rsrc_t r, int voff) {
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff, 0, AUX);
-}
-template <int AUX = 0> __device__ __forceinline__ void bstore4(float v, __amdgpu_buffer_rsrc_t r, int voff) {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, AUX);
-}
-// Workgroup barrier ordering LDS traffic only: the wave's own LDS operations
-// complete, the compiler moves no memory access across it, and -- unlike
-// __syncthreads() -- it does not wait for outstanding global loads or stores.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // LDS of one chain workgroup
 template <int DK> struct ChainLds {
@@ -2119,10 +2199,11 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
 }
 
 template <int DK>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_state_chain_pair(Params p, ChainAlt a) {
+__global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_state_chain_pair(Params p, ChainAlt a) {
+    __shared__ F32ChainLds<DK> lds;
     int bid = blockIdx.x;
     if (bid >= a.first) { p.v = a.v; p.S0 = a.S0; p.o = a.o; p.ST = a.ST; p.st_t = a.st_t; p.DV = a.DV; bid -= a.first; }
-    state_chain_f32<DK>(p, bid);
+    state_chain_f32<DK>(p, bid, lds);
 }
 
 // ------------------------------------------------------------------ causal attention prefill
@@ -2333,12 +2414,11 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
     long slots;          // chunk slots per head
-    size_t meta, G, T, P, F, total;
+    size_t meta, G, T, P, F, KQ, total;
 };
 
 // Workspace layout; returns false for arguments that are out of range.
 bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* L) {
-    (void)dk;
     (void)dv;
     const size_t esz = io == GDN_BF16 ? 2 : 4;
     const long cpt = ((long)T + CH - 1) / CH;
@@ -2346,7 +2426,7 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     if (L->slots * (long)H > (1L << 24)) return false;
     const size_t per = (size_t)L->slots * H;
     if (per == 0) {   // no chunk: nothing to keep (not even the status word)
-        L->meta = L->G = L->T = L->P = L->F = L->total = 0;
+        L->meta = L->G = L->T = L->P = L->F = L->KQ = L->total = 0;
         return true;
     }
     L->meta = 256;   // bytes [0, 8): the status word (gdn_workspace_status)
@@ -2355,7 +2435,9 @@ bool ws_layout(int B, int T, int H, int dk, int dv, int n_seqs, int io, Layout* 
     const size_t tp = io == GDN_BF16 ? tp_elems<bf16_t>() : tp_elems<float>();
     L->P = L->T + round_up(per * tp * esz, 256);
     L->F = L->P + round_up(per * tp * esz, 256);
-    L->total = L->F + (io == GDN_BF16 ? round_up(per * sizeof(uint64_t), 256) : 0);
+    L->KQ = L->F + (io == GDN_BF16 ? round_up(per * sizeof(uint64_t), 256) : 0);
+    // fp32 io: K and Q of every (chunk slot, head) as high and low bf16 parts, in the chain's LDS order
+    L->total = L->KQ + (io == GDN_BF16 ? 0 : round_up(per * 4 * CH * (size_t)dk * sizeof(bf16_t), 256));
     return true;
 }
 
@@ -2372,7 +2454,7 @@ bool gen_layout(int B, int T, int H, int C, int n_seqs, Layout* L) {
     if (L->slots * (long)H > (1L << 24)) return false;
     const size_t per = (size_t)L->slots * H;
     if (per == 0) {
-        L->meta = L->G = L->T = L->P = L->F = L->total = 0;
+        L->meta = L->G = L->T = L->P = L->F = L->KQ = L->total = 0;
         return true;
     }
     L->meta = 256;
@@ -2380,7 +2462,7 @@ bool gen_layout(int B, int T, int H, int C, int n_seqs, Layout* L) {
     L->T = L->G + round_up(per * 4 * C * sizeof(float), 256);
     L->P = L->T + round_up(per * C * C * sizeof(float), 256);
     L->F = L->P + round_up(per * C * C * sizeof(float), 256);
-    L->total = L->F;
+    L->KQ = L->total = L->F;
     return true;
 }
 
@@ -2481,7 +2563,7 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
     if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_state_chain_bf16<DK, SNAP, NORM>), grid, dim3(NT_CHAIN), 0, st, p);
     else
-        hipLaunchKernelGGL((k_state_chain<DK, SNAP>), grid, dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_state_chain<DK, SNAP>), grid, dim3(NT_CHAIN), 0, st, p);
 }
 
 // ---- evaluation plans: sequential chain, segment-parallel (narrow and wide); workspace; launches
@@ -2659,7 +2741,7 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
     if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_state_chain_pair_bf16<DK, NORM>), grid, dim3(NT_CHAIN), 0, st, p, a);
     else
-        hipLaunchKernelGGL((k_state_chain_pair<DK>), grid, dim3(NT), 0, st, p, a);
+        hipLaunchKernelGGL((k_state_chain_pair<DK>), grid, dim3(NT_CHAIN), 0, st, p, a);
     const long units = (long)sq.nseq * sq.H;   // (sequence, head) pairs, each on one XCD
     hipLaunchKernelGGL((k_segment_scan<IO, DK>), dim3((unsigned)(8 * ((units + 7) / 8) * (sq.DV / SL))), dim3(DK * 4), 0,
                        st, sq);
@@ -2841,6 +2923,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.wsG = reinterpret_cast<float*>(ws + L.G);
     p.wsT = ws + L.T;
     p.wsP = ws + L.P;
+    p.wsKQ = ws + L.KQ;
     p.flags = reinterpret_cast<uint64_t*>(ws + L.F);
     p.epoch = 0;
     p.status = reinterpret_cast<uint64_t*>(ws);
@@ -2853,7 +2936,9 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
     p.snaps = snaps;
     p.snap_every = snap_every;
     p.n_snap = snap_every > 0 ? (T - 1) / (snap_every * CH) : 0;
-    if (L.total == 0) { p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.flags = nullptr; p.status = nullptr; }
+    if (L.total == 0) {
+        p.wsG = nullptr; p.wsT = nullptr; p.wsP = nullptr; p.wsKQ = nullptr; p.flags = nullptr; p.status = nullptr;
+    }
 
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     (void)hipGetLastError();
@@ -2924,6 +3009,7 @@ static gdn_status prefill(const void* q, const void* k, const void* v, const flo
         r.wsG = reinterpret_cast<float*>(ws + S.base.G);
         r.wsT = ws + S.base.T;
         r.wsP = ws + S.base.P;
+        r.wsKQ = ws + S.base.KQ;
         r.flags = reinterpret_cast<uint64_t*>(ws + S.base.F);
         const bool norm = pre & PRE_L2;
         if (io_dtype == GDN_BF16) {
