@@ -417,17 +417,21 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     const long t0 = start + (long)c * CH;
     const int n = min(CH, len - c * CH);
 
-    // The K and Q tiles are dead once the token-token products are in registers:
-    // A, T and P take their space (two workgroups fit a CU's LDS).
-    constexpr int SZ_TILES = 2 * CH * (DK + PAD) * (int)sizeof(IO), SZ_MATS = 3 * CH * (CH + 4) * 4;
+    // K and Q are held as high and low bf16 parts (x = hi + lo, split8); once the
+    // token-token products are in registers, A, T and P take the tiles' space (two
+    // workgroups fit a CU's LDS).
+    constexpr int KP = DK + 8;   // row pitch of the bf16 tiles
+    constexpr int SZ_TILES = 4 * CH * KP * 2, SZ_MATS = 3 * CH * (CH + 4) * 4;
     __shared__ __attribute__((aligned(16))) char smem[SZ_TILES > SZ_MATS ? SZ_TILES : SZ_MATS];
-    IO(*sK)[DK + PAD] = reinterpret_cast<IO(*)[DK + PAD]>(smem);
-    IO(*sQ)[DK + PAD] = sK + CH;
+    bf16_t(*sKh)[KP] = reinterpret_cast<bf16_t(*)[KP]>(smem);
+    bf16_t(*sKl)[KP] = sKh + CH;
+    bf16_t(*sQh)[KP] = sKh + 2 * CH;
+    bf16_t(*sQl)[KP] = sKh + 3 * CH;
     float(*sA)[CH + 4] = reinterpret_cast<float(*)[CH + 4]>(smem);
     float(*sTi)[CH + 4] = sA + CH;
     float(*sP)[CH + 4] = sTi + CH;
     __shared__ float sZ[4][16][17];
-    __shared__ double sG[CH];
+    __shared__ double sG[CH];   // prefix sums of g in log2 units
     __shared__ float sB[CH], sD[CH], sSk[CH], sSq[CH];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -436,6 +440,27 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     bf16_t* Tg = reinterpret_cast<bf16_t*>(p.wsT) + slot * 2 * CH * CH;   // [hi | lo]
     bf16_t* Pg = reinterpret_cast<bf16_t*>(p.wsP) + slot * 2 * CH * CH;
 
+    // K and Q rows: every load issued before the first store
+    constexpr int NPR = DK / 8;                 // 8-channel pieces per row
+    constexpr int NPC = CH * NPR / NT;          // pieces per thread and tensor
+    uint4 kv[NPC][2], qv[NPC][2];
+    {
+        const int HK = p.HK, hk = h / p.G;     // q and k carry HK heads; this head reads key head h / G
+        const float* gk = reinterpret_cast<const float*>(p.k);
+        const float* gq = reinterpret_cast<const float*>(p.q);
+#pragma unroll
+        for (int j = 0; j < NPC; ++j) {
+            const int i = tid + NT * j, r = i / NPR, pc = i % NPR;
+            kv[j][0] = kv[j][1] = qv[j][0] = qv[j][1] = make_uint4(0, 0, 0, 0);
+            if (r < n) {   // rows past the chunk: zeros
+                const long off = ((t0 + r) * HK + hk) * (long)DK + 8 * pc;
+                kv[j][0] = *reinterpret_cast<const uint4*>(gk + off);
+                kv[j][1] = *reinterpret_cast<const uint4*>(gk + off + 4);
+                qv[j][0] = *reinterpret_cast<const uint4*>(gq + off);
+                qv[j][1] = *reinterpret_cast<const uint4*>(gq + off + 4);
+            }
+        }
+    }
     if (wave == 0) {
         float gv = 0.f, bv = 0.f;   // padded rows: no decay, no write
         if (lane < n) {
@@ -446,7 +471,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
                 bv = gate_beta(bv);
             }
         }
-        double x = gv;   // inclusive prefix sum over the chunk, fp64
+        double x = (double)gv * 1.4426950408889634;   // inclusive prefix sum over the chunk, fp64, log2 units
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
             const double y = __shfl_up(x, off, 64);
@@ -455,25 +480,48 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         const double xn = __shfl(x, 63, 64);   // G_n (padded rows add nothing)
         sG[lane] = x;
         sB[lane] = bv;
-        sD[lane] = expf((float)(xn - x));
-        p.wsG[slot * GS + lane] = expf((float)x);
+        sD[lane] = __builtin_amdgcn_exp2f((float)(xn - x));
+        p.wsG[slot * GS + lane] = __builtin_amdgcn_exp2f((float)x);
     }
-    stage_rows2<IO, DK, DK + PAD>(sK, reinterpret_cast<const IO*>(p.k), sQ, reinterpret_cast<const IO*>(p.q), t0, n, p.HK,
-                                  h / p.G);
-    __syncthreads();
     const bool l2 = p.pre & PRE_L2;
-    if (l2) {   // reciprocal row lengths of K (threads 0..63) and Q (64..127); rows past the chunk: 0
-        if (tid < 2 * CH) {
-            const int r = tid % CH;
-            const IO(*X)[DK + PAD] = tid < CH ? sK : sQ;
-            float ss = 0.f;
-            for (int j = 0; j < DK; ++j) ss += X[r][j] * X[r][j];
-            (tid < CH ? sSk : sSq)[r] = r < n ? 1.f / sqrtf(ss + L2_EPS) : 0.f;
+    {   // split each piece: the LDS tiles, and the chain's copy in its LDS order (f32_kq_at); with
+        // PRE_L2 the squared row lengths, summed over the NPR consecutive lanes that hold a row
+        bf16_t* kq = reinterpret_cast<bf16_t*>(p.wsKQ) + slot * 4 * CH * DK;   // [K hi | K lo | Q hi | Q lo]
+#pragma unroll
+        for (int j = 0; j < NPC; ++j) {
+            const int i = tid + NT * j, r = i / NPR, pc = i % NPR;
+            const int at = 8 * (r * NPR + (pc ^ f32_kq_swz<DK>(r)));
+            const floatx4 k0 = __builtin_bit_cast(floatx4, kv[j][0]), k1 = __builtin_bit_cast(floatx4, kv[j][1]);
+            const floatx4 q0 = __builtin_bit_cast(floatx4, qv[j][0]), q1 = __builtin_bit_cast(floatx4, qv[j][1]);
+            bf16x8 hi, lo;
+            split8(k0, k1, hi, lo);
+            *reinterpret_cast<bf16x8*>(&sKh[r][8 * pc]) = hi;
+            *reinterpret_cast<bf16x8*>(&sKl[r][8 * pc]) = lo;
+            *reinterpret_cast<bf16x8*>(kq + at) = hi;
+            *reinterpret_cast<bf16x8*>(kq + CH * DK + at) = lo;
+            split8(q0, q1, hi, lo);
+            *reinterpret_cast<bf16x8*>(&sQh[r][8 * pc]) = hi;
+            *reinterpret_cast<bf16x8*>(&sQl[r][8 * pc]) = lo;
+            *reinterpret_cast<bf16x8*>(kq + 2 * CH * DK + at) = hi;
+            *reinterpret_cast<bf16x8*>(kq + 3 * CH * DK + at) = lo;
+            if (l2) {
+                const floatx4 kk2 = k0 * k0 + k1 * k1, qq2 = q0 * q0 + q1 * q1;
+                float sk = kk2[0] + kk2[1] + kk2[2] + kk2[3], sq = qq2[0] + qq2[1] + qq2[2] + qq2[3];
+#pragma unroll
+                for (int m = 1; m < NPR; m <<= 1) {
+                    sk += __shfl_xor(sk, m, 64);
+                    sq += __shfl_xor(sq, m, 64);
+                }
+                if (pc == 0) {   // reciprocal row lengths; rows past the chunk: 0
+                    sSk[r] = r < n ? 1.f / sqrtf(sk + L2_EPS) : 0.f;
+                    sSq[r] = r < n ? 1.f / sqrtf(sq + L2_EPS) : 0.f;
+                }
+            }
         }
-        __syncthreads();
     }
+    __syncthreads();
     if (tid < CH) {   // D (times s_k with PRE_L2), and the scaled decays the chain applies to K S^T and Q S^T
-        const float gam = expf((float)sG[tid]);
+        const float gam = __builtin_amdgcn_exp2f((float)sG[tid]);
         p.wsG[slot * GS + CH + tid] = l2 ? sD[tid] * sSk[tid] : sD[tid];
         if (l2) {
             p.wsG[slot * GS + 2 * CH + tid] = gam * sSk[tid];
@@ -481,20 +529,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
     }
 
-    {   // K and Q for the chain: high and low bf16 parts, in its LDS order (f32_kq_at)
-        bf16_t* kq = reinterpret_cast<bf16_t*>(p.wsKQ) + slot * 4 * CH * DK;   // [K hi | K lo | Q hi | Q lo]
-        for (int i = tid; i < 2 * CH * DK / 8; i += NT) {
-            const int t = i / (CH * DK / 8), pc = i % (CH * DK / 8), r = pc / (DK / 8);
-            const int col = 8 * ((pc % (DK / 8)) ^ f32_kq_swz<DK>(r));
-            const IO(*X)[DK + PAD] = t ? sQ : sK;
-            bf16x8 hi, lo;
-            split8(f4(&X[r][col]), f4(&X[r][col + 4]), hi, lo);
-            *reinterpret_cast<bf16x8*>(kq + (2 * t) * CH * DK + 8 * pc) = hi;
-            *reinterpret_cast<bf16x8*>(kq + (2 * t + 1) * CH * DK + 8 * pc) = lo;
-        }
-    }
-
-    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P): job = wave + 4 u
+    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P): job = wave + 4 u, each
+    // as split bf16 products
     auto job_block = [](int job, int& which, int& bi, int& bj) {
         which = job / 10;
         int t = job % 10;
@@ -507,16 +543,17 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     for (int u = 0; u < 5; ++u) {
         int which, bi, bj;
         job_block(wave + 4 * u, which, bi, bj);
-        const IO(*X)[DK + PAD] = which ? sQ : sK;
-        // instruction 4 j + e: lane group lg carries contraction index 16 j + 4 lg + e
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        const bf16_t(*Xh)[KP] = which ? sQh : sKh;
+        const bf16_t(*Xl)[KP] = which ? sQl : sKl;
+        const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
+        floatx4 a3[3] = {z4, z4, z4};
 #pragma unroll
-        for (int j = 0; j < DK / 16; ++j) {
-            const floatx4 a4 = f4(&X[bi * 16 + l16][16 * j + 4 * lg]), b4 = f4(&sK[bj * 16 + l16][16 * j + 4 * lg]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[e], b4[e], acc, 0, 0, 0);
-        }
-        accs[u] = acc;
+        for (int kk = 0; kk < DK / 32; ++kk)
+            mma3x(*reinterpret_cast<const bf16x8*>(&Xh[bi * 16 + l16][32 * kk + 8 * lg]),
+                  *reinterpret_cast<const bf16x8*>(&Xl[bi * 16 + l16][32 * kk + 8 * lg]),
+                  *reinterpret_cast<const bf16x8*>(&sKh[bj * 16 + l16][32 * kk + 8 * lg]),
+                  *reinterpret_cast<const bf16x8*>(&sKl[bj * 16 + l16][32 * kk + 8 * lg]), a3);
+        accs[u] = a3[0] + a3[1] + a3[2];
     }
     __syncthreads();   // every tile read done: A and P overwrite them
 #pragma unroll
@@ -528,9 +565,9 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
             const int r = bi * 16 + 4 * lg + e, i = bj * 16 + l16;
             const float nrm = l2 ? (which ? sSq[r] : sSk[r]) * sSk[i] : 1.f;
             if (which == 0) {
-                sA[r][i] = (r > i) ? sB[r] * expf((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
+                sA[r][i] = (r > i) ? sB[r] * __builtin_amdgcn_exp2f((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
             } else {
-                sP[r][i] = (r >= i) ? expf((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
+                sP[r][i] = (r >= i) ? __builtin_amdgcn_exp2f((float)(sG[r] - sG[i])) * (nrm * accs[u][e]) : 0.f;
             }
         }
     }
