@@ -2636,7 +2636,7 @@ struct SegCost {
     double seq_fixed, chunk, seg_fixed, per_token_head, per_segment;
 };
 constexpr SegCost COST_BF16 = {17.0, 0.73, 28.5, 3.6e-4, 1.4};
-constexpr SegCost COST_F32 = {12.0, 4.2, 35.5, 1.7e-3, 2.6};
+constexpr SegCost COST_F32 = {15.0, 2.0, 30.0, 5.0e-4, 2.0};
 // The wide form (dense bf16, 16 segments, every pass one workgroup per
 // (sequence, segment, head)): a fixed part (four launches, each pass's first
 // loads) and a cost per chunk of a sequence that grows with the units it runs
