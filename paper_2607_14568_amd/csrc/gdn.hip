@@ -638,12 +638,13 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 //   O = scale (diag(gamma_q) Q S_c^T + P U).
 // Waves 0-3 compute (wave w: token tile w of X, R, U and O, and the key tiles
 // w + 4 m of the state update); waves 4-7 copy each chunk's operands into LDS
-// with buffer loads to LDS: K, Q, T and P as the high and low bf16 parts the
-// chunk terms left in the workspace (in the LDS order), the V slice, the decay
-// vectors and beta.  Four barriers per chunk:
+// with buffer loads to LDS: K, T and P as the high and low bf16 parts the chunk
+// terms left in the workspace (in the LDS order), the V slice, the decay vectors
+// and beta.  Each compute wave loads its own Q rows (split likewise) into
+// registers at the start of the chunk.  Four barriers per chunk:
 //   A_c  chunk c resident; the compute waves read every tile operand they need
-//        (K rows and K^T fragments, Q, T, P) into registers;
-//   A'_c the copy waves issue chunk c+1's copies of K and Q into the same tiles;
+//        (K rows and K^T fragments, T, P) into registers;
+//   A'_c the copy waves issue chunk c+1's copy of K into the same tile;
 //        the compute waves form X, R;
 //   B_c  the copy waves issue the copies of T, P, V and the decay vectors (V and
 //        the decay vectors alternate by chunk parity); the compute waves form U;
@@ -654,7 +655,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 // Every fp32 product is three bf16 MFMA products of high and low parts (mma3x);
 // accumulation is fp32.
 template <int DK> struct __attribute__((aligned(16))) F32ChainLds {
-    bf16_t kq[4][CH * DK];                            // K hi, K lo, Q hi, Q lo (f32_kq_at)
+    bf16_t kq[2][CH * DK];                            // K hi, K lo (f32_kq_at)
     bf16_t tp[4][CH * CH];                            // T hi, T lo, P hi, P lo (f32_tp_at)
     bf16_t Sb[2][2][SL][DK + 8];                      // the slice of S, high and low parts, by chunk parity
     float V[2][CH * SL];                              // [token][value channel of the slice], by chunk parity
@@ -687,15 +688,12 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid, 
         // ------------------------------------------------ copy waves
         const int li = wave - 4;
         constexpr int KQB = 4 * CH * DK * 2, TPB = 2 * CH * CH * 2;   // bytes per (slot, head)
-        // K (hi, lo) and then Q (hi, lo): half of the KQB bytes each
-        auto issue_kq = [&](int c, int half) {
+        // K (hi, lo): the first half of the K/Q image (the compute waves load their Q rows themselves)
+        auto issue_k = [&](int c) {
             const long slot = (long)(cbase + c) * H + h;
-            const auto rkq = rsrc(reinterpret_cast<const char*>(p.wsKQ) + slot * KQB, KQB);
+            const auto rk = rsrc(reinterpret_cast<const char*>(p.wsKQ) + slot * KQB, KQB / 2);
 #pragma unroll
-            for (int i = li; i < KQB / 2048; i += 4) {
-                const int o = half * (KQB / 2) + i * 1024;
-                bdma16(rkq, reinterpret_cast<char*>(&lds.kq[0][0]) + o, o + lane * 16);
-            }
+            for (int i = li; i < KQB / 2048; i += 4) bdma16(rk, reinterpret_cast<char*>(&lds.kq[0][0]) + i * 1024, i * 1024 + lane * 16);
         };
         auto issue_rest = [&](int c) {
             const long slot = (long)(cbase + c) * H + h, t0 = start + (long)c * CH;
@@ -716,21 +714,17 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid, 
             if (li == 1) bdma4(rsrc(p.beta + t0 * H + h, (uint32_t)(rb * 4)), &lds.g[c & 1][4 * CH], lane * H * 4);
         };
         if (nc > 0) {
-            issue_kq(0, 0);
-            issue_kq(0, 1);
+            issue_k(0);
             issue_rest(0);
         }
-        // the copies of chunk c+1 go out over chunk c's phases (issuing the 100 KB takes
-        // about as long as their arithmetic; of the splits measured, K and Q after A'_c and
-        // the rest after B_c was the fastest)
+        // the copies of chunk c+1 go out over chunk c's phases (issuing them takes about as
+        // long as their arithmetic; of the splits measured, K after A'_c and the rest after
+        // B_c was the fastest)
         for (int c = 0; c < nc; ++c) {
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             lds_barrier();   // A_c
             lds_barrier();   // A'_c
-            if (c + 1 < nc) {
-                issue_kq(c + 1, 0);
-                issue_kq(c + 1, 1);
-            }
+            if (c + 1 < nc) issue_k(c + 1);
             lds_barrier();   // B_c
             if (c + 1 < nc) issue_rest(c + 1);
             lds_barrier();   // C_c
@@ -778,15 +772,25 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid, 
                 for (int m = 0; m < NMW; ++m) *reinterpret_cast<floatx4*>(sn + chan(wave + 4 * m)) = acc[m];
             }
         }
-        // this chunk's tile operands into registers before A'_c (the copy waves refill the tiles after it)
+        // this wave's Q rows (high and low parts) straight from the workspace into registers, for
+        // the output product at the end of the chunk (one LDS pass fewer)
         bf16x8 kh[NKD], kl[NKD], qh[NKD], ql[NKD], th[2], tl[2], ph[2], pl[2], kth[NMW][2], ktl[NMW][2];
+        {
+            constexpr int KQB = 4 * CH * DK * 2;
+            const auto rq = rsrc(reinterpret_cast<const char*>(p.wsKQ) + ((long)(cbase + c) * H + h) * KQB + KQB / 2, KQB / 2);
+#pragma unroll
+            for (int kk = 0; kk < NKD; ++kk) {
+                const int at = 2 * f32_kq_at<DK>(row, 32 * kk + 8 * lg);   // bytes
+                qh[kk] = bload16(rq, at);
+                ql[kk] = bload16(rq, CH * DK * 2 + at);
+            }
+        }
+        // the tile operands into registers before A'_c (the copy waves refill the tiles after it)
 #pragma unroll
         for (int kk = 0; kk < NKD; ++kk) {
             const int at = f32_kq_at<DK>(row, 32 * kk + 8 * lg);
             kh[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[0][at]);
             kl[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[1][at]);
-            qh[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[2][at]);
-            ql[kk] = *reinterpret_cast<const bf16x8*>(&lds.kq[3][at]);
         }
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
