@@ -393,7 +393,6 @@ __device__ __forceinline__ int f32_tp_at(int r, int cc) { return r * CH + (((cc 
 template <int DK>
 __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     using IO = float;
-    constexpr int PAD = 16 / sizeof(IO);
     const int H = p.H;
     const int slot_x = blockIdx.x;
     const int gc = slot_x / H, h = slot_x % H;
