@@ -2251,15 +2251,17 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
 // per head, a causal softmax, then P V; grouped query heads share a key/value
 // head): per (sequence, head h),
 //     o_i = sum_{j <= i} softmax_j(scale q_i . k_j) v_j,   key/value head h / (H / H_kv).
-// One workgroup per (sequence, head, block of AQ queries), 8 waves of 16 queries;
-// blocks of AKB keys and values stream through a double-buffered LDS ring (16-byte
-// chunks XOR-swizzled by row) up to the causal diagonal.  Per key block a wave
-// forms S^T = K Q^T (its Q^T operands held in registers), the running softmax of
-// each query column in fp32 (max and sum across the lane groups by shuffles),
-// and O^T += V^T P^T: the exponentiated S^T accumulators are the B operand as
-// they stand (contraction over keys in the order 32 kk + 16 (j / 4) + 4 lg + j % 4),
-// and the V^T operands come from transpose LDS reads in that order.  The full
-// score matrix never exists; the work skips key blocks past a wave's last query.
+// One workgroup per (sequence, head, block of AQ queries): 8 waves of one 16-query
+// tile, or 4 waves of two (QT); blocks of AKB keys and values stream through a
+// double-buffered LDS ring (16-byte chunks XOR-swizzled by row) up to the causal
+// diagonal.  Per key block a wave forms S^T = K Q^T for each of its query tiles
+// (Q^T operands held in registers; each K operand read serves all the tiles), the
+// running softmax of each query column in fp32 (the block maximum across the lane
+// groups by shuffles), and O^T += V^T P^T: the exponentiated S^T accumulators are
+// the B operand as they stand (contraction over keys in the order
+// 32 kk + 16 (j / 4) + 4 lg + j % 4), and the V^T operands come from transpose LDS
+// reads in that order.  The full score matrix never exists; the work skips key
+// blocks past a wave's last query.
 constexpr int AQ = 128, AKB = 64, NT_ATT = 512;
 
 struct AttnParams {
@@ -2279,8 +2281,9 @@ template <int DH> struct AttnLds {
     bf16_t v[2][AKB * DH];
 };
 
-template <int DH>
-__global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
+template <int DH, int QT>
+__global__ __launch_bounds__(NT_ATT / QT) __attribute__((amdgpu_waves_per_eu(4 / QT))) void k_attn_causal(AttnParams p) {
+    constexpr int NW = NT_ATT / 64 / QT;   // waves; each holds QT tiles of 16 queries
     constexpr int NCH = DH / 8;         // 16-byte chunks per row
     constexpr int RPI = 64 / NCH;       // rows per 1 KB copy
     constexpr int NKB = DH / 32;        // contraction blocks over the head dimension
@@ -2291,7 +2294,9 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
     int qb = p.nqb - 1 - (int)(blockIdx.x / BH);   // blocks with the most keys first
     const int bh = (int)(blockIdx.x % BH);
     const int b = bh / p.H, h = bh % p.H, hk = h / (p.H / p.HKV);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index as a scalar: the branches on it below (masking, skipped blocks,
+    // K or V copies) are then scalar branches
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     long seq0 = (long)b * p.T;   // first row of this workgroup's sequence
     int T = p.T;                 // its length
@@ -2317,7 +2322,7 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
         if (found < 0) return;   // past the last block (the grid is an upper bound)
         qb = found;
     }
-    const int q0 = qb * AQ, qw = q0 + 16 * wave;   // the workgroup's and this wave's first query
+    const int q0 = qb * AQ, qw = q0 + 16 * QT * wave;   // the workgroup's and this wave's first query
     const long rsq = (long)p.H * DH, rsk = (long)p.HKV * DH;   // row strides (elements)
     const bf16_t* qbase = p.q + (seq0 * p.H + h) * DH;
     const bf16_t* kbase = p.k + (seq0 * p.HKV + hk) * DH;
@@ -2337,12 +2342,14 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
         return rsrc(base + (long)r0 * rs, m > 0 ? (uint32_t)(((long)(m - 1) * rs + DH) * 2) : 0u);
     };
 
-    // Q^T operand: lane holds q[qw + l16][32 kb + 8 lg .. + 7]
-    bf16x8 qf[NKB];
+    // Q^T operands: lane holds q[qw + 16 u + l16][32 kb + 8 lg .. + 7] for query tile u
+    bf16x8 qf[QT][NKB];
     {
-        const auto rq = rows_rsrc(qbase, rsq, qw, 16);
+        const auto rq = rows_rsrc(qbase, rsq, qw, 16 * QT);
 #pragma unroll
-        for (int kb = 0; kb < NKB; ++kb) qf[kb] = bload16(rq, (int)((l16 * rsq + 32 * kb + 8 * lg) * 2));
+        for (int u = 0; u < QT; ++u)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) qf[u][kb] = bload16(rq, (int)(((16 * u + l16) * rsq + 32 * kb + 8 * lg) * 2));
     }
     // copies of key block j into ring slot j & 1: copy c < NCP / 2 is K rows RPI c .., the rest V
     const int nkb = min((T + AKB - 1) / AKB, (q0 + AQ) / AKB);
@@ -2351,87 +2358,141 @@ __global__ __launch_bounds__(NT_ATT) void k_attn_causal(AttnParams p) {
         const auto rk = rows_rsrc(kbase, rsk, kb0, AKB);
         const auto rv = rows_rsrc(vbase, rsk, kb0, AKB);
 #pragma unroll
-        for (int c = wave; c < NCP; c += NT_ATT / 64) {
+        for (int c = wave; c < NCP; c += NW) {
             const int cc = c % (NCP / 2), r = RPI * cc + lane / NCH;
             const int off = (int)((r * rsk + (((lane % NCH) ^ swz(r)) << 3)) * 2);
             if (c < NCP / 2) bdma16(rk, &lds.k[sl][RPI * cc * DH], off);
             else bdma16(rv, &lds.v[sl][RPI * cc * DH], off);
         }
     };
-    float m = -INFINITY, l = 0.f;   // running max (log2 units) and sum of query qw + l16
-    floatx4 oacc[NDT];
+    // Running softmax per query in log2 units.  m is a reference at most RESLACK below
+    // the largest scaled score seen (it moves only when a block exceeds it by more:
+    // the weights 2^(x - m) stay below 2^RESLACK, and O and the weight sum are
+    // rescaled only then).  The weight sum is one more product tile, ones times the
+    // bf16 weights, so it sums exactly the weights the products with V use: every
+    // entry of lsum is the sum of this lane's query.
+    constexpr float RESLACK = 8.f;
+    const float sl2 = p.scale_log2;
+    const floatx4 one4 = {1.f, 1.f, 1.f, 1.f};
+    const bf16x8 ones = pack_bf16(one4, one4);
+    float m[QT];
+    floatx4 lsum[QT], oacc[QT][NDT];
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) oacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (nkb > 0) issue(0);
-    for (int j = 0; j < nkb; ++j) {
+    for (int u = 0; u < QT; ++u) {
+        m[u] = -INFINITY;
+        lsum[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) oacc[u][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    // key block j in ring slot SL = j & 1 (a constant: the loop below is unrolled by two,
+    // so the LDS addresses are this lane's offsets plus immediates)
+    auto block = [&](const int j, auto SLOT) {
+        constexpr int SL = decltype(SLOT)::value;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of block j
         lds_barrier();                                       // everyone's; slot (j + 1) & 1 no longer read
         if (j + 1 < nkb) issue(j + 1);
         const int kb0 = j * AKB;
-        if (kb0 > qw + 15) continue;   // every key of the block follows this wave's queries
-        const bf16_t* sk = lds.k[j & 1];
-        const bf16_t* sv = lds.v[j & 1];
-        floatx4 st[4];   // S^T: keys 16 t + 4 lg + e, query l16
+        if (kb0 > qw + 16 * QT - 1) return;   // every key of the block follows this wave's queries
+        const bf16_t* sk = lds.k[SL];
+        const bf16_t* sv = lds.v[SL];
+        floatx4 st[QT][4];   // S^T of query tile u: keys 16 t + 4 lg + e, query l16
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            st[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < QT; ++u)
 #pragma unroll
-            for (int kb = 0; kb < NKB; ++kb)
-                st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    *reinterpret_cast<const bf16x8*>(&sk[kq(16 * t + l16, 32 * kb + 8 * lg)]), qf[kb], st[t], 0, 0, 0);
+            for (int t = 0; t < 4; ++t) st[u][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&sk[kq(16 * t + l16, 32 * kb + 8 * lg)]);
+#pragma unroll
+                for (int u = 0; u < QT; ++u) st[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[u][kb], st[u][t], 0, 0, 0);
+            }
+        bf16x8 pf[QT][2];
+#pragma unroll
+        for (int u = 0; u < QT; ++u) {
+            const int qt0 = qw + 16 * u;   // the tile's first query
+            // some key of the block is masked for this tile (wave-uniform)
+            const bool diag = kb0 + AKB - 1 > qt0 || kb0 + AKB > T;
+            // bm: the block's largest scaled score of this lane's query; the weights are
+            // 2^(fs x - m).  Blocks with no masked key and a scale >= 0 take the largest
+            // raw score times the scale (fs = scale); otherwise the scores are scaled and
+            // masked first (fs = 1).
+            float bm, fs;
+            if (!diag && sl2 >= 0.f) {
+                bm = st[u][0][0];
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) bm = fmaxf(bm, st[u][t][e]);
+                bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+                bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+                bm *= sl2;
+                fs = sl2;
+            } else {
+                const int qi = qt0 + l16;
+                bm = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int kj = kb0 + 16 * t + 4 * lg + e;
+                        const float x = (kj > qi || kj >= T) ? -INFINITY : st[u][t][e] * sl2;
+                        st[u][t][e] = x;
+                        bm = fmaxf(bm, x);
+                    }
+                bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+                bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+                fs = 1.f;
+            }
+            // the first block holds key 0 <= every query, so m is finite from then on; a
+            // later block may mask every key of a query (bm = -inf): m stays
+            const bool up = bm > m[u] + RESLACK;
+            if (__builtin_amdgcn_ballot_w64(up)) {
+                const float mn = up ? bm : m[u];
+                const float alpha = __builtin_amdgcn_exp2f(m[u] - mn);   // 1 where m stays; 0 at the first block
+#pragma unroll
+                for (int t = 0; t < NDT; ++t) oacc[u][t] *= alpha;
+                lsum[u] *= alpha;
+                m[u] = mn;
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) st[u][t][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[u][t][e], fs, -m[u]));
+            pf[u][0] = pack_bf16(st[u][0], st[u][1]);
+            pf[u][1] = pack_bf16(st[u][2], st[u][3]);
+            lsum[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[u][0], lsum[u], 0, 0, 0);
+            lsum[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[u][1], lsum[u], 0, 0, 0);
         }
-        const int qi = qw + l16;
-        const bool diag = kb0 + AKB - 1 > qw || kb0 + AKB > T;   // some key of the block is masked
-        float bm = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float x = st[t][e] * p.scale_log2;
-                if (diag) {
-                    const int kj = kb0 + 16 * t + 4 * lg + e;
-                    if (kj > qi || kj >= T) x = -INFINITY;
-                }
-                st[t][e] = x;
-                bm = fmaxf(bm, x);
-            }
-        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-        const float mn = fmaxf(m, bm);   // finite: block 0 holds key 0 <= every query
-        const float alpha = __builtin_amdgcn_exp2f(m - mn);
-        float ls = 0.f;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                st[t][e] = __builtin_amdgcn_exp2f(st[t][e] - mn);
-                ls += st[t][e];
-            }
-        ls += __shfl_xor(ls, 16, 64);
-        ls += __shfl_xor(ls, 32, 64);
-        l = l * alpha + ls;
-        m = mn;
-        const bf16x8 pf0 = pack_bf16(st[0], st[1]), pf1 = pack_bf16(st[2], st[3]);
 #pragma unroll
         for (int t = 0; t < NDT; ++t) {
-            oacc[t] *= alpha;
 #pragma unroll
             for (int kk = 0; kk < 2; ++kk) {
                 const int r = 32 * kk + 4 * lg + (l16 >> 2), c = 16 * t + 4 * (l16 & 3);
                 const bf16x8 va = join4(lds_tr8(&sv[kq(r, c)]), lds_tr8(&sv[kq(r + 16, c)]));
-                oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, kk ? pf1 : pf0, oacc[t], 0, 0, 0);
+#pragma unroll
+                for (int u = 0; u < QT; ++u) oacc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pf[u][kk], oacc[u][t], 0, 0, 0);
             }
         }
+    };
+    if (nkb > 0) issue(0);
+    for (int j = 0; j < nkb; j += 2) {
+        block(j, Ic<0>{});
+        if (j + 1 < nkb) block(j + 1, Ic<1>{});
     }
-    // o[qw + l16][16 t + 4 lg + e] = O^T / l
-    const int qi = qw + l16;
-    if (qi < T) {
-        const float inv = 1.f / l;
-        bf16_t* orow = p.o + ((seq0 + qi) * p.H + h) * DH;
+    // o[qw + 16 u + l16][16 t + 4 lg + e] = O^T / (weight sum)
 #pragma unroll
-        for (int t = 0; t < NDT; ++t) {
-            const floatx4 ov = oacc[t] * inv;
-            *reinterpret_cast<bf16x4*>(orow + 16 * t + 4 * lg) = __builtin_convertvector(ov, bf16x4);
+    for (int u = 0; u < QT; ++u) {
+        const int qi = qw + 16 * u + l16;
+        if (qi < T) {
+            const float inv = 1.f / lsum[u][0];
+            bf16_t* orow = p.o + ((seq0 + qi) * p.H + h) * DH;
+#pragma unroll
+            for (int t = 0; t < NDT; ++t) {
+                const floatx4 ov = oacc[u][t] * inv;
+                *reinterpret_cast<bf16x4*>(orow + 16 * t + 4 * lg) = __builtin_convertvector(ov, bf16x4);
+            }
         }
     }
 }
@@ -2811,7 +2872,17 @@ void launch_decode(const void* q, const void* k, const void* v, const float* g, 
 
 template <int DH>
 void launch_attention(AttnParams a, hipStream_t st) {
-    hipLaunchKernelGGL((k_attn_causal<DH>), dim3((unsigned)((long)a.nqb * a.B * a.H)), dim3(NT_ATT), 0, st, a);
+    // Two query tiles per wave (four waves, two per SIMD) halve the LDS reads per
+    // product; they pay at d = 128 when the grid gives every CU several workgroups
+    // (10k 16-head prompt: 546-554 against 578 us; 2k: 57.6 against 49 us)
+    const long wgs = (long)a.nqb * a.B * a.H;
+    if constexpr (DH == 128) {
+        if (wgs >= 4 * stream_cus(st)) {
+            hipLaunchKernelGGL((k_attn_causal<DH, 2>), dim3((unsigned)wgs), dim3(NT_ATT / 2), 0, st, a);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((k_attn_causal<DH, 1>), dim3((unsigned)wgs), dim3(NT_ATT), 0, st, a);
 }
 
 }  // namespace

@@ -53,6 +53,41 @@ def test_attention_sharp_scores():
     _check(1, 500, 2, 1, 128, seed=720, scale=1.5)
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("scale", [0.0, -0.1])
+def test_attention_nonpositive_scale(d, scale):
+    """scale = 0 (uniform weights over each prefix) and scale < 0 (the largest
+    scaled score is the smallest raw one)."""
+    _check(1, 300, 2, 1, d, seed=722 + d, scale=scale)
+
+
+@pytest.mark.parametrize("growth", [5.0, 20.0])
+@pytest.mark.parametrize("B,H", [(1, 2), (4, 64)])
+def test_attention_rising_scores(growth, B, H):
+    """Scores that rise along the keys by `growth` (log2 units) per 64-key block, on
+    top of random ones: the softmax's reference maximum lags the running maximum
+    (growth 5) or moves at every block (growth 20).  B = 4, H = 64 is a grid with
+    two query tiles per wave."""
+    T, d = 400, 128
+    if H == 64:
+        assert (T + 127) // 128 * B * H >= _wgs_for_two_tiles()
+    print("case: attention rising scores growth=%g B=%d H=%d" % (growth, B, H), flush=True)
+    x = inputs.make_attention(B, T, H, 1, d, seed=724)
+    step = growth / (64 * np.log2(np.e))   # raw score added per key position
+    j = torch.arange(T, dtype=torch.float64)
+    # q . k_j = j step plus a small random part
+    q = 1.0 + 0.1 * x["q"].double()
+    k = (j * step / d)[None, :, None, None] + 0.1 * x["k"].double()
+    qb, kb = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    o = gdn.gdn_attention_prefill(qb.cuda(), kb.cuda(), x["v"].cuda(), scale=1.0)
+    torch.cuda.synchronize()
+    ref = att.causal_attention(f64(qb), f64(kb), f64(x["v"]), 1.0)
+    e = _rel(f64(o), ref)
+    print("  max rel err o=%.3e" % e, flush=True)
+    assert np.isfinite(f64(o)).all()
+    assert e < TOL, e
+
+
 def test_attention_2k():
     _check(1, 2048, 16, 8, 128, seed=721)
 
@@ -73,15 +108,34 @@ def test_attention_deterministic_and_grouped_equals_repeated_heads():
     assert torch.equal(a, b) and torch.equal(a, c)
 
 
-@pytest.mark.parametrize("d", [64, 128])
-def test_attention_packed_sequences(d):
+def _wgs_for_two_tiles():
+    """Workgroups from which the d = 128 kernel takes two query tiles per wave."""
+    return 4 * torch.cuda.get_device_properties(0).multi_processor_count
+
+
+@pytest.mark.parametrize("T", [65, 300])
+def test_attention_two_query_tiles_per_wave(T):
+    """A grid of at least four workgroups per CU at d = 128 (the form with two 16-query tiles per
+    wave), with one-block and ragged tails."""
+    nqb = (T + 127) // 128
+    B, H = 8, 64
+    while nqb * B * H < _wgs_for_two_tiles():
+        B *= 2
+    _check(B, T, H, 16, 128, seed=730 + T)
+
+
+@pytest.mark.parametrize("d,H,Hkv", [(64, 4, 2), (128, 4, 2), (128, 64, 16)])
+def test_attention_packed_sequences(d, H, Hkv):
     """Sequences packed with cu_seqlens (empty, one-token, block-edge and ragged lengths) attend only within
-    themselves: each compared with the oracle over that sequence alone."""
+    themselves: each compared with the oracle over that sequence alone.  At 64 heads the grid takes the
+    form with two query tiles per wave."""
     lens = [0, 1, 128, 129, 300, 64, 0, 777, 5]
     cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     T = int(cu[-1])
-    print("case: attention packed lengths %s d=%d" % (lens, d), flush=True)
-    x = inputs.make_attention(1, T, 4, 2, d, seed=740 + d)
+    if H == 64:
+        assert ((T + 127) // 128 + len(lens)) * H >= _wgs_for_two_tiles()
+    print("case: attention packed lengths %s d=%d H=%d" % (lens, d, H), flush=True)
+    x = inputs.make_attention(1, T, H, Hkv, d, seed=740 + d + H)
     sc = 1.0 / d ** 0.5
     o = gdn.gdn_attention_prefill(x["q"].cuda(), x["k"].cuda(), x["v"].cuda(), scale=sc,
                                   cu_seqlens=torch.from_numpy(cu).cuda())
