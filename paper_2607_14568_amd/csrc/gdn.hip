@@ -144,8 +144,13 @@ struct Params {
     int n_snap;
 };
 
+// Entry i of a sequence table, read where every lane of the wave reads the same
+// entry: held in a scalar register, so descriptors built from it stay scalar (a
+// vector-register descriptor makes the compiler loop over its distinct values).
+__device__ __forceinline__ int tab(const int32_t* a, long i) { return __builtin_amdgcn_readfirstlane(a[i]); }
+
 // Sequence at rank r when sequences are taken longest first (ragged), else r.
-__device__ __forceinline__ int seq_at_rank(const Params& p, int r) { return p.ragged ? p.seq_perm[r] : r; }
+__device__ __forceinline__ int seq_at_rank(const Params& p, int r) { return p.ragged ? tab(p.seq_perm, r) : r; }
 
 // Work item k of the chunk terms in the order the chains consume them: chunk
 // index within its sequence, then sequence rank, then head.
@@ -156,11 +161,11 @@ __device__ __forceinline__ long item_slot(const Params& p, long k) {
         int lo = 0, hi = p.cpt;   // largest c with cprefix[c] * H <= k
         while (hi - lo > 1) {
             const int mid = (lo + hi) >> 1;
-            if ((long)p.cprefix[mid] * H <= k) lo = mid; else hi = mid;
+            if ((long)tab(p.cprefix, mid) * H <= k) lo = mid; else hi = mid;
         }
         c = lo;
-        r = (int)((k - (long)p.cprefix[c] * H) / H);
-        return ((long)p.chunk_off[p.seq_perm[r]] + c) * H + (int)(k % H);
+        r = (int)((k - (long)tab(p.cprefix, c) * H) / H);
+        return ((long)tab(p.chunk_off, tab(p.seq_perm, r)) + c) * H + (int)(k % H);
     }
     c = (int)(k / ((long)p.n_seq * H));
     r = (int)((k / H) % p.n_seq);
@@ -169,9 +174,9 @@ __device__ __forceinline__ long item_slot(const Params& p, long k) {
 
 __device__ __forceinline__ void seq_info(const Params& p, int s, long& start, int& len, int& cbase) {
     if (p.ragged) {
-        start = p.seq_start[s];
-        len = p.seq_len[s];
-        cbase = p.chunk_off[s];
+        start = tab(p.seq_start, s);
+        len = tab(p.seq_len, s);
+        cbase = tab(p.chunk_off, s);
     } else {
         start = (long)s * p.T;
         len = p.T;
@@ -399,11 +404,11 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 
     int s;
     if (p.ragged) {
-        if (gc >= p.chunk_off[p.n_seq]) return;
+        if (gc >= tab(p.chunk_off, p.n_seq)) return;
         int lo = 0, hi = p.n_seq;
         while (hi - lo > 1) {
             const int mid = (lo + hi) >> 1;
-            if (p.chunk_off[mid] <= gc) lo = mid; else hi = mid;
+            if (tab(p.chunk_off, mid) <= gc) lo = mid; else hi = mid;
         }
         s = lo;
     } else {
@@ -433,7 +438,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __shared__ double sG[CH];   // prefix sums of g in log2 units
     __shared__ float sB[CH], sD[CH], sSk[CH], sSq[CH];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     const long slot = (long)gc * H + h;
     bf16_t* Tg = reinterpret_cast<bf16_t*>(p.wsT) + slot * 2 * CH * CH;   // [hi | lo]
@@ -679,7 +684,7 @@ __device__ __forceinline__ void state_chain_f32(const Params& p, const int bid, 
     seq_info(p, s, start, len, cbase);
     const int nc = (len + CH - 1) / CH;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
 
@@ -1013,7 +1018,7 @@ __device__ __forceinline__ void state_chain_bf16(const Params& p, const int bid,
     auto& sQ = lds.sQ;
     constexpr int AUX = FUSED ? 17 : 0;   // sc0 sc1: coherent with the writers' stores
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     const long srow0 = ((long)(s * H + h) * DV + js * SL) * DK;
     auto rows = [&](int c) { return min(CH, len - c * CH); };
@@ -1595,11 +1600,11 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     const int gc = (int)(gi / H), h = (int)(gi % H);
     int s;
     if (p.ragged) {
-        if (gc >= p.chunk_off[p.n_seq]) return;
+        if (gc >= tab(p.chunk_off, p.n_seq)) return;
         int lo = 0, hi = p.n_seq;
         while (hi - lo > 1) {
             const int mid = (lo + hi) >> 1;
-            if (p.chunk_off[mid] <= gc) lo = mid; else hi = mid;
+            if (tab(p.chunk_off, mid) <= gc) lo = mid; else hi = mid;
         }
         s = lo;
     } else {
@@ -1626,7 +1631,7 @@ __device__ __forceinline__ void chunk_terms_bf16(const Params& p, const long gi,
     bf16_t(*sPb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0 + 2 * CH * PA * 4);
     bf16_t(*sTb)[PB] = reinterpret_cast<bf16_t(*)[PB]>(r0);
 
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     auto swz = [](int r) { return ((4 * (r & 3)) | ((r >> 2) & 3)) & (NCH - 1); };
 
@@ -1844,7 +1849,7 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
         } t[2];
     } lds;
     if ((int)blockIdx.x < p.npw) {
-        const int half = threadIdx.x / NT;
+        const int half = __builtin_amdgcn_readfirstlane(threadIdx.x / NT);   // wave-uniform
         if (p.xcd_items) {
             // Dispatch deals workgroups to the 8 XCDs round-robin, so chain
             // workgroups of head h sit on XCD (npw + h) % 8.  Workgroup b forms
@@ -1862,7 +1867,7 @@ __global__ __launch_bounds__(NT_CHAIN) __attribute__((amdgpu_waves_per_eu(1, 2))
                 __syncthreads();   // the next item reuses the LDS
             }
         } else {
-            const long items = (long)(p.ragged ? p.chunk_off[p.n_seq] : p.n_seq * p.NC) * p.H;
+            const long items = (long)(p.ragged ? tab(p.chunk_off, p.n_seq) : p.n_seq * p.NC) * p.H;
             for (long k = 2L * blockIdx.x; k < items; k += 2L * p.npw) {
                 const long gi = item_slot(p, min(k + half, items - 1));   // both halves run every step together
                 chunk_terms_bf16<DK, true, NORM>(p, gi, lds.t[half].t, threadIdx.x % NT, k + half < items,
@@ -2028,7 +2033,7 @@ __global__ __launch_bounds__(DK * 4) void k_segment_scan(SegParams sp) {
     const int unit = (k / nsl) * 8 + xcd, js = k % nsl;
     if (unit >= sp.nseq * H) return;
     const int h = unit % H, b = unit / H;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), l16 = lane & 15, lg = lane >> 4;
     const int col = 16 * wave + l16;
     const long mat = (long)DV * DK;
     auto rows_at = [&](int seg) { return ((long)seg * H + h) * mat + (long)js * SL * DK; };
@@ -2148,7 +2153,7 @@ __global__ __launch_bounds__(NT_CORR) void k_segment_correct(SegParams sp) {
     const int c_end = min((p + 1) * sp.L, sp.NC);   // one past the segment's last chunk
     const int c0 = p * sp.L + 2 * q;
     if (c0 >= c_end) return;                        // workgroup-uniform
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), l16 = lane & 15, lg = lane >> 4;
     const int c = c0 + wave / 4;
     const long t_end = (long)b * sp.T + sp.T;       // one past the sequence's last token
     const long t = (long)b * sp.T + (long)c * CH + 16 * (wave % 4) + l16;   // this lane's token
@@ -2307,7 +2312,7 @@ __global__ __launch_bounds__(NT_ATT / QT) __attribute__((amdgpu_waves_per_eu(4 /
         int prev = 0, before = 0, s = 0;
         int found = -1;
         for (; s < p.n_seq; ++s) {
-            const int next = min(max(p.cu[s + 1], prev), p.T);
+            const int next = min(max(tab(p.cu, s + 1), prev), p.T);
             const int nb = (next - prev + AQ - 1) / AQ;
             const int r = p.nqb - 1 - qb;   // rank of this block in that numbering
             if (r < before + nb) {

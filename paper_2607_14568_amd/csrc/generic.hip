@@ -31,15 +31,15 @@ constexpr int GEN_RS = 16;    // state rows per chain workgroup
 __device__ __forceinline__ bool gen_item(const Params& p, long slot, long& t0, int& n) {
     const int C = p.C;
     if (p.ragged) {
-        if (slot >= p.chunk_off[p.n_seq]) return false;
+        if (slot >= tab(p.chunk_off, p.n_seq)) return false;
         int lo = 0, hi = p.n_seq;   // the sequence whose chunk slots hold `slot`
         while (hi - lo > 1) {
             const int mid = (lo + hi) >> 1;
-            if (p.chunk_off[mid] <= slot) lo = mid; else hi = mid;
+            if (tab(p.chunk_off, mid) <= slot) lo = mid; else hi = mid;
         }
-        const int c = (int)(slot - p.chunk_off[lo]);
-        t0 = p.seq_start[lo] + (long)c * C;
-        n = min(C, p.seq_len[lo] - c * C);
+        const int c = (int)(slot - tab(p.chunk_off, lo));
+        t0 = tab(p.seq_start, lo) + (long)c * C;
+        n = min(C, tab(p.seq_len, lo) - c * C);
     } else {
         const int s = (int)(slot / p.NC), c = (int)(slot % p.NC);
         t0 = (long)s * p.T + (long)c * C;

@@ -98,7 +98,7 @@ __device__ __forceinline__ void wide_body(const WideParams& p, WideLds<DK, OUT>&
     static_assert(NCH == 2 * NW, "two K copies per wave");
     const int H = p.H, D = p.D, HK = p.HK, hk = h / p.G;
     const int c0 = seg * p.L, nc = min(p.L, p.NC - c0);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, lg = lane >> 4;
     const int run = OUT ? WIDE_OUT : (wave < NW / 2 ? WIDE_VALUE : WIDE_IDENT);
     const int rw0 = OUT ? RW * wave : RW * (wave % (NW / 2));   // first state row of this wave
@@ -454,7 +454,7 @@ __global__ __launch_bounds__(DK * 4) void k_wide_scan(WideParams p) {
     const int unit = (k / nsl) * 8 + xcd, js = k % nsl;
     if (unit >= p.B * H) return;
     const int h = unit % H, b = unit / H;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), l16 = lane & 15, lg = lane >> 4;
     const int col = 16 * wave + l16;
     const long mat = (long)p.D * DK;
     auto at = [&](int seg) { return ((long)(b * P + seg) * H + h) * mat; };
