@@ -394,9 +394,11 @@ template <int DK> __device__ __forceinline__ int f32_kq_at(int r, int cc) {
 __device__ __forceinline__ int f32_tp_at(int r, int cc) { return r * CH + (((cc >> 3) ^ (r & 7)) << 3) + (cc & 7); }
 
 // ------------------------------------------------------------------ fp32 chunk terms
-// One workgroup per (chunk slot, head), fp32 io: G, T = (I+A)^{-1} and P for one chunk.
+// One workgroup of eight waves per (chunk slot, head), fp32 io: G, T = (I+A)^{-1}
+// and P for one chunk.
+constexpr int NT_T32 = 512;
 template <int DK>
-__global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
+__global__ __launch_bounds__(NT_T32) void k_chunk_terms(Params p) {
     using IO = float;
     const int H = p.H;
     const int slot_x = blockIdx.x;
@@ -446,7 +448,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
 
     // K and Q rows: every load issued before the first store
     constexpr int NPR = DK / 8;                 // 8-channel pieces per row
-    constexpr int NPC = CH * NPR / NT;          // pieces per thread and tensor
+    constexpr int NPC = CH * NPR / NT_T32;      // pieces per thread and tensor
     uint4 kv[NPC][2], qv[NPC][2];
     {
         const int HK = p.HK, hk = h / p.G;     // q and k carry HK heads; this head reads key head h / G
@@ -454,7 +456,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         const float* gq = reinterpret_cast<const float*>(p.q);
 #pragma unroll
         for (int j = 0; j < NPC; ++j) {
-            const int i = tid + NT * j, r = i / NPR, pc = i % NPR;
+            const int i = tid + NT_T32 * j, r = i / NPR, pc = i % NPR;
             kv[j][0] = kv[j][1] = qv[j][0] = qv[j][1] = make_uint4(0, 0, 0, 0);
             if (r < n) {   // rows past the chunk: zeros
                 const long off = ((t0 + r) * HK + hk) * (long)DK + 8 * pc;
@@ -493,7 +495,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         bf16_t* kq = reinterpret_cast<bf16_t*>(p.wsKQ) + slot * 4 * CH * DK;   // [K hi | K lo | Q hi | Q lo]
 #pragma unroll
         for (int j = 0; j < NPC; ++j) {
-            const int i = tid + NT * j, r = i / NPR, pc = i % NPR;
+            const int i = tid + NT_T32 * j, r = i / NPR, pc = i % NPR;
             const int at = 8 * (r * NPR + (pc ^ f32_kq_swz<DK>(r)));
             const floatx4 k0 = __builtin_bit_cast(floatx4, kv[j][0]), k1 = __builtin_bit_cast(floatx4, kv[j][1]);
             const floatx4 q0 = __builtin_bit_cast(floatx4, qv[j][0]), q1 = __builtin_bit_cast(floatx4, qv[j][1]);
@@ -533,8 +535,8 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         }
     }
 
-    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P): job = wave + 4 u, each
-    // as split bf16 products
+    // 10 lower 16x16 blocks of K K^T (-> A) and of Q K^T (-> P): job = wave + 8 u < 20,
+    // each as split bf16 products
     auto job_block = [](int job, int& which, int& bi, int& bj) {
         which = job / 10;
         int t = job % 10;
@@ -542,11 +544,13 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         while (t > bi) { t -= bi + 1; ++bi; }
         bj = t;
     };
-    floatx4 accs[5];
+    constexpr int NJ = 3;   // jobs per wave, at most
+    floatx4 accs[NJ];
 #pragma unroll
-    for (int u = 0; u < 5; ++u) {
+    for (int u = 0; u < NJ; ++u) {
+        if (wave + 8 * u >= 20) break;
         int which, bi, bj;
-        job_block(wave + 4 * u, which, bi, bj);
+        job_block(wave + 8 * u, which, bi, bj);
         const bf16_t(*Xh)[KP] = which ? sQh : sKh;
         const bf16_t(*Xl)[KP] = which ? sQl : sKl;
         const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
@@ -561,9 +565,10 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     }
     __syncthreads();   // every tile read done: A and P overwrite them
 #pragma unroll
-    for (int u = 0; u < 5; ++u) {
+    for (int u = 0; u < NJ; ++u) {
+        if (wave + 8 * u >= 20) break;
         int which, bi, bj;
-        job_block(wave + 4 * u, which, bi, bj);
+        job_block(wave + 8 * u, which, bi, bj);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int r = bi * 16 + 4 * lg + e, i = bj * 16 + l16;
@@ -578,9 +583,9 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
     __syncthreads();
 
     // T = (I + A)^{-1}, blocked by 16: the four diagonal blocks are inverted by
-    // forward substitution (wave b, lane = column), then block row b follows from
+    // forward substitution (wave b < 4, lane = column), then block row b follows from
     // T_bj = -T_bb * sum_{j <= m < b} A_bm T_mj with fp32 MFMA products.
-    {
+    if (wave < 4) {
         const int b = wave;
         float x[16];
 #pragma unroll
@@ -620,7 +625,7 @@ __global__ __launch_bounds__(NT) void k_chunk_terms(Params p) {
         __syncthreads();
     }
     // T and P for the chain: high and low bf16 parts in its LDS order (f32_tp_at), zero above the diagonal blocks
-    for (int i = tid; i < CH * CH / 8; i += NT) {
+    for (int i = tid; i < CH * CH / 8; i += NT_T32) {
         const int r = i / (CH / 8), col = 8 * ((i % (CH / 8)) ^ (r & 7));
         const bool up = (col >> 4) > (r >> 4);
         const floatx4 z = {0.f, 0.f, 0.f, 0.f};
@@ -2663,7 +2668,7 @@ void launch_prefill(Params p, long slots, hipStream_t st) {
         if constexpr (sizeof(IO) == 2)
             hipLaunchKernelGGL((k_chunk_terms_bf16<DK, NORM>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
         else
-            hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+            hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT_T32), 0, st, p);
     }
     const dim3 grid((unsigned)(p.n_seq * p.H * (p.DV / SL)));
     if constexpr (sizeof(IO) == 2)
@@ -2839,7 +2844,7 @@ void launch_segmented(Params p, const SegParams& sq, long slots, hipStream_t st)
     if constexpr (sizeof(IO) == 2)
         hipLaunchKernelGGL((k_chunk_terms_bf16<DK, NORM>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
     else
-        hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT), 0, st, p);
+        hipLaunchKernelGGL((k_chunk_terms<DK>), dim3((unsigned)(slots * p.H)), dim3(NT_T32), 0, st, p);
     ChainAlt a;
     a.v = nullptr; a.S0 = sq.Iseg; a.st_t = sizeof(IO) == 2 ? 2 : 1; a.o = const_cast<void*>(sq.Y); a.ST = const_cast<float*>(sq.M); a.DV = DK;
     a.first = (int)(nseg * p.H * (p.DV / SL));
