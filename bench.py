@@ -240,8 +240,8 @@ def main():
                     help="run one plain device copy of MIB MiB before timing (scale for rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
-              "(the multi-GPU sharding is a design note only)" % args.gpus, file=sys.stderr)
+        print("bench.py: the benchmark runs on exactly one GPU; --gpus %d is not supported "
+              "(sharding across GPUs is described, not implemented)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     if args.workload in ATTN:
