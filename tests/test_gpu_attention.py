@@ -113,7 +113,7 @@ def _wgs_for_two_tiles():
     return 4 * torch.cuda.get_device_properties(0).multi_processor_count
 
 
-@pytest.mark.parametrize("T", [65, 300])
+@pytest.mark.parametrize("T", [1, 17, 65, 300])
 def test_attention_two_query_tiles_per_wave(T):
     """A grid of at least four workgroups per CU at d = 128 (the form with two 16-query tiles per
     wave), with one-block and ragged tails."""
